@@ -1,0 +1,143 @@
+/*
+ * linsimp.h -- C ABI of the LinSimp (Linearized 2-Simplicial Attention) core
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The operation (paper: "Linearized 2-Simplicial Attention", Sec. 3.2-3.3;
+ * App. A; App. C), for every batch b, head h and 0-based row i = 0..n-1:
+ *
+ *   phi(x) = m^{-1/2} exp(Omega_h x - |x|^2/2 * 1)          Sec. 3.2, eq:prf
+ *   z_ic   = q_i (*) r_c                                     Sec. 3.2 (composite query)
+ *   M_i    = sum_{j<=i} phi(k_j) v_j^T,  a_i = sum_{j<=i} phi(k_j)   eq:Mstate, eq:astate
+ *   C_i    = {max(0, i-w+1), ..., i}                          Sec. 3.3
+ *   N_i    = sum_{c in C_i} [phi(z_ic)^T M_i] (*) u_c          eq:Ni
+ *   Z_i    = sum_{c in C_i} phi(z_ic)^T a_i                    eq:Zi
+ *   out_i  = N_i / (Z_i + eps)                                 eq:linearized-output
+ *
+ * q, k, r are used exactly as passed: the caller applies the L2 normalisation
+ * and the temperature of Sec. 3.1 (q = tau*q_hat, k = k_hat, r = r_hat) and
+ * the gated RMSNorm of eq:gated-output outside this library.  Omega is one
+ * [m, D] feature bank per head (App. B.1), float32, not differentiated.
+ *
+ * Numerics: all exponentials are evaluated in log space with a per-row query
+ * shift (App. B.2) and a causal running maximum of the key log features; the
+ * shifts cancel in the ratio, and eps is added to Z after both shifts (so eps
+ * only matters where the shifted Z underflows).  bf16 inputs are used as
+ * matrix-core operands with float32 accumulation and float32 prefix states.
+ *
+ * Conventions for every entry point:
+ *   - Tensor pointers are DEVICE pointers owned by the caller, 16-byte aligned,
+ *     dense, row-major, in the layouts stated per argument.  The library never
+ *     allocates device memory; scratch comes from the caller's workspace
+ *     (256-byte aligned, size from linsimp_workspace_size).
+ *   - `stream` is a hipStream_t (may be NULL for the default stream).  Calls
+ *     only enqueue work on it; nothing synchronises the device.
+ *   - Return value: LINSIMP_OK or a negative linsimp_status; the library never
+ *     aborts or throws across the ABI.  linsimp_last_error() gives a message
+ *     for the last failure on the calling thread.
+ *   - Supported shapes: dtype bf16 with (D = Dv, m) in {(32,32), (64,64),
+ *     (64,128), (128,64), (128,128), (128,256)}; dtype f32 with D = Dv in
+ *     {32, 64} and m in {32, 64}; 1 <= w <= 64; any n >= 1 (tails are masked).
+ *     Other shapes return LINSIMP_E_UNSUPPORTED: there is no fallback path.
+ */
+#ifndef LINSIMP_H
+#define LINSIMP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LINSIMP_OK = 0,
+  LINSIMP_E_INVALID_ARG = -1,   /* null / misaligned pointer, bad size          */
+  LINSIMP_E_UNSUPPORTED = -2,   /* valid but unsupported shape or dtype         */
+  LINSIMP_E_WORKSPACE = -3,     /* workspace missing, misaligned or too small   */
+  LINSIMP_E_HIP = -4            /* a HIP runtime call or kernel launch failed   */
+} linsimp_status;
+
+typedef enum { LINSIMP_F32 = 0, LINSIMP_BF16 = 1 } linsimp_dtype;
+
+typedef struct {
+  int64_t B;       /* batch                                   */
+  int64_t H;       /* heads                                   */
+  int64_t n;       /* sequence length (rows)                  */
+  int32_t D;       /* width of q, k, r                        */
+  int32_t Dv;      /* width of v, u, out                      */
+  int32_t m;       /* feature rank (rows of Omega)            */
+  int32_t w;       /* anchor window width                     */
+  int32_t dtype;   /* linsimp_dtype of q, k, v, r, u, out, grads */
+  float eps;       /* denominator guard, 1e-30 in the paper   */
+} linsimp_dims;
+
+/* Bytes of workspace linsimp_fwd (for_backward = 0), linsimp_bwd
+ * (for_backward = 1) or linsimp_prefill (for_backward = 0) needs for `dims`.
+ * Returns 0 for invalid or unsupported dims. */
+size_t linsimp_workspace_size(const linsimp_dims* dims, int for_backward);
+
+/* Forward pass (Sec. 3.3 eq:Ni, eq:Zi, eq:linearized-output; App. C Alg. 1).
+ *   q, k, r : [B, H, n, D]  dtype        v, u : [B, H, n, Dv] dtype
+ *   omega   : [H, m, D] float32 (the feature bank Omega of each head)
+ *   out     : [B, H, n, Dv] dtype, written (the pre-RMSNorm output o~)
+ *   stats   : [B, H, n, 2] float32 or NULL; per row (L_i, Zhat_i): the query
+ *             log2 shift and the doubly shifted denominator.  linsimp_bwd
+ *             needs it (the paper saves one stabiliser per row, Sec. 4.2).
+ * Workspace is scratch; its contents after the call are unspecified. */
+int linsimp_fwd(const linsimp_dims* dims, const void* q, const void* k, const void* v,
+                const void* r, const void* u, const float* omega, void* out, float* stats,
+                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward pass: exact gradient of sum_i dout_i . out_i with respect to q, k,
+ * v, r, u, with the stabilising shifts treated as constants (they cancel in
+ * the ratio, App. B.2); App. C "Backward query sweep" / "Backward state sweep".
+ *   q, k, v, r, u, omega : as in linsimp_fwd (same values)
+ *   out, stats           : what linsimp_fwd returned for these inputs
+ *   dout                 : [B, H, n, Dv] dtype, upstream gradient
+ *   dq, dk, dr : [B, H, n, D] dtype; dv, du : [B, H, n, Dv] dtype; overwritten.
+ * No gradient is produced for omega (a fixed buffer, App. B.1). */
+int linsimp_bwd(const linsimp_dims* dims, const void* q, const void* k, const void* v,
+                const void* r, const void* u, const float* omega, const void* out,
+                const float* stats, const void* dout, void* dq, void* dk, void* dv, void* dr,
+                void* du, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Prefill: build the decode state of Theorem 1 from a prefix of n tokens
+ * (dims->n) per sequence; dims->B is the number of sequences S.
+ *   k, r : [S, H, n, D] dtype;  v, u : [S, H, n, Dv] dtype; omega [H, m, D] f32
+ *   M    : [S, H, m, Dv] float32 out;  a : [S, H, m] float32 out
+ *   rho  : [S, H] float32 out.  The prefix state of eq:Mstate / eq:astate is
+ *          M_true = 2^rho * M and a_true = 2^rho * a (rho is a log2 frame that
+ *          keeps M finite whatever the key scale).
+ *   ring_r : [S, H, w, D], ring_u : [S, H, w, Dv] dtype out: token j of the
+ *          last min(n, w) tokens sits in slot j mod w; other slots are zeroed.
+ *   pos  : [S] int64 out, set to n. */
+int linsimp_prefill(const linsimp_dims* dims, const void* k, const void* v, const void* r,
+                    const void* u, const float* omega, float* M, float* a, float* rho,
+                    void* ring_r, void* ring_u, int64_t* pos, void* workspace,
+                    size_t workspace_bytes, void* stream);
+
+/* One autoregressive decode step (Theorem 1) for S independent sequences:
+ * token t = pos[s] of sequence s updates M and a (eq:Mstate, eq:astate),
+ * writes (r_t, u_t) into ring slot t mod w, and reads q_t out over the
+ * min(t+1, w) most recent anchors, the new token included.
+ *   q, k, r : [S, H, D] dtype;  v, u : [S, H, Dv] dtype;  omega [H, m, D] f32
+ *   M, a, rho, ring_r, ring_u, pos : in/out, layouts as in linsimp_prefill
+ *   out : [S, H, Dv] dtype
+ * Uses no workspace.  Same shape support as the forward; S >= 1. */
+int linsimp_decode_step(int64_t S, int32_t H, int32_t D, int32_t Dv, int32_t m, int32_t w,
+                        int32_t dtype, float eps, const void* q, const void* k, const void* v,
+                        const void* r, const void* u, const float* omega, float* M, float* a,
+                        float* rho, void* ring_r, void* ring_u, int64_t* pos, void* out,
+                        void* stream);
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char* linsimp_last_error(void);
+
+/* ABI version (major * 100 + minor). */
+int linsimp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LINSIMP_H */

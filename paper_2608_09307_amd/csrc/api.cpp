@@ -1,0 +1,212 @@
+// C ABI of the LinSimp library: argument validation, workspace carving and
+// dispatch to the HIP kernels.  Declarations and contracts: include/linsimp.h.
+#include "../../include/linsimp.h"
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "linsimp_internal.h"
+
+namespace linsimp {
+
+static thread_local char g_err[512] = "";
+
+void set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+}
+
+static size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t workspace_bytes(const Shape& s, bool backward) {
+  const size_t H = (size_t)s.H, BH = (size_t)s.BH(), nch = (size_t)s.nch();
+  const size_t md = (size_t)s.m * s.D, S = (size_t)s.state_elems();
+  size_t t = 0;
+  t += al(H * md * s.esize());                 // omq
+  t += al(H * md * 4);                         // omk (bf16 hi+lo, or f32)
+  t += al(BH * nch * S * 4);                   // states
+  t += al(BH * nch * 4);                       // rho
+  t += al(BH * (nch + 1) * 4);                 // rex
+  if (s.m > 128) t += al((size_t)(s.m / 128) * BH * s.n * (s.Dv + 2) * 4);   // part
+  if (backward) {
+    const size_t n = (size_t)s.n, win = kChunk + 64 - 1;
+    t += al(BH * nch * S * 4);                 // gstates
+    t += al(BH * n * s.m * 4);                 // dchi
+    t += al(BH * n * s.Dv * 4);                // dvin
+    t += al(BH * nch * win * s.Dv * 4);        // du32
+    t += al(BH * nch * win * s.D * 4);         // dr32
+    t += al(BH * n * 4 * 4);                   // rowstat
+  }
+  return t;
+}
+
+void carve(const Shape& s, void* base, bool backward, Workspace* ws) {
+  const size_t H = (size_t)s.H, BH = (size_t)s.BH(), nch = (size_t)s.nch();
+  const size_t md = (size_t)s.m * s.D, S = (size_t)s.state_elems();
+  char* p = (char*)base;
+  memset(ws, 0, sizeof(*ws));
+  ws->omq = p; p += al(H * md * s.esize());
+  ws->omk = p; p += al(H * md * 4);
+  ws->states = (float*)p; p += al(BH * nch * S * 4);
+  ws->rho = (float*)p; p += al(BH * nch * 4);
+  ws->rex = (float*)p; p += al(BH * (nch + 1) * 4);
+  if (s.m > 128) { ws->part = (float*)p; p += al((size_t)(s.m / 128) * BH * s.n * (s.Dv + 2) * 4); }
+  if (backward) {
+    const size_t n = (size_t)s.n, win = kChunk + 64 - 1;
+    ws->gstates = (float*)p; p += al(BH * nch * S * 4);
+    ws->dchi = (float*)p; p += al(BH * n * s.m * 4);
+    ws->dvin = (float*)p; p += al(BH * n * s.Dv * 4);
+    ws->du32 = (float*)p; p += al(BH * nch * win * s.Dv * 4);
+    ws->dr32 = (float*)p; p += al(BH * nch * win * s.D * 4);
+    ws->rowstat = (float*)p; p += al(BH * n * 4 * 4);
+  }
+}
+
+bool shape_supported(const Shape& s, bool /*backward*/) {
+  if (s.w < 1 || s.w > 64) return false;
+  return fwd_combo_supported(s.dtype, s.D, s.Dv, s.m);
+}
+
+}  // namespace linsimp
+
+using namespace linsimp;
+
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+// Validates dims; fills `s`.  Returns LINSIMP_OK or an error status.
+static int check_dims(const linsimp_dims* d, Shape* s, bool backward) {
+  if (d == nullptr) { set_error("dims is NULL"); return LINSIMP_E_INVALID_ARG; }
+  if (d->B < 1 || d->H < 1 || d->n < 1 || d->D < 1 || d->Dv < 1 || d->m < 1 || d->w < 1) {
+    set_error("dims must be positive (B=%lld H=%lld n=%lld D=%d Dv=%d m=%d w=%d)",
+              (long long)d->B, (long long)d->H, (long long)d->n, d->D, d->Dv, d->m, d->w);
+    return LINSIMP_E_INVALID_ARG;
+  }
+  if (d->dtype != LINSIMP_F32 && d->dtype != LINSIMP_BF16) {
+    set_error("dtype %d is not LINSIMP_F32 or LINSIMP_BF16", d->dtype);
+    return LINSIMP_E_INVALID_ARG;
+  }
+  if (!(d->eps >= 0.0f)) { set_error("eps must be >= 0"); return LINSIMP_E_INVALID_ARG; }
+  if (d->n > (int64_t)1 << 30 || d->B * d->H > (int64_t)1 << 30) {
+    set_error("sequence or batch too large");
+    return LINSIMP_E_UNSUPPORTED;
+  }
+  s->B = d->B; s->H = d->H; s->n = d->n; s->D = d->D; s->Dv = d->Dv; s->m = d->m; s->w = d->w;
+  s->dtype = d->dtype; s->eps = d->eps;
+  if (!shape_supported(*s, backward)) {
+    set_error("unsupported shape: dtype=%d D=%d Dv=%d m=%d w=%d", d->dtype, d->D, d->Dv, d->m, d->w);
+    return LINSIMP_E_UNSUPPORTED;
+  }
+  return LINSIMP_OK;
+}
+
+static int check_ptrs(const char* names, const void* const* ps, int np) {
+  for (int i = 0; i < np; ++i) {
+    if (ps[i] == nullptr) {
+      set_error("argument %d of (%s) is NULL", i, names);
+      return LINSIMP_E_INVALID_ARG;
+    }
+    if (!aligned16(ps[i])) {
+      set_error("argument %d of (%s) is not 16-byte aligned", i, names);
+      return LINSIMP_E_INVALID_ARG;
+    }
+  }
+  return LINSIMP_OK;
+}
+
+static int check_ws(const Shape& s, bool backward, const void* ws, size_t bytes) {
+  size_t need = workspace_bytes(s, backward);
+  if (ws == nullptr || ((uintptr_t)ws & 255) != 0) {
+    set_error("workspace must be a non-NULL 256-byte aligned device pointer");
+    return LINSIMP_E_WORKSPACE;
+  }
+  if (bytes < need) {
+    set_error("workspace too small: %zu bytes given, %zu needed", bytes, need);
+    return LINSIMP_E_WORKSPACE;
+  }
+  return LINSIMP_OK;
+}
+
+extern "C" {
+
+size_t linsimp_workspace_size(const linsimp_dims* dims, int for_backward) {
+  Shape s;
+  if (check_dims(dims, &s, for_backward != 0) != LINSIMP_OK) return 0;
+  return workspace_bytes(s, for_backward != 0);
+}
+
+int linsimp_fwd(const linsimp_dims* dims, const void* q, const void* k, const void* v,
+                const void* r, const void* u, const float* omega, void* out, float* stats,
+                void* workspace, size_t workspace_bytes_, void* stream) {
+  Shape s;
+  int rc = check_dims(dims, &s, false);
+  if (rc) return rc;
+  const void* ps[] = {q, k, v, r, u, omega, out};
+  if ((rc = check_ptrs("q,k,v,r,u,omega,out", ps, 7))) return rc;
+  if (stats != nullptr && !aligned16(stats)) {
+    set_error("stats is not 16-byte aligned");
+    return LINSIMP_E_INVALID_ARG;
+  }
+  if ((rc = check_ws(s, false, workspace, workspace_bytes_))) return rc;
+  Workspace ws;
+  carve(s, workspace, false, &ws);
+  return launch_forward(s, q, k, v, r, u, omega, out, stats, nullptr, nullptr, nullptr, ws,
+                        (hipStream_t)stream);
+}
+
+int linsimp_bwd(const linsimp_dims* dims, const void* q, const void* k, const void* v,
+                const void* r, const void* u, const float* omega, const void* out,
+                const float* stats, const void* dout, void* dq, void* dk, void* dv, void* dr,
+                void* du, void* workspace, size_t workspace_bytes_, void* stream) {
+  Shape s;
+  int rc = check_dims(dims, &s, true);
+  if (rc) return rc;
+  const void* ps[] = {q, k, v, r, u, omega, out, stats, dout, dq, dk, dv, dr, du};
+  if ((rc = check_ptrs("q,k,v,r,u,omega,out,stats,dout,dq,dk,dv,dr,du", ps, 14))) return rc;
+  if ((rc = check_ws(s, true, workspace, workspace_bytes_))) return rc;
+  Workspace ws;
+  carve(s, workspace, true, &ws);
+  return launch_backward(s, q, k, v, r, u, omega, out, stats, dout, dq, dk, dv, dr, du, ws,
+                         (hipStream_t)stream);
+}
+
+int linsimp_prefill(const linsimp_dims* dims, const void* k, const void* v, const void* r,
+                    const void* u, const float* omega, float* M, float* a, float* rho,
+                    void* ring_r, void* ring_u, int64_t* pos, void* workspace,
+                    size_t workspace_bytes_, void* stream) {
+  Shape s;
+  int rc = check_dims(dims, &s, false);
+  if (rc) return rc;
+  const void* ps[] = {k, v, r, u, omega, M, a, rho, ring_r, ring_u, pos};
+  if ((rc = check_ptrs("k,v,r,u,omega,M,a,rho,ring_r,ring_u,pos", ps, 11))) return rc;
+  if ((rc = check_ws(s, false, workspace, workspace_bytes_))) return rc;
+  Workspace ws;
+  carve(s, workspace, false, &ws);
+  rc = launch_forward(s, k, k, v, r, u, omega, nullptr, nullptr, M, a, rho, ws, (hipStream_t)stream);
+  if (rc) return rc;
+  return launch_ring_fill(s, r, u, ring_r, ring_u, pos, (hipStream_t)stream);
+}
+
+int linsimp_decode_step(int64_t S, int32_t H, int32_t D, int32_t Dv, int32_t m, int32_t w,
+                        int32_t dtype, float eps, const void* q, const void* k, const void* v,
+                        const void* r, const void* u, const float* omega, float* M, float* a,
+                        float* rho, void* ring_r, void* ring_u, int64_t* pos, void* out,
+                        void* stream) {
+  linsimp_dims d;
+  d.B = S; d.H = H; d.n = 1; d.D = D; d.Dv = Dv; d.m = m; d.w = w; d.dtype = dtype; d.eps = eps;
+  Shape s;
+  int rc = check_dims(&d, &s, false);
+  if (rc) return rc;
+  const void* ps[] = {q, k, v, r, u, omega, M, a, rho, ring_r, ring_u, pos, out};
+  if ((rc = check_ptrs("q,k,v,r,u,omega,M,a,rho,ring_r,ring_u,pos,out", ps, 13))) return rc;
+  return launch_decode(S, H, D, Dv, m, w, dtype, eps, q, k, v, r, u, omega, M, a, rho, ring_r,
+                       ring_u, pos, out, (hipStream_t)stream);
+}
+
+const char* linsimp_last_error(void) { return g_err; }
+
+int linsimp_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,151 @@
+// Shared device helpers for the LinSimp HIP kernels (gfx950 / CDNA4).
+//
+// Matrix-core conventions used everywhere (wave64, 32x32 MFMA tiles):
+//   lane l: col = l & 31, half h = l >> 5.
+//   Operand fragment of k-step s (A or B): lane holds KPL consecutive k values
+//     k = s*KS + h*KPL + e,  e = 0..KPL-1          ("natural" order)
+//     bf16: v_mfma_f32_32x32x16_bf16, KS = 16, KPL = 8
+//     f32 : v_mfma_f32_32x32x2_f32,   KS = 2,  KPL = 1
+//   Accumulator (C/D) register v = 0..15 of a 32x32 tile holds
+//     row = 8*(v>>2) + 4*h + (v&3),  col = l & 31.
+//   A tile whose rows are a contraction index can be fed straight back to the
+//   next MFMA as an operand (its columns become that operand's M or N index):
+//   k-step s' of the 32-row tile uses registers 8s'..8s'+7 (bf16) or s' (f32),
+//   i.e. tile rows crow(s', h, e).  The other operand of such an MFMA is read
+//   from LDS with the same permutation: for bf16 it is stored permuted
+//   (sigma swaps the 4-groups 1 and 2 of each 16-block) so that those rows
+//   are one contiguous 16-byte read; for f32 it is indexed directly.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16;
+typedef bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+#define LS_DEV __device__ __forceinline__
+
+static constexpr float kLog2e = 1.4426950408889634f;
+static constexpr float kNegInf = -__builtin_inff();
+
+LS_DEV int lane_id() { return threadIdx.x & 63; }
+
+template <typename T> struct MF;
+
+template <> struct MF<bf16> {
+  static constexpr int KS = 16;      // k per instruction
+  static constexpr int KPL = 8;      // k per lane
+  static constexpr int PAD = 8;      // LDS row padding (elements) = 16 bytes
+  typedef bf16x8 frag;
+  LS_DEV static f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  LS_DEV static frag zero() { frag z; for (int e = 0; e < 8; ++e) z[e] = (bf16)0.0f; return z; }
+  // natural fragment at row + k0 (k0 = s*KS + h*KPL)
+  LS_DEV static frag ld(const bf16* row, int k0) { return *(const frag*)(row + k0); }
+  // fragment of tile rows crow(s', h, *) from a permuted-storage row
+  LS_DEV static frag ldc(const bf16* row, int base, int sp, int h) {
+    return *(const frag*)(row + base + 16 * sp + 8 * h);
+  }
+  // C-derived fragment: registers 8s'..8s'+7 of an accumulator, scaled
+  LS_DEV static frag cfrag(const f32x16& acc, int sp) {
+    frag f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) f[e] = (bf16)acc[8 * sp + e];
+    return f;
+  }
+  static constexpr int CSTEPS = 2;   // k-steps per 32-row C tile
+  // storage position of contraction index k for permuted operands
+  LS_DEV static int sigma(int k) {
+    int g = (k >> 2) & 3;
+    int gs = (g == 1) ? 2 : (g == 2) ? 1 : g;
+    return (k & ~15) | (gs << 2) | (k & 3);
+  }
+};
+
+template <> struct MF<float> {
+  static constexpr int KS = 2;
+  static constexpr int KPL = 1;
+  static constexpr int PAD = 1;
+  typedef float frag;
+  LS_DEV static f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  LS_DEV static frag zero() { return 0.0f; }
+  LS_DEV static frag ld(const float* row, int k0) { return row[k0]; }
+  LS_DEV static frag ldc(const float* row, int base, int sp, int h) {
+    return row[base + 8 * (sp >> 2) + 4 * h + (sp & 3)];
+  }
+  LS_DEV static frag cfrag(const f32x16& acc, int sp) { return acc[sp]; }
+  static constexpr int CSTEPS = 16;
+  LS_DEV static int sigma(int k) { return k; }
+};
+
+// row index of accumulator register v in a 32x32 tile
+LS_DEV int crow(int v, int h) { return 8 * (v >> 2) + 4 * h + (v & 3); }
+
+LS_DEV f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.0f;
+  return z;
+}
+
+template <typename T> LS_DEV float tof(T x) { return (float)x; }
+template <typename T> LS_DEV T fromf(float x) { return (T)x; }
+
+// fragment element access as float
+LS_DEV float fel(const bf16x8& f, int e) { return (float)f[e]; }
+LS_DEV float fel(const float& f, int) { return f; }
+
+LS_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// value known to be equal in every lane -> scalar register (uniform branches)
+LS_DEV float uniform(float x) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
+}
+LS_DEV int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// compiler-only barrier: memory reads after it cannot be hoisted above it
+LS_DEV void no_hoist() { asm volatile("" ::: "memory"); }
+
+// ---- wave reductions (64 lanes) ----
+LS_DEV float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+LS_DEV float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+LS_DEV float half_swap_add(float x) { return x + __shfl_xor(x, 32, 64); }
+LS_DEV float half_swap_max(float x) { return fmaxf(x, __shfl_xor(x, 32, 64)); }
+
+// ---- cooperative global -> LDS copies (block-wide) ----
+// 2D copy of a [rows][cols] T matrix (global row stride gstride) into LDS with
+// row stride lstride; rows >= valid_rows (or < 0 via row offset) become zero.
+template <typename T>
+LS_DEV void copy_rows(T* lds, int lstride, const T* g, int gstride, int rows, int cols,
+                      int row0, int valid_lo, int valid_hi, int tid, int nthreads) {
+  // row r of the LDS tile is global row row0 + r; valid if in [valid_lo, valid_hi)
+  const int vec = (sizeof(T) == 2) ? 8 : 4;   // 16-byte chunks
+  const int cpr = cols / vec;
+  for (int idx = tid; idx < rows * cpr; idx += nthreads) {
+    int rr = idx / cpr, cc = (idx % cpr) * vec;
+    int grow = row0 + rr;
+    T* dst = lds + rr * lstride + cc;
+    if (grow >= valid_lo && grow < valid_hi) {
+      const T* src = g + (size_t)grow * gstride + cc;
+#pragma unroll
+      for (int e = 0; e < vec; ++e) dst[e] = src[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < vec; ++e) dst[e] = (T)0.0f;
+    }
+  }
+}

@@ -1,0 +1,648 @@
+// LinSimp forward on gfx950: feature-bank preparation, chunk prefix states,
+// the chunk scan with a causal log-space frame, and the anchor-window readout.
+//
+// Method (per head, 0-based rows; the paper counts from 1):
+//   phi(x) = m^{-1/2} exp(Omega x - |x|^2/2)                  [Sec. 3.2, eq:prf]
+//   M_i = sum_{j<=i} phi(k_j) v_j^T, a_i = sum_{j<=i} phi(k_j) [eq:Mstate, eq:astate]
+//   z_ic = q_i (*) r_c,  C_i = {max(0,i-w+1) .. i}              [Sec. 3.2, 3.3]
+//   N_i = sum_c [phi(z_ic)^T M_i] (*) u_c,  Z_i = sum_c phi(z_ic)^T a_i,
+//   out_i = N_i / (Z_i + eps)                                   [eq:Ni, eq:Zi, eq:linearized-output]
+//
+// Everything is evaluated in log2 space.  Query side (App. B.2): one shift
+// L_i = max over valid (c, p) of the log features, kept online across anchor
+// tiles and feature blocks.  Key side: a causal running maximum R_j of the key
+// log features; key features are exp2(lambda_j - R_j)/sqrt(m) and every state
+// carries its frame, so neither side can overflow and a row never sees a
+// future token's scale.  The 1/sqrt(m) of the query feature is dropped (it
+// cancels in the ratio, App. A "Feature scaling").
+#include "common.h"
+#include "linsimp_internal.h"
+
+namespace linsimp {
+
+struct FwdArgs {
+  const void* q; const void* k; const void* v; const void* r; const void* u;
+  const float* omega;
+  void* out; float* stats;
+  void* omq; void* omk;
+  float* states; float* rho; float* rex;
+  float* final_M; float* final_a; float* final_rex;   // optional state after the last token
+  float* part;                                        // [NFB][BH][n][Dv+2] when m > 128
+  int H; int n; int w; int nch; int BH; float eps;
+};
+
+// ---------------------------------------------------------------------------
+// K0: Omega * log2(e) in the operand type; key side keeps a hi/lo bf16 split so
+// that key log features are accurate to ~2^-16 relative (bf16 keys are exact).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_prep_omega(const float* __restrict__ omega, T* __restrict__ omq,
+                                                    T* __restrict__ omk, int H, int MD) {
+  int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= H * MD) return;
+  float x = omega[idx] * kLog2e;
+  omq[idx] = (T)x;
+  if constexpr (sizeof(T) == 2) {
+    int hh = idx / MD, e = idx % MD;
+    bf16 hi = (bf16)x;
+    omk[(size_t)hh * 2 * MD + e] = hi;
+    omk[(size_t)hh * 2 * MD + MD + e] = (bf16)(x - (float)hi);
+  } else {
+    omk[idx] = (T)x;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Key log2-features of 32 tokens [tok0, tok0+32) against all M feature rows.
+// TOKEN_COLS: lanes <-> token, registers <-> feature p (acc[pt] rows p = 32pt+crow).
+// else      : lanes <-> feature p, registers <-> token.
+// The |k|^2/2 term is not applied; nk returns |k_tok|^2 for the lane's token.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int M, bool TOKEN_COLS>
+LS_DEV void key_logits(f32x16 (&acc)[M / 32], float& nk, const T* __restrict__ kseq, int tok0, int n,
+                       const T* __restrict__ omk_h) {
+  using F = MF<T>;
+  const int l = lane_id(), col = l & 31, h = l >> 5;
+  const int j = tok0 + col;
+  const bool vj = j < n;
+#pragma unroll
+  for (int pt = 0; pt < M / 32; ++pt) acc[pt] = zero16();
+  nk = 0.0f;
+#pragma unroll 1
+  for (int s = 0; s < D / F::KS; ++s) {
+    const int k0 = s * F::KS + h * F::KPL;
+    typename F::frag kf = vj ? F::ld(kseq + (size_t)j * D, k0) : F::zero();
+#pragma unroll
+    for (int e = 0; e < F::KPL; ++e) { float x = fel(kf, e); nk += x * x; }
+#pragma unroll
+    for (int pt = 0; pt < M / 32; ++pt) {
+      typename F::frag of = F::ld(omk_h + (size_t)(pt * 32 + col) * D, k0);
+      acc[pt] = TOKEN_COLS ? F::mma(of, kf, acc[pt]) : F::mma(kf, of, acc[pt]);
+      if constexpr (sizeof(T) == 2) {
+        typename F::frag ol = F::ld(omk_h + (size_t)M * D + (size_t)(pt * 32 + col) * D, k0);
+        acc[pt] = TOKEN_COLS ? F::mma(ol, kf, acc[pt]) : F::mma(kf, ol, acc[pt]);
+      }
+    }
+  }
+  nk = half_swap_add(nk);
+}
+
+// ---------------------------------------------------------------------------
+// K2: per 32-token chunk b, its contribution to the prefix state in the frame
+// rho_b = max key log2-feature of the chunk:
+//   Mt_b = sum_j chi_j v_j^T, at_b = sum_j chi_j, chi_j = exp2(lambda_j - rho_b)/sqrt(m)
+// One wave per chunk.  [App. C "Host preparation": per-chunk contributions]
+// ---------------------------------------------------------------------------
+template <typename T, int D, int DV, int M>
+__global__ __launch_bounds__(256) void k_chunk_state(FwdArgs a) {
+  using F = MF<T>;
+  constexpr int PAD = F::PAD;
+  constexpr int S = M * DV + M;
+  __shared__ __align__(16) T sVt[4][DV][32 + PAD];
+  __shared__ float snk[4][32];
+  const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
+  const int b = blockIdx.x * 4 + wv;
+  const int bh = blockIdx.y, hh = bh % a.H, n = a.n;
+  const bool active = b < a.nch;
+  const int tok0 = b * 32;
+  const T* ks = (const T*)a.k + (size_t)bh * n * D;
+  const T* vs = (const T*)a.v + (size_t)bh * n * DV;
+  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
+  f32x16 acc[M / 32];
+  float nk = 0.0f;
+  if (active) {
+    // V^T of the chunk, token index permuted (it pairs with a register operand)
+    for (int idx = l; idx < 32 * (DV / 4); idx += 64) {
+      int jj = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
+      bool ok = tok0 + jj < n;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        sVt[wv][d0 + e][F::sigma(jj)] = ok ? vs[(size_t)(tok0 + jj) * DV + d0 + e] : (T)0.0f;
+    }
+    key_logits<T, D, M, false>(acc, nk, ks, tok0, n, omk_h);
+    if (h == 0) snk[wv][col] = nk;
+  }
+  __syncthreads();
+  if (!active) return;
+  float mx = kNegInf;
+#pragma unroll
+  for (int pt = 0; pt < M / 32; ++pt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      int tk = crow(v, h);
+      float x = (tok0 + tk < n) ? acc[pt][v] - 0.5f * kLog2e * snk[wv][tk] : kNegInf;
+      acc[pt][v] = x;
+      mx = fmaxf(mx, x);
+    }
+  const float rb = wave_max(mx);
+  const float rs = rsqrtf((float)M);
+  float* st = a.states + ((size_t)bh * a.nch + b) * S;
+#pragma unroll
+  for (int pt = 0; pt < M / 32; ++pt) {
+    float asum = 0.0f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      float c = fast_exp2(acc[pt][v] - rb) * rs;
+      acc[pt][v] = c;
+      asum += c;
+    }
+    asum = half_swap_add(asum);
+    if (h == 0) st[M * DV + pt * 32 + col] = asum;
+#pragma unroll
+    for (int dt = 0; dt < DV / 32; ++dt) {
+      f32x16 o = zero16();
+#pragma unroll
+      for (int sp = 0; sp < F::CSTEPS; ++sp)
+        o = F::mma(F::cfrag(acc[pt], sp), F::ldc(&sVt[wv][dt * 32 + col][0], 0, sp, h), o);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) st[(size_t)(pt * 32 + crow(v, h)) * DV + dt * 32 + col] = o[v];
+    }
+  }
+  if (l == 0) a.rho[(size_t)bh * a.nch + b] = rb;
+}
+
+// ---------------------------------------------------------------------------
+// K2b: exclusive scan over chunks with the log-scale monoid
+//   (M1, R1) + (M2, r2) = (e^{R1-R} M1 + e^{r2-R} M2, R = max(R1, r2))
+// in place: chunk b's contribution is replaced by the state of every token
+// before chunk b, in frame rex[b] (-inf for the empty state).  Element-parallel,
+// sequential over chunks, loads issued PF chunks ahead.
+// [App. C "Host preparation": exclusive cumulative sum -> boundary states]
+// ---------------------------------------------------------------------------
+template <int M, int DV>
+__global__ __launch_bounds__(256) void k_state_scan(FwdArgs a) {
+  constexpr int PF = 8;
+  constexpr int S = M * DV + M;
+  const int bh = blockIdx.y;
+  const int i4 = (blockIdx.x * 256 + threadIdx.x) * 4;
+  const bool act = i4 < S;
+  const int nch = a.nch;
+  float* st = a.states + (size_t)bh * nch * S;
+  const float* rh = a.rho + (size_t)bh * nch;
+  float* rx = a.rex + (size_t)bh * (nch + 1);
+  const bool writer = (blockIdx.x == 0 && threadIdx.x == 0);
+  f32x4 run = {0.f, 0.f, 0.f, 0.f};
+  float R = kNegInf;
+  for (int b0 = 0; b0 < nch; b0 += PF) {
+    f32x4 x[PF];
+#pragma unroll
+    for (int e = 0; e < PF; ++e) {
+      if (act && b0 + e < nch) x[e] = *(const f32x4*)(st + (size_t)(b0 + e) * S + i4);
+      else x[e] = run * 0.0f;
+    }
+#pragma unroll
+    for (int e = 0; e < PF; ++e) {
+      int b = b0 + e;
+      if (b >= nch) break;
+      float rb = rh[b];
+      float Rn = fmaxf(R, rb);
+      float sa = fast_exp2(R - Rn);      // 0 when R = -inf
+      float sb = fast_exp2(rb - Rn);
+      if (act) *(f32x4*)(st + (size_t)b * S + i4) = run;
+      if (writer) rx[b] = R;
+      run = run * sa + x[e] * sb;
+      R = Rn;
+    }
+  }
+  if (a.final_M != nullptr && act) {
+    if (i4 < M * DV) *(f32x4*)(a.final_M + (size_t)bh * M * DV + i4) = run;
+    else *(f32x4*)(a.final_a + (size_t)bh * M + (i4 - M * DV)) = run;
+  }
+  if (writer) {
+    rx[nch] = R;
+    if (a.final_rex != nullptr) a.final_rex[bh] = R;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// K3: anchor-window readout for one chunk of 32 rows.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int DV, int M, int NW, int NA>
+struct RCfg {
+  static constexpr int PAD = MF<T>::PAD;
+  static constexpr int BC = 32;
+  static constexpr int FB = M < 128 ? M : 128;          // feature block (<= 128 as in Alg. 1)
+  static constexpr int NFB = M / FB;
+  static constexpr int WIN = BC + 32 * NA - 1;           // anchor rows the chunk can touch
+  static constexpr int UST = WIN + 1;
+  static constexpr int RPW = BC / NW;
+  static constexpr int ES = sizeof(T);
+  static constexpr int a16(int x) { return (x + 15) & ~15; }
+  static constexpr int oOm = 0;
+  static constexpr int oMt = oOm + a16(FB * (D + PAD) * ES);
+  static constexpr int oA = oMt + a16(DV * (FB + PAD) * ES);
+  static constexpr int oChi = oA + a16(M * 4);
+  static constexpr int oVt = oChi + a16(BC * (M + PAD) * ES);
+  static constexpr int oR = oVt + a16(DV * (BC + PAD) * ES);
+  static constexpr int oUt = oR + a16(WIN * (D + PAD) * ES);
+  static constexpr int oQ = oUt + a16(DV * UST * ES);
+  static constexpr int oRj = oQ + a16(BC * (D + PAD) * ES);
+  static constexpr int BYTES = oRj + a16(BC * 4);
+};
+
+template <typename T, int D, int DV, int M, int NW, int NA>
+__global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
+  using F = MF<T>;
+  using C = RCfg<T, D, DV, M, NW, NA>;
+  constexpr int PAD = C::PAD, FB = C::FB, WIN = C::WIN, UST = C::UST, RPW = C::RPW;
+  static_assert(C::BYTES <= 160 * 1024, "readout LDS budget");
+  __shared__ __align__(16) char smem[C::BYTES];
+  T* sOm = (T*)(smem + C::oOm);
+  T* sMt = (T*)(smem + C::oMt);
+  float* sA = (float*)(smem + C::oA);
+  T* sChi = (T*)(smem + C::oChi);
+  T* sVt = (T*)(smem + C::oVt);
+  T* sR = (T*)(smem + C::oR);
+  T* sUt = (T*)(smem + C::oUt);
+  T* sQ = (T*)(smem + C::oQ);
+  float* sRj = (float*)(smem + C::oRj);
+
+  const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
+  constexpr int NT = 64 * NW;
+  const int cb = blockIdx.x, bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch;
+  const int s0 = cb * 32;
+  const int wb = s0 - (32 * NA - 1);
+  constexpr int S = M * DV + M;
+  const size_t seq = (size_t)bh * n;
+  const T* qs = (const T*)a.q + seq * D;
+  const T* ks = (const T*)a.k + seq * D;
+  const T* vs = (const T*)a.v + seq * DV;
+  const T* rs_ = (const T*)a.r + seq * D;
+  const T* us = (const T*)a.u + seq * DV;
+  const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
+  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
+  const float* bst = a.states + ((size_t)bh * nch + cb) * S;
+  const float Rexb = a.rex[(size_t)bh * (nch + 1) + cb];
+  const bool has_bnd = cb > 0;
+
+  // ---- prologue: key features of the chunk (wave 0) ----
+  if (wv == 0) {
+    f32x16 acc[M / 32];
+    float nk;
+    key_logits<T, D, M, true>(acc, nk, ks, s0, n, omk_h);
+    const bool vt = s0 + col < n;
+    float mx = kNegInf;
+#pragma unroll
+    for (int pt = 0; pt < M / 32; ++pt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float x = vt ? acc[pt][v] - 0.5f * kLog2e * nk : kNegInf;
+        acc[pt][v] = x;
+        mx = fmaxf(mx, x);
+      }
+    mx = half_swap_max(mx);                      // rho of token col
+    float R = mx;                                // causal running max within the chunk
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) {
+      float t = __shfl_up(R, o, 32);
+      if (col >= o) R = fmaxf(R, t);
+    }
+    R = fmaxf(R, Rexb);
+    if (h == 0) sRj[col] = R;
+    const float rsm = rsqrtf((float)M);
+    T* crow_p = sChi + col * (M + PAD);
+#pragma unroll
+    for (int pt = 0; pt < M / 32; ++pt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        int p = pt * 32 + crow(v, h);
+        crow_p[F::sigma(p)] = (T)(fast_exp2(acc[pt][v] - R) * rsm);
+      }
+  }
+  // ---- prologue: everything else (all waves) ----
+  const int fbk = blockIdx.z;
+  copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fbk * FB * D, D, FB, D, 0, 0, FB, tid, NT);
+  for (int idx = tid; idx < FB * (DV / 4); idx += NT) {
+    int p = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
+    f32x4 x = has_bnd ? *(const f32x4*)(bst + (size_t)(fbk * FB + p) * DV + d0)
+                      : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = (T)x[e];
+  }
+  for (int p = tid; p < M; p += NT) sA[p] = has_bnd ? bst[(size_t)M * DV + p] : 0.0f;
+  for (int idx = tid; idx < 32 * (DV / 4); idx += NT) {
+    int jj = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
+    bool ok = s0 + jj < n;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      sVt[(d0 + e) * (32 + PAD) + F::sigma(jj)] = ok ? vs[(size_t)(s0 + jj) * DV + d0 + e] : (T)0.0f;
+  }
+  copy_rows<T>(sR, D + PAD, rs_, D, WIN, D, wb, 0, n, tid, NT);
+  for (int idx = tid; idx < WIN * (DV / 4); idx += NT) {
+    int wi = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
+    int c = wb + wi;
+    bool ok = c >= 0 && c < n;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sUt[(d0 + e) * UST + wi] = ok ? us[(size_t)c * DV + d0 + e] : (T)0.0f;
+  }
+  copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
+  __syncthreads();
+
+  const int fb = blockIdx.z;       // feature block handled by this workgroup
+#pragma unroll 1
+  for (int rr = 0; rr < RPW; ++rr) {
+    const int t = wv + NW * rr;
+    const int i = s0 + t;
+    if (i >= n) continue;
+    float nacc[DV / 32];
+    float zacc = 0.0f, Lrun = kNegInf;
+#pragma unroll
+    for (int dt = 0; dt < DV / 32; ++dt) nacc[dt] = 0.0f;
+    const float Ri = uniform(sRj[t]);
+    const float sb = uniform(has_bnd ? fast_exp2(Rexb - Ri) : 0.0f);
+    float sj[16];
+    const float* sRjh = sRj + 4 * h;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int j = crow(v, h);
+      sj[v] = (j <= t) ? fast_exp2(sRjh[8 * (v >> 2) + (v & 3)] - Ri) : 0.0f;
+    }
+    const T* qrow = sQ + t * (D + PAD);
+#pragma unroll 1
+    for (int an = 0; an < NA; ++an) {
+      // keep the loop-invariant LDS operand reads inside the loop (hoisting
+      // them all would exhaust the register file)
+      no_hoist();
+      const int c = i - 32 * an - col;
+      const bool valid = (32 * an + col < a.w) && (c >= 0);
+      const int wi = t + 32 * NA - 1 - 32 * an - col;
+      const T* rrow = sR + wi * (D + PAD);
+      // G1: log2 features of the composite queries, lanes <-> anchor, regs <-> p
+      f32x16 accL[FB / 32];
+#pragma unroll
+      for (int pt = 0; pt < FB / 32; ++pt) accL[pt] = zero16();
+      float nz = 0.0f;
+#pragma unroll 2
+      for (int s = 0; s < D / F::KS; ++s) {
+        const int k0 = s * F::KS + h * F::KPL;
+        typename F::frag qf = F::ld(qrow, k0), rf = F::ld(rrow, k0), zf;
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            float p = valid ? fel(qf, e) * fel(rf, e) : 0.0f;
+            nz += p * p;
+            zf[e] = (bf16)p;
+          }
+        } else {
+          float p = valid ? qf * rf : 0.0f;
+          nz += p * p;
+          zf = p;
+        }
+#pragma unroll
+        for (int pt = 0; pt < FB / 32; ++pt)
+          accL[pt] = F::mma(F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), zf, accL[pt]);
+      }
+      nz = half_swap_add(nz);
+      const float bias = valid ? -0.5f * kLog2e * nz : kNegInf;
+      float tm = kNegInf;
+#pragma unroll
+      for (int pt = 0; pt < FB / 32; ++pt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) tm = fmaxf(tm, accL[pt][v]);
+      tm = uniform(wave_max(valid ? tm + bias : kNegInf));
+      const float Lnew = fmaxf(Lrun, tm);
+      if (Lnew > Lrun) {
+        const float sc = fast_exp2(Lrun - Lnew);
+        zacc *= sc;
+#pragma unroll
+        for (int dt = 0; dt < DV / 32; ++dt) nacc[dt] *= sc;
+        Lrun = Lnew;
+      }
+      const float off = bias - Lnew;
+      float zc = 0.0f;
+      // psi in place, boundary part of Z, then the operand-typed copy
+      typename F::frag pf[FB / 32][F::CSTEPS];
+      const float* sAh = sA + fb * FB + 4 * h;      // + pt*32 + 8*(v>>2) + (v&3)
+#pragma unroll
+      for (int pt = 0; pt < FB / 32; ++pt) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 av = *(const f32x4*)(sAh + pt * 32 + 8 * g);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float psi = fast_exp2(accL[pt][4 * g + e] + off);
+            accL[pt][4 * g + e] = psi;
+            zc += psi * av[e];
+          }
+        }
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp) pf[pt][sp] = F::cfrag(accL[pt], sp);
+      }
+      zc *= sb;
+      // intra-chunk causal correction: P^T[j, anchor] = chi_j . psi_anchor, scaled
+      // by the frame ratio 2^(R_j - R_i) and masked to j <= i
+      f32x16 accP = zero16();
+      const T* chirow = sChi + col * (M + PAD);
+#pragma unroll
+      for (int pt = 0; pt < FB / 32; ++pt)
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp)
+          accP = F::mma(F::ldc(chirow, fb * FB + pt * 32, sp, h), pf[pt][sp], accP);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        accP[v] *= sj[v];
+        zc += accP[v];
+      }
+      typename F::frag ppf[F::CSTEPS];
+#pragma unroll
+      for (int sp = 0; sp < F::CSTEPS; ++sp) ppf[sp] = F::cfrag(accP, sp);
+      // per 32-wide slice of d: boundary readout + correction, then the anchor
+      // combine N += A_c (*) u_c  (lanes <-> d, regs <-> anchor)
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt) {
+        no_hoist();
+        f32x16 accA = zero16();
+        if (has_bnd) {
+          const T* mrow = sMt + (dt * 32 + col) * (FB + PAD);
+#pragma unroll
+          for (int pt = 0; pt < FB / 32; ++pt)
+#pragma unroll
+            for (int sp = 0; sp < F::CSTEPS; ++sp)
+              accA = F::mma(pf[pt][sp], F::ldc(mrow, pt * 32, sp, h), accA);
+          if (sb != 1.0f) accA *= sb;
+        }
+        const T* vrow = sVt + (dt * 32 + col) * (32 + PAD);
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp) accA = F::mma(ppf[sp], F::ldc(vrow, 0, sp, h), accA);
+        // anchor row index crow(v,h) = 8*(v>>2) + 4h + (v&3) -> window index falls with it
+        const T* urow = sUt + (dt * 32 + col) * UST + (t + 32 * NA - 1 - 32 * an) - 4 * h;
+        float sacc = 0.0f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) sacc += accA[v] * tof(urow[-(8 * (v >> 2) + (v & 3))]);
+        nacc[dt] += sacc;
+      }
+        zacc += zc;
+    }
+    // ---- row epilogue ----
+    const float Z = wave_sum(zacc);
+    if constexpr (C::NFB == 1) {
+      const float inv = 1.0f / (Z + a.eps);
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt) {
+        float N = half_swap_add(nacc[dt]);
+        if (h == 0) ((T*)a.out)[(seq + i) * DV + dt * 32 + col] = (T)(N * inv);
+      }
+      if (l == 0 && a.stats != nullptr) {
+        a.stats[(seq + i) * 2 + 0] = Lrun;
+        a.stats[(seq + i) * 2 + 1] = Z;
+      }
+    } else {
+      // partial (N, Z, L) of this feature block; merged by k_merge_blocks
+      float* pr = a.part + (((size_t)fb * a.BH + bh) * n + i) * (DV + 2);
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt) {
+        float N = half_swap_add(nacc[dt]);
+        if (h == 0) pr[dt * 32 + col] = N;
+      }
+      if (l == 0) { pr[DV] = Z; pr[DV + 1] = Lrun; }
+    }
+  }
+}
+
+// Merge the per-feature-block partials (online-max combine of Alg. 1 across
+// blocks):  L = max_b L_b,  N = sum_b 2^(L_b - L) N_b,  Z likewise.
+template <typename T, int DV, int NFB>
+__global__ __launch_bounds__(256) void k_merge_blocks(FwdArgs a) {
+  const size_t rows = (size_t)a.BH * a.n;
+  const size_t row = (size_t)blockIdx.x * (256 / 32) + (threadIdx.x >> 5);
+  const int lane = threadIdx.x & 31;
+  if (row >= rows) return;
+  float L = kNegInf;
+#pragma unroll
+  for (int b = 0; b < NFB; ++b) L = fmaxf(L, a.part[((size_t)b * rows + row) * (DV + 2) + DV + 1]);
+  float Z = 0.0f;
+  float sc[NFB];
+#pragma unroll
+  for (int b = 0; b < NFB; ++b) {
+    const float* pr = a.part + ((size_t)b * rows + row) * (DV + 2);
+    sc[b] = fast_exp2(pr[DV + 1] - L);
+    Z += sc[b] * pr[DV];
+  }
+  const float inv = 1.0f / (Z + a.eps);
+  for (int d = lane; d < DV; d += 32) {
+    float N = 0.0f;
+#pragma unroll
+    for (int b = 0; b < NFB; ++b) N += sc[b] * a.part[((size_t)b * rows + row) * (DV + 2) + d];
+    ((T*)a.out)[row * DV + d] = (T)(N * inv);
+  }
+  if (lane == 0 && a.stats != nullptr) {
+    a.stats[row * 2 + 0] = L;
+    a.stats[row * 2 + 1] = Z;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------
+template <typename T, int D, int DV, int M, int NA>
+static int run_fwd(const Shape& s, FwdArgs a, hipStream_t st) {
+  constexpr int NW = 8;
+  const int BH = (int)s.BH();
+  const int nch = (int)s.nch();
+  {
+    int tot = (int)s.H * M * D;
+    k_prep_omega<T><<<(tot + 255) / 256, 256, 0, st>>>(a.omega, (T*)a.omq, (T*)a.omk, (int)s.H, M * D);
+  }
+  k_chunk_state<T, D, DV, M><<<dim3((nch + 3) / 4, BH), 256, 0, st>>>(a);
+  {
+    constexpr int S = M * DV + M;
+    k_state_scan<M, DV><<<dim3((S / 4 + 255) / 256, BH), 256, 0, st>>>(a);
+  }
+  if (a.out != nullptr) {
+    constexpr int NFB = RCfg<T, D, DV, M, NW, NA>::NFB;
+    k_readout<T, D, DV, M, NW, NA><<<dim3(nch, BH, NFB), 64 * NW, 0, st>>>(a);
+    if constexpr (NFB > 1) {
+      size_t rows = (size_t)BH * s.n;
+      k_merge_blocks<T, DV, NFB><<<(unsigned)((rows + 7) / 8), 256, 0, st>>>(a);
+    }
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    set_error("forward launch failed: %s", hipGetErrorString(e));
+    return -4;
+  }
+  return 0;
+}
+
+// Prefill ring: slot j mod w holds token j of the last min(n, w) tokens.
+template <typename T>
+__global__ __launch_bounds__(256) void k_ring_fill(const T* __restrict__ r, const T* __restrict__ u,
+                                                   T* __restrict__ rr, T* __restrict__ ru,
+                                                   int64_t* __restrict__ pos, int H, int n, int w,
+                                                   int D, int DV) {
+  const int bh = blockIdx.x;
+  const int width = D + DV;
+  for (int idx = threadIdx.x; idx < w * width; idx += 256) {
+    int slot = idx / width, e = idx % width;
+    // newest token j < n with j mod w == slot
+    int j = (n - 1) - (((n - 1 - slot) % w + w) % w);
+    bool ok = j >= 0 && j >= n - w;
+    if (e < D)
+      rr[((size_t)bh * w + slot) * D + e] = ok ? r[((size_t)bh * n + j) * D + e] : (T)0.0f;
+    else
+      ru[((size_t)bh * w + slot) * DV + (e - D)] = ok ? u[((size_t)bh * n + j) * DV + (e - D)] : (T)0.0f;
+  }
+  if (threadIdx.x == 0 && bh % H == 0) pos[bh / H] = n;
+}
+
+int launch_ring_fill(const Shape& s, const void* r, const void* u, void* ring_r, void* ring_u,
+                     int64_t* pos, hipStream_t st) {
+  const int BH = (int)s.BH();
+  if (s.dtype == 1)
+    k_ring_fill<bf16><<<BH, 256, 0, st>>>((const bf16*)r, (const bf16*)u, (bf16*)ring_r, (bf16*)ring_u,
+                                          pos, (int)s.H, (int)s.n, s.w, s.D, s.Dv);
+  else
+    k_ring_fill<float><<<BH, 256, 0, st>>>((const float*)r, (const float*)u, (float*)ring_r,
+                                           (float*)ring_u, pos, (int)s.H, (int)s.n, s.w, s.D, s.Dv);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    set_error("ring fill launch failed: %s", hipGetErrorString(e));
+    return -4;
+  }
+  return 0;
+}
+
+// Supported (dtype, D = Dv, m) combinations; w <= 64.
+#define LS_FWD_CASES(X)               \
+  X(bf16, 32, 32, 32)                 \
+  X(bf16, 64, 64, 64)                 \
+  X(bf16, 64, 64, 128)                \
+  X(bf16, 128, 128, 64)               \
+  X(bf16, 128, 128, 128)              \
+  X(bf16, 128, 128, 256)              \
+  X(float, 32, 32, 32)                \
+  X(float, 32, 32, 64)                \
+  X(float, 64, 64, 32)                \
+  X(float, 64, 64, 64)
+
+bool fwd_combo_supported(int dtype, int D, int Dv, int m) {
+#define X(T, D_, DV_, M_) \
+  if (dtype == (sizeof(T) == 2 ? 1 : 0) && D == D_ && Dv == DV_ && m == M_) return true;
+  LS_FWD_CASES(X)
+#undef X
+  return false;
+}
+
+int launch_forward(const Shape& s, const void* q, const void* k, const void* v, const void* r,
+                   const void* u, const float* omega, void* out, float* stats, float* final_M,
+                   float* final_a, float* final_rex, const Workspace& ws, hipStream_t st) {
+  FwdArgs a;
+  a.q = q; a.k = k; a.v = v; a.r = r; a.u = u; a.omega = omega;
+  a.out = out; a.stats = stats;
+  a.omq = ws.omq; a.omk = ws.omk; a.states = ws.states; a.rho = ws.rho; a.rex = ws.rex;
+  a.final_M = final_M; a.final_a = final_a; a.final_rex = final_rex;
+  a.H = (int)s.H; a.n = (int)s.n; a.w = s.w; a.nch = (int)s.nch(); a.BH = (int)s.BH(); a.eps = s.eps;
+  a.part = ws.part;
+  const int NA = (s.w + 31) / 32;
+#define X(T, D_, DV_, M_)                                                          \
+  if (s.dtype == (sizeof(T) == 2 ? 1 : 0) && s.D == D_ && s.Dv == DV_ && s.m == M_) { \
+    if (NA == 1) return run_fwd<T, D_, DV_, M_, 1>(s, a, st);                      \
+    return run_fwd<T, D_, DV_, M_, 2>(s, a, st);                                   \
+  }
+  LS_FWD_CASES(X)
+#undef X
+  set_error("unsupported shape (dtype=%d D=%d Dv=%d m=%d)", s.dtype, s.D, s.Dv, s.m);
+  return -2;
+}
+
+}  // namespace linsimp

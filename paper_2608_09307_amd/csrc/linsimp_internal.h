@@ -1,0 +1,67 @@
+// Internal (host + device) declarations shared by the LinSimp HIP sources.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace linsimp {
+
+// Sequence chunk used by every kernel: key chunks for the prefix-state scan and
+// the row chunks of the readout share it.
+constexpr int kChunk = 32;
+
+struct Shape {
+  int64_t B, H, n;
+  int D, Dv, m, w;
+  int dtype;   // 0 = f32, 1 = bf16
+  float eps;
+  int64_t BH() const { return B * H; }
+  int64_t nch() const { return (n + kChunk - 1) / kChunk; }
+  int64_t state_elems() const { return (int64_t)m * Dv + m; }   // M (m x Dv) then a (m)
+  size_t esize() const { return dtype == 1 ? 2 : 4; }
+};
+
+// Workspace carve shared by forward and backward.
+struct Workspace {
+  void* omq;        // [H][m][D] operand type: query-side Omega * log2(e)
+  void* omk;        // bf16: [H][2][m][D] hi/lo split of Omega*log2(e); f32: [H][m][D]
+  float* states;    // [BH][nch][m*Dv + m]  chunk contributions, then boundary states
+  float* rho;       // [BH][nch]            chunk max of key log2-features
+  float* rex;       // [BH][nch + 1]        frame (log2) of each boundary state; [nch] = final
+  float* part;      // [m/128][BH][n][Dv+2] per-feature-block readout partials (m > 128)
+  // backward-only regions (null in forward)
+  float* gstates;   // [BH][nch][m*Dv + m]  per-chunk state gradients, then reverse-scanned
+  float* dchi;      // [BH][n][m]           intra-chunk key-feature gradient (frame R_j)
+  float* dvin;      // [BH][n][Dv]          intra-chunk value gradient
+  float* du32;      // [BH][nch][WIN][Dv]   per-chunk anchor-gradient partials (du)
+  float* dr32;      // [BH][nch][WIN][D]    per-chunk anchor-gradient partials (dr)
+  float* rowstat;   // [BH][n][4]           per-row backward scalars
+};
+
+size_t workspace_bytes(const Shape& s, bool backward);
+void carve(const Shape& s, void* base, bool backward, Workspace* ws);
+
+// Returns 0 on success, negative linsimp status otherwise (message via set_error).
+int launch_forward(const Shape& s, const void* q, const void* k, const void* v, const void* r,
+                   const void* u, const float* omega, void* out, float* stats,
+                   float* final_M, float* final_a, float* final_rex, const Workspace& ws,
+                   hipStream_t st);
+bool fwd_combo_supported(int dtype, int D, int Dv, int m);
+int launch_ring_fill(const Shape& s, const void* r, const void* u, void* ring_r, void* ring_u,
+                     int64_t* pos, hipStream_t st);
+
+int launch_backward(const Shape& s, const void* q, const void* k, const void* v, const void* r,
+                    const void* u, const float* omega, const void* out, const float* stats,
+                    const void* dout, void* dq, void* dk, void* dv, void* dr, void* du,
+                    const Workspace& ws, hipStream_t st);
+
+int launch_decode(int64_t S, int H, int D, int Dv, int m, int w, int dtype, float eps,
+                  const void* q, const void* k, const void* v, const void* r, const void* u,
+                  const float* omega, float* M, float* a, float* rho, void* ring_r, void* ring_u,
+                  int64_t* pos, void* out, hipStream_t st);
+
+void set_error(const char* fmt, ...);
+bool shape_supported(const Shape& s, bool backward);
+
+}  // namespace linsimp

@@ -1,0 +1,194 @@
+"""Thin ctypes binding of liblinsimp.so (the C ABI in include/linsimp.h).
+
+Argument marshalling only: torch tensors are turned into device pointers and
+the current HIP stream is passed through.  Every step of the computation runs
+in the library's HIP kernels; there is no CPU or PyTorch fallback, and every
+entry point raises if the library is not built or a tensor is not on the GPU.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_lib", "liblinsimp.so")
+_lib = None
+
+F32, BF16 = 0, 1
+EPS = 1e-30
+
+
+class LinSimpError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"linsimp status {status}: {message}")
+        self.status = status
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int64), ("H", ctypes.c_int64), ("n", ctypes.c_int64),
+                ("D", ctypes.c_int32), ("Dv", ctypes.c_int32), ("m", ctypes.c_int32),
+                ("w", ctypes.c_int32), ("dtype", ctypes.c_int32), ("eps", ctypes.c_float)]
+
+
+EXPORTS = ("linsimp_workspace_size", "linsimp_fwd", "linsimp_bwd", "linsimp_prefill",
+           "linsimp_decode_step", "linsimp_last_error", "linsimp_version")
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def lib():
+    """Load liblinsimp.so (raises if it is not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError(f"{_LIB_PATH} is not built; run paper_2608_09307_amd.build.build()")
+    L = ctypes.CDLL(_LIB_PATH)
+    vp, sz, i32, i64, f32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    pd = ctypes.POINTER(Dims)
+    L.linsimp_workspace_size.argtypes = [pd, ctypes.c_int]
+    L.linsimp_workspace_size.restype = sz
+    L.linsimp_fwd.argtypes = [pd] + [vp] * 8 + [vp, sz, vp]
+    L.linsimp_fwd.restype = ctypes.c_int
+    L.linsimp_bwd.argtypes = [pd] + [vp] * 14 + [vp, sz, vp]
+    L.linsimp_bwd.restype = ctypes.c_int
+    L.linsimp_prefill.argtypes = [pd] + [vp] * 11 + [vp, sz, vp]
+    L.linsimp_prefill.restype = ctypes.c_int
+    L.linsimp_decode_step.argtypes = [i64, i32, i32, i32, i32, i32, i32, f32] + [vp] * 13 + [vp]
+    L.linsimp_decode_step.restype = ctypes.c_int
+    L.linsimp_last_error.argtypes = []
+    L.linsimp_last_error.restype = ctypes.c_char_p
+    L.linsimp_version.argtypes = []
+    L.linsimp_version.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(rc: int):
+    if rc != 0:
+        raise LinSimpError(rc, lib().linsimp_last_error().decode())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _ptr(t: Optional[torch.Tensor], name: str):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def make_dims(B, H, n, D, Dv, m, w, dtype, eps=EPS) -> Dims:
+    return Dims(B, H, n, D, Dv, m, w, dtype, eps)
+
+
+def dims_of(q: torch.Tensor, v: torch.Tensor, omega: torch.Tensor, w: int, eps: float = EPS) -> Dims:
+    B, H, n, D = q.shape
+    return make_dims(B, H, n, D, v.shape[-1], omega.shape[1], w, _dtype_code(q), eps)
+
+
+def workspace_size(d: Dims, backward: bool) -> int:
+    return int(lib().linsimp_workspace_size(ctypes.byref(d), 1 if backward else 0))
+
+
+def alloc_workspace(d: Dims, backward: bool, device) -> torch.Tensor:
+    nbytes = workspace_size(d, backward)
+    if nbytes == 0:
+        _check(lib().linsimp_workspace_size(ctypes.byref(d), 1 if backward else 0) or -2)
+    ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+    off = (-ws.data_ptr()) % 256
+    return ws[off: off + nbytes]
+
+
+def fwd(q, k, v, r, u, omega, w, eps=EPS, out=None, stats=None, workspace=None,
+        want_stats=True):
+    """Forward pass; returns (out, stats).  See linsimp_fwd."""
+    d = dims_of(q, v, omega, w, eps)
+    if out is None:
+        out = torch.empty(q.shape[:3] + (v.shape[-1],), dtype=q.dtype, device=q.device)
+    if stats is None and want_stats:
+        stats = torch.empty(q.shape[:3] + (2,), dtype=torch.float32, device=q.device)
+    if workspace is None:
+        workspace = alloc_workspace(d, False, q.device)
+    _check(lib().linsimp_fwd(ctypes.byref(d), _ptr(q, "q"), _ptr(k, "k"), _ptr(v, "v"),
+                             _ptr(r, "r"), _ptr(u, "u"), _ptr(omega, "omega"), _ptr(out, "out"),
+                             _ptr(stats, "stats"), _ptr(workspace, "workspace"),
+                             workspace.numel(), _stream()))
+    return out, stats
+
+
+def bwd(q, k, v, r, u, omega, w, out, stats, dout, eps=EPS, grads=None, workspace=None):
+    """Backward pass; returns (dq, dk, dv, dr, du).  See linsimp_bwd."""
+    d = dims_of(q, v, omega, w, eps)
+    if grads is None:
+        grads = tuple(torch.empty_like(x) for x in (q, k, v, r, u))
+    dq, dk, dv, dr, du = grads
+    if workspace is None:
+        workspace = alloc_workspace(d, True, q.device)
+    _check(lib().linsimp_bwd(ctypes.byref(d), _ptr(q, "q"), _ptr(k, "k"), _ptr(v, "v"),
+                             _ptr(r, "r"), _ptr(u, "u"), _ptr(omega, "omega"), _ptr(out, "out"),
+                             _ptr(stats, "stats"), _ptr(dout, "dout"), _ptr(dq, "dq"),
+                             _ptr(dk, "dk"), _ptr(dv, "dv"), _ptr(dr, "dr"), _ptr(du, "du"),
+                             _ptr(workspace, "workspace"), workspace.numel(), _stream()))
+    return dq, dk, dv, dr, du
+
+
+def prefill(k, v, r, u, omega, w, eps=EPS, workspace=None):
+    """Decode state after a prefix (k, v, r, u: [S, H, n, *]).  Returns a dict
+    with M [S,H,m,Dv], a [S,H,m], rho [S,H] (log2 frame), ring_r, ring_u, pos."""
+    S, H, n, D = k.shape
+    Dv = v.shape[-1]
+    m = omega.shape[1]
+    d = make_dims(S, H, n, D, Dv, m, w, _dtype_code(k), eps)
+    dev = k.device
+    st = {"M": torch.empty(S, H, m, Dv, dtype=torch.float32, device=dev),
+          "a": torch.empty(S, H, m, dtype=torch.float32, device=dev),
+          "rho": torch.empty(S, H, dtype=torch.float32, device=dev),
+          "ring_r": torch.empty(S, H, w, D, dtype=k.dtype, device=dev),
+          "ring_u": torch.empty(S, H, w, Dv, dtype=k.dtype, device=dev),
+          "pos": torch.empty(S, dtype=torch.int64, device=dev)}
+    if workspace is None:
+        workspace = alloc_workspace(d, False, dev)
+    _check(lib().linsimp_prefill(ctypes.byref(d), _ptr(k, "k"), _ptr(v, "v"), _ptr(r, "r"),
+                                 _ptr(u, "u"), _ptr(omega, "omega"), _ptr(st["M"], "M"),
+                                 _ptr(st["a"], "a"), _ptr(st["rho"], "rho"),
+                                 _ptr(st["ring_r"], "ring_r"), _ptr(st["ring_u"], "ring_u"),
+                                 _ptr(st["pos"], "pos"), _ptr(workspace, "workspace"),
+                                 workspace.numel(), _stream()))
+    return st
+
+
+def decode_step(state, q, k, v, r, u, omega, w, eps=EPS, out=None):
+    """One decode step for S sequences (q, k, v, r, u: [S, H, *]); updates
+    ``state`` in place and returns out [S, H, Dv]."""
+    S, H, D = q.shape
+    Dv = v.shape[-1]
+    m = omega.shape[1]
+    if out is None:
+        out = torch.empty(S, H, Dv, dtype=q.dtype, device=q.device)
+    _check(lib().linsimp_decode_step(S, H, D, Dv, m, w, _dtype_code(q), eps, _ptr(q, "q"),
+                                     _ptr(k, "k"), _ptr(v, "v"), _ptr(r, "r"), _ptr(u, "u"),
+                                     _ptr(omega, "omega"), _ptr(state["M"], "M"),
+                                     _ptr(state["a"], "a"), _ptr(state["rho"], "rho"),
+                                     _ptr(state["ring_r"], "ring_r"),
+                                     _ptr(state["ring_u"], "ring_u"), _ptr(state["pos"], "pos"),
+                                     _ptr(out, "out"), _stream()))
+    return out

@@ -1,0 +1,77 @@
+"""CPU-side checks of the C ABI: the library loads, exports every symbol the
+header declares, and rejects bad arguments before touching a GPU."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_09307_amd import linsimp as L
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "linsimp.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(linsimp_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = L.lib()
+    names = _declared()
+    assert set(names) == set(L.EXPORTS)
+    for name in names:
+        assert hasattr(lib, name), name
+    assert lib.linsimp_version() == 100
+
+
+def test_workspace_size_and_unsupported_shapes():
+    d = L.make_dims(2, 16, 16384, 128, 128, 128, 64, L.BF16)
+    fw, bw = L.workspace_size(d, False), L.workspace_size(d, True)
+    assert 0 < fw < bw
+    for bad in (L.make_dims(1, 1, 256, 48, 48, 32, 64, L.BF16),     # D not supported
+                L.make_dims(1, 1, 256, 32, 32, 32, 65, L.BF16),     # w > 64
+                L.make_dims(1, 1, 256, 128, 128, 128, 64, L.F32),   # f32 only up to 64
+                L.make_dims(1, 1, 0, 32, 32, 32, 64, L.BF16),       # n = 0
+                L.make_dims(1, 1, 8, 32, 32, 32, 64, 7)):           # bad dtype
+        assert L.workspace_size(bad, False) == 0
+        assert L.lib().linsimp_last_error()
+
+
+def _call_fwd(d, ptrs, ws, nbytes):
+    lib = L.lib()
+    vp = ctypes.c_void_p
+    return lib.linsimp_fwd(ctypes.byref(d), *[vp(p) for p in ptrs], vp(ws), nbytes, vp(0))
+
+
+def test_argument_errors_are_reported_not_raised():
+    d = L.make_dims(1, 1, 64, 32, 32, 32, 8, L.F32)
+    good = [4096 * (i + 1) for i in range(8)]
+    need = L.workspace_size(d, False)
+    # NULL q
+    assert _call_fwd(d, [0] + good[1:], 1 << 20, need) == -1
+    assert b"NULL" in L.lib().linsimp_last_error()
+    # misaligned k
+    assert _call_fwd(d, [good[0], good[1] + 4] + good[2:], 1 << 20, need) == -1
+    # workspace too small / misaligned
+    assert _call_fwd(d, good, 1 << 20, need - 1) == -3
+    assert _call_fwd(d, good, (1 << 20) + 16, need) == -3
+    # unsupported shape
+    d2 = L.make_dims(1, 1, 64, 96, 96, 32, 8, L.F32)
+    assert _call_fwd(d2, good, 1 << 20, 1 << 30) == -2
+    # decode: bad window
+    lib = L.lib()
+    vp = ctypes.c_void_p
+    rc = lib.linsimp_decode_step(4, 2, 32, 32, 32, 0, L.BF16, 1e-30,
+                                 *[vp(4096 * (i + 1)) for i in range(13)], vp(0))
+    assert rc == -1
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    x = torch.zeros(1, 1, 8, 32)
+    om = torch.zeros(1, 32, 32)
+    with pytest.raises((ValueError, RuntimeError)):
+        L.fwd(x, x, x, x, x, om, 4, workspace=torch.zeros(1 << 16, dtype=torch.uint8))
