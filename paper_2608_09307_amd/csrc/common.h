@@ -113,18 +113,35 @@ LS_DEV int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
 LS_DEV void no_hoist() { asm volatile("" ::: "memory"); }
 
 // ---- wave reductions (64 lanes) ----
+// DPP within each 16-lane row, then the four row results are read into scalar
+// registers: the result is wave-uniform and lives in an SGPR.
+template <int CTRL> LS_DEV float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(x), __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+LS_DEV float rlane(float x, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l)); }
 LS_DEV float wave_max(float x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
-  return x;
+  x = fmaxf(x, dpp<0xB1>(x));     // quad_perm [1,0,3,2]
+  x = fmaxf(x, dpp<0x4E>(x));     // quad_perm [2,3,0,1]
+  x = fmaxf(x, dpp<0x124>(x));    // row_ror:4
+  x = fmaxf(x, dpp<0x128>(x));    // row_ror:8
+  return fmaxf(fmaxf(rlane(x, 0), rlane(x, 16)), fmaxf(rlane(x, 32), rlane(x, 48)));
 }
 LS_DEV float wave_sum(float x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
-  return x;
+  x += dpp<0xB1>(x);
+  x += dpp<0x4E>(x);
+  x += dpp<0x124>(x);
+  x += dpp<0x128>(x);
+  return (rlane(x, 0) + rlane(x, 16)) + (rlane(x, 32) + rlane(x, 48));
 }
-LS_DEV float half_swap_add(float x) { return x + __shfl_xor(x, 32, 64); }
-LS_DEV float half_swap_max(float x) { return fmaxf(x, __shfl_xor(x, 32, 64)); }
+// x[l] (op) x[l ^ 32] via v_permlane32_swap
+LS_DEV float half_swap_add(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+LS_DEV float half_swap_max(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
 
 // ---- cooperative global -> LDS copies (block-wide) ----
 // 2D copy of a [rows][cols] T matrix (global row stride gstride) into LDS with

@@ -1,13 +1,299 @@
-// LinSimp autoregressive decode step on gfx950.
+// LinSimp autoregressive decode step on gfx950 (Theorem 1: the persistent
+// state of a head is M, a and the last w anchor rows (r_c, u_c)).
+//
+// Per (sequence s, head h), token t = pos[s]:
+//   lambda = log2-features of k_t;  R' = max(R, max_p lambda_p)
+//   M <- 2^(R-R') M + chi v_t^T,  a <- 2^(R-R') a + chi,  chi = 2^(lambda - R')/sqrt(m)
+//   (eq:Mstate / eq:astate in the frame R'; M_true = 2^R' M)
+//   ring slot t mod w <- (r_t, u_t)
+//   out = N / (Z + eps) over the min(t+1, w) most recent anchors (eq:Ni, eq:Zi)
+// The readout uses the contraction order W = Psi^T U (matrix cores, sum over
+// anchors), then N_d = sum_p M[p,d] W[p,d] fused with the state update, so
+// every float32 state element is read once and written once.
 #include "common.h"
 #include "linsimp_internal.h"
 
 namespace linsimp {
 
-int launch_decode(int64_t, int, int D, int, int m, int, int dtype, float, const void*, const void*,
-                  const void*, const void*, const void*, const float*, float*, float*, float*,
-                  void*, void*, int64_t*, void*, hipStream_t) {
-  set_error("decode not built for dtype=%d D=%d m=%d", dtype, D, m);
+struct DecArgs {
+  const void* q; const void* k; const void* v; const void* r; const void* u;
+  const float* omega;
+  float* M; float* a; float* rho;
+  void* ring_r; void* ring_u;
+  int64_t* pos;
+  void* out;
+  int H; int w; float eps;
+};
+
+template <typename T, int D, int DV, int M, int NA>
+struct DCfg {
+  static constexpr int PAD = MF<T>::PAD;
+  static constexpr int W = 32 * NA;
+  static constexpr int ES = sizeof(T);
+  static constexpr int a16(int x) { return (x + 15) & ~15; }
+  static constexpr int oOm = 0;
+  static constexpr int oRr = oOm + a16(M * (D + PAD) * ES);
+  static constexpr int oUt = oRr + a16(W * (D + PAD) * ES);
+  static constexpr int oQ = oUt + a16(DV * (W + PAD) * ES);
+  static constexpr int oK = oQ + a16(D * 4);
+  static constexpr int oV = oK + a16(D * 4);
+  static constexpr int oChi = oV + a16(DV * 4);
+  static constexpr int oAn = oChi + a16(M * 4);
+  static constexpr int oNz = oAn + a16(M * 4);
+  static constexpr int oRed = oNz + a16(W * 4);
+  static constexpr int oN = oRed + a16(64 * 4);
+  static constexpr int BYTES = oN + a16(4 * DV * 4);
+};
+
+template <typename T, int D, int DV, int M, int NA>
+__global__ __launch_bounds__(256) void k_decode(DecArgs A) {
+  using F = MF<T>;
+  using C = DCfg<T, D, DV, M, NA>;
+  constexpr int PAD = C::PAD, W = C::W;
+  constexpr int PT = M / 32;                  // feature tiles
+  constexpr int PTW = (PT + 3) / 4;           // feature tiles per wave
+  static_assert(C::BYTES <= 160 * 1024, "decode LDS budget");
+  __shared__ __align__(16) char smem[C::BYTES];
+  T* sOm = (T*)(smem + C::oOm);
+  T* sRr = (T*)(smem + C::oRr);
+  T* sUt = (T*)(smem + C::oUt);
+  float* sq = (float*)(smem + C::oQ);
+  float* sk = (float*)(smem + C::oK);
+  float* sv = (float*)(smem + C::oV);
+  float* schi = (float*)(smem + C::oChi);
+  float* san = (float*)(smem + C::oAn);
+  float* snz = (float*)(smem + C::oNz);
+  float* sred = (float*)(smem + C::oRed);
+  float* sN = (float*)(smem + C::oN);
+
+  const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
+  const int sh = blockIdx.x, H = A.H, w = A.w;
+  const int s = sh / H, hh = sh % H;
+  const int64_t t = A.pos[s];
+  const int slot = (int)(t % w);
+  const int nvalid = (int)((t + 1 < w) ? t + 1 : w);
+  const T* qt = (const T*)A.q + (size_t)sh * D;
+  const T* kt = (const T*)A.k + (size_t)sh * D;
+  const T* vt = (const T*)A.v + (size_t)sh * DV;
+  const T* rt = (const T*)A.r + (size_t)sh * D;
+  const T* ut = (const T*)A.u + (size_t)sh * DV;
+  T* rr = (T*)A.ring_r + (size_t)sh * w * D;
+  T* ru = (T*)A.ring_u + (size_t)sh * w * DV;
+  const float* om = A.omega + (size_t)hh * M * D;
+  float* Ms = A.M + (size_t)sh * M * DV;
+  float* as = A.a + (size_t)sh * M;
+
+  // ---- stage the token, the ring (slot t mod w replaced by the new token) and Omega ----
+  for (int i = tid; i < D; i += 256) { sq[i] = tof(qt[i]); sk[i] = tof(kt[i]); }
+  for (int i = tid; i < DV; i += 256) sv[i] = tof(vt[i]);
+  for (int i = tid; i < W * D; i += 256) {
+    int c = i / D, e = i % D;
+    T x = (T)0.0f;
+    if (c < w) x = (c == slot) ? rt[e] : rr[(size_t)c * D + e];
+    sRr[c * (D + PAD) + e] = x;
+  }
+  for (int i = tid; i < W * DV; i += 256) {
+    int c = i / DV, e = i % DV;
+    T x = (T)0.0f;
+    if (c < w) x = (c == slot) ? ut[e] : ru[(size_t)c * DV + e];
+    sUt[e * (W + PAD) + F::sigma(c)] = x;
+  }
+  for (int i = tid; i < M * D; i += 256) sOm[(i / D) * (D + PAD) + (i % D)] = (T)(om[i] * kLog2e);
+  const float Rold = A.rho[sh];
+  __syncthreads();
+
+  // ---- key features of k_t (float32 GEMV) and the frame update ----
+  float nk = 0.0f;
+  for (int e = 0; e < D; ++e) nk += sk[e] * sk[e];
+  float lam = kNegInf;
+  if (tid < M) {
+    const float* orow = om + (size_t)tid * D;
+    float acc = 0.0f;
+    for (int e = 0; e < D; ++e) acc += orow[e] * sk[e];
+    lam = (acc - 0.5f * nk) * kLog2e;
+  }
+  float mx = wave_max(lam);
+  if (l == 0) sred[wv] = mx;
+  __syncthreads();
+  const float rho_t = fmaxf(fmaxf(sred[0], sred[1]), fmaxf(sred[2], sred[3]));
+  const float Rn = fmaxf(Rold, rho_t);
+  const float sa = fast_exp2(Rold - Rn);          // 0 for an empty state (R = -inf)
+  if (tid < M) {
+    float chi = fast_exp2(lam - Rn) * rsqrtf((float)M);
+    schi[tid] = chi;
+    float an = sa * as[tid] + chi;
+    san[tid] = an;
+    as[tid] = an;
+  }
+  // ---- composite-query logits, lanes <-> feature p, registers <-> anchor ----
+  f32x16 acc[PTW][NA];
+  float nz[NA];
+#pragma unroll
+  for (int pi = 0; pi < PTW; ++pi)
+#pragma unroll
+    for (int ct = 0; ct < NA; ++ct) acc[pi][ct] = zero16();
+#pragma unroll
+  for (int ct = 0; ct < NA; ++ct) nz[ct] = 0.0f;
+#pragma unroll
+  for (int ct = 0; ct < NA; ++ct) {
+    const int c = ct * 32 + col;
+    const bool valid = c < nvalid;
+#pragma unroll 2
+    for (int ks = 0; ks < D / F::KS; ++ks) {
+      const int k0 = ks * F::KS + h * F::KPL;
+      typename F::frag rf = F::ld(sRr + c * (D + PAD), k0), zf;
+      if constexpr (sizeof(T) == 2) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          float p = valid ? sq[k0 + e] * fel(rf, e) : 0.0f;
+          nz[ct] += p * p;
+          zf[e] = (bf16)p;
+        }
+      } else {
+        float p = valid ? sq[k0] * rf : 0.0f;
+        nz[ct] += p * p;
+        zf = p;
+      }
+#pragma unroll
+      for (int pi = 0; pi < PTW; ++pi) {
+        const int pt = wv + 4 * pi;
+        if (pt < PT)
+          acc[pi][ct] = F::mma(zf, F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), acc[pi][ct]);
+      }
+    }
+    nz[ct] = half_swap_add(nz[ct]);
+    if (wv == 0 && h == 0) snz[c] = valid ? -0.5f * kLog2e * nz[ct] : kNegInf;
+  }
+  __syncthreads();
+  // row maximum over valid (anchor, feature)
+  float tm = kNegInf;
+#pragma unroll
+  for (int pi = 0; pi < PTW; ++pi) {
+    if (wv + 4 * pi >= PT) continue;
+#pragma unroll
+    for (int ct = 0; ct < NA; ++ct)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float x = acc[pi][ct][v] + snz[ct * 32 + crow(v, h)];
+        acc[pi][ct][v] = x;
+        tm = fmaxf(tm, x);
+      }
+  }
+  tm = wave_max(tm);
+  if (l == 0) sred[8 + wv] = tm;
+  __syncthreads();
+  const float L = fmaxf(fmaxf(sred[8], sred[9]), fmaxf(sred[10], sred[11]));
+  // psi, Z, then W = Psi^T U and N = sum_p M'[p,:] (*) W[p,:] with the state update
+  float zpart = 0.0f;
+  float npart[DV / 32];
+#pragma unroll
+  for (int dt = 0; dt < DV / 32; ++dt) npart[dt] = 0.0f;
+#pragma unroll
+  for (int pi = 0; pi < PTW; ++pi) {
+    const int pt = wv + 4 * pi;
+    if (pt >= PT) continue;
+    const float anp = san[pt * 32 + col];
+#pragma unroll
+    for (int ct = 0; ct < NA; ++ct)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        float psi = fast_exp2(acc[pi][ct][v] - L);
+        acc[pi][ct][v] = psi;
+        zpart += psi * anp;
+      }
+#pragma unroll 1
+    for (int dt = 0; dt < DV / 32; ++dt) {
+      no_hoist();
+      f32x16 accW = zero16();
+      const T* urow = sUt + (dt * 32 + col) * (W + PAD);
+#pragma unroll
+      for (int ct = 0; ct < NA; ++ct)
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp)
+          accW = F::mma(F::cfrag(acc[pi][ct], sp), F::ldc(urow, ct * 32, sp, h), accW);
+      // accW: lanes <-> d, registers <-> p
+      const int d = dt * 32 + col;
+      const float vd = sv[d];
+      float np = 0.0f;
+#pragma unroll
+      for (int vv = 0; vv < 16; ++vv) {
+        const int p = pt * 32 + crow(vv, h);
+        float* mp = Ms + (size_t)p * DV + d;
+        float mnew = sa * (*mp) + schi[p] * vd;
+        *mp = mnew;
+        np += mnew * accW[vv];
+      }
+      npart[dt] += np;
+    }
+  }
+  // (feature tile pt belongs to wave pt mod 4, so every state row is updated once)
+  zpart = wave_sum(zpart);
+  if (l == 0) sred[16 + wv] = zpart;
+#pragma unroll
+  for (int dt = 0; dt < DV / 32; ++dt) {
+    float nn = half_swap_add(npart[dt]);
+    if (h == 0) sN[wv * DV + dt * 32 + col] = nn;
+  }
+  __syncthreads();
+  const float Z = (sred[16] + sred[17]) + (sred[18] + sred[19]);
+  const float inv = 1.0f / (Z + A.eps);
+  for (int d = tid; d < DV; d += 256) {
+    float N = (sN[d] + sN[DV + d]) + (sN[2 * DV + d] + sN[3 * DV + d]);
+    ((T*)A.out)[(size_t)sh * DV + d] = (T)(N * inv);
+  }
+  // ring slot and frame
+  for (int e = tid; e < D; e += 256) rr[(size_t)slot * D + e] = rt[e];
+  for (int e = tid; e < DV; e += 256) ru[(size_t)slot * DV + e] = ut[e];
+  if (tid == 0) A.rho[sh] = Rn;
+}
+
+// pos[s] += 1 after every head of sequence s has read it
+__global__ __launch_bounds__(256) void k_decode_advance(int64_t* pos, int64_t S) {
+  int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < S) pos[i] += 1;
+}
+
+template <typename T, int D, int DV, int M, int NA>
+static int run_decode(int64_t S, DecArgs a, hipStream_t st) {
+  k_decode<T, D, DV, M, NA><<<(unsigned)(S * a.H), 256, 0, st>>>(a);
+  k_decode_advance<<<(unsigned)((S + 255) / 256), 256, 0, st>>>(a.pos, S);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    set_error("decode launch failed: %s", hipGetErrorString(e));
+    return -4;
+  }
+  return 0;
+}
+
+#define LS_DEC_CASES(X)   \
+  X(bf16, 32, 32, 32)     \
+  X(bf16, 64, 64, 64)     \
+  X(bf16, 64, 64, 128)    \
+  X(bf16, 128, 128, 64)   \
+  X(bf16, 128, 128, 128)  \
+  X(bf16, 128, 128, 256)  \
+  X(float, 32, 32, 32)    \
+  X(float, 32, 32, 64)    \
+  X(float, 64, 64, 32)    \
+  X(float, 64, 64, 64)
+
+int launch_decode(int64_t S, int H, int D, int Dv, int m, int w, int dtype, float eps,
+                  const void* q, const void* k, const void* v, const void* r, const void* u,
+                  const float* omega, float* M, float* a, float* rho, void* ring_r, void* ring_u,
+                  int64_t* pos, void* out, hipStream_t st) {
+  DecArgs A;
+  A.q = q; A.k = k; A.v = v; A.r = r; A.u = u; A.omega = omega;
+  A.M = M; A.a = a; A.rho = rho; A.ring_r = ring_r; A.ring_u = ring_u; A.pos = pos; A.out = out;
+  A.H = H; A.w = w; A.eps = eps;
+  const int NA = (w + 31) / 32;
+#define X(T, D_, DV_, M_)                                                              \
+  if (dtype == (sizeof(T) == 2 ? 1 : 0) && D == D_ && Dv == DV_ && m == M_) {          \
+    if (NA == 1) return run_decode<T, D_, DV_, M_, 1>(S, A, st);                       \
+    return run_decode<T, D_, DV_, M_, 2>(S, A, st);                                    \
+  }
+  LS_DEC_CASES(X)
+#undef X
+  set_error("decode: unsupported shape (dtype=%d D=%d Dv=%d m=%d)", dtype, D, Dv, m);
   return -2;
 }
 

@@ -399,7 +399,7 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
       for (int pt = 0; pt < FB / 32; ++pt)
 #pragma unroll
         for (int v = 0; v < 16; ++v) tm = fmaxf(tm, accL[pt][v]);
-      tm = uniform(wave_max(valid ? tm + bias : kNegInf));
+      tm = wave_max(valid ? tm + bias : kNegInf);
       const float Lnew = fmaxf(Lrun, tm);
       if (Lnew > Lrun) {
         const float sc = fast_exp2(Lrun - Lnew);
@@ -448,7 +448,7 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
       for (int sp = 0; sp < F::CSTEPS; ++sp) ppf[sp] = F::cfrag(accP, sp);
       // per 32-wide slice of d: boundary readout + correction, then the anchor
       // combine N += A_c (*) u_c  (lanes <-> d, regs <-> anchor)
-#pragma unroll
+#pragma unroll 1
       for (int dt = 0; dt < DV / 32; ++dt) {
         no_hoist();
         f32x16 accA = zero16();
