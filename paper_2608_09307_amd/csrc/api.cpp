@@ -32,13 +32,12 @@ size_t workspace_bytes(const Shape& s, bool backward) {
   t += al(BH * (nch + 1) * 4);                 // rex
   if (s.m > 128) t += al((size_t)(s.m / 128) * BH * s.n * (s.Dv + 2) * 4);   // part
   if (backward) {
-    const size_t n = (size_t)s.n, win = kChunk + 64 - 1;
+    const size_t n = (size_t)s.n, nfb = s.m > 128 ? (size_t)s.m / 128 : 1;
     t += al(BH * nch * S * 4);                 // gstates
     t += al(BH * n * s.m * 4);                 // dchi
-    t += al(BH * n * s.Dv * 4);                // dvin
-    t += al(BH * nch * win * s.Dv * 4);        // du32
-    t += al(BH * nch * win * s.D * 4);         // dr32
-    t += al(BH * n * 4 * 4);                   // rowstat
+    // du32, dvin, dr32, dq32 (contiguous): [nfb][BH][n][Dv | Dv | D | D]
+    t += al(nfb * BH * n * (2 * (size_t)s.Dv + 2 * (size_t)s.D) * 4);
+    t += al(BH * n * 2 * 4);                   // rowstat
   }
   return t;
 }
@@ -55,13 +54,16 @@ void carve(const Shape& s, void* base, bool backward, Workspace* ws) {
   ws->rex = (float*)p; p += al(BH * (nch + 1) * 4);
   if (s.m > 128) { ws->part = (float*)p; p += al((size_t)(s.m / 128) * BH * s.n * (s.Dv + 2) * 4); }
   if (backward) {
-    const size_t n = (size_t)s.n, win = kChunk + 64 - 1;
+    const size_t n = (size_t)s.n, nfb = s.m > 128 ? (size_t)s.m / 128 : 1;
     ws->gstates = (float*)p; p += al(BH * nch * S * 4);
     ws->dchi = (float*)p; p += al(BH * n * s.m * 4);
-    ws->dvin = (float*)p; p += al(BH * n * s.Dv * 4);
-    ws->du32 = (float*)p; p += al(BH * nch * win * s.Dv * 4);
-    ws->dr32 = (float*)p; p += al(BH * nch * win * s.D * 4);
-    ws->rowstat = (float*)p; p += al(BH * n * 4 * 4);
+    float* acc = (float*)p;
+    p += al(nfb * BH * n * (2 * (size_t)s.Dv + 2 * (size_t)s.D) * 4);
+    ws->du32 = acc;
+    ws->dvin = ws->du32 + nfb * BH * n * s.Dv;
+    ws->dr32 = ws->dvin + nfb * BH * n * s.Dv;
+    ws->dq32 = ws->dr32 + nfb * BH * n * s.D;
+    ws->rowstat = (float*)p; p += al(BH * n * 2 * 4);
   }
 }
 

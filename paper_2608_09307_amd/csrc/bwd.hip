@@ -1,13 +1,1273 @@
-// LinSimp backward on gfx950 (query sweep, state sweep, key side).
+// LinSimp backward on gfx950: exact gradient of sum_i dO_i . out_i with the
+// stabilising shifts held constant (they cancel in the ratio, App. B.2).
+//
+// Per row i (log2 frames as in the forward; psi = 2^(ell - L_i), the query
+// feature without 1/sqrt(m); M^(i), a^(i) the state of row i in frame R_i):
+//   dN = g / (Z + eps),  dZ = -(g . out) / (Z + eps)
+//   per anchor c:  dA_c = dN (*) u_c,  du_c += dN (*) A_c,  A_c = psi_c^T M^(i)
+//                  dpsi_c = M^(i) dA_c + dZ a^(i)
+//                  dell_c = dpsi_c (*) psi_c            (natural-log derivative)
+//                  dz_c = Omega^T dell_c - (sum_p dell_cp) z_c    (d ell/d z = omega - z, App. C)
+//                  dq_i += dz_c (*) r_c,  dr_c += dz_c (*) q_i
+//   state:         dM^(i) = sum_c psi_c dA_c^T,  da^(i) = dZ sum_c psi_c
+// M^(i) = sb_i M_b + sum_{j in chunk, j<=i} 2^(R_j-R_i) chi_j v_j^T, so the state
+// gradient splits into the chunk boundary (GB_b = sum_i sb_i dM^(i), carried to
+// earlier chunks by a reverse scan: App. C "Backward state sweep") and the
+// intra-chunk tail (dchi_j, dv_j from rows j <= i of the same chunk).  The key
+// feature map is then differentiated: dlambda = dchi (*) chi,
+// dk = Omega^T dlambda - (sum_p dlambda_p) k.
+//
+// Kernels:
+//   k_bwd_prep     row scalars (1/(Z+eps), dZ) and zeroed accumulators
+//   k_bwd_du       query sweep 1: du (anchor side) and the intra-chunk dv
+//   k_bwd_dqdr     query sweep 2: dq (row side) and dr (anchor side)
+//   k_bwd_state    state sweep: GB_b, gb_b and the intra-chunk dchi (matrix cores,
+//                  contraction over (row, anchor) pairs)
+//   k_bwd_revscan  reverse exclusive scan of (GB, gb) with the frame monoid
+//   k_bwd_keys     key side: dk, dv
+//   k_bwd_final    float32 accumulators -> output dtype
+// The query sweeps walk a segment of rows in order, keeping the anchor-side
+// accumulators in an LDS ring that slides with the window: an anchor is written
+// once it has seen all of its rows; only anchors at segment edges use atomics.
 #include "common.h"
+#include "keyfeat.h"
 #include "linsimp_internal.h"
 
 namespace linsimp {
 
-int launch_backward(const Shape& s, const void*, const void*, const void*, const void*,
-                    const void*, const float*, const void*, const float*, const void*, void*,
-                    void*, void*, void*, void*, const Workspace&, hipStream_t) {
-  set_error("backward not built for dtype=%d D=%d m=%d", s.dtype, s.D, s.m);
+struct BwdArgs {
+  const void *q, *k, *v, *r, *u;
+  const float* omega;
+  const void* out;
+  const float* stats;
+  const void* dout;
+  void *dq, *dk, *dv, *dr, *du;
+  const void* omq;
+  const void* omk;
+  const float* states;
+  const float* rex;
+  float* gst;       // [BH][nch][M*DV + M]  GB_b, then Ghat_b
+  float* dchi;      // [BH][n][M]           intra-chunk key-feature gradient
+  float* dvin;      // [NFB][BH][n][DV]     intra-chunk value gradient
+  float* du32;      // [NFB][BH][n][DV]
+  float* dr32;      // [NFB][BH][n][D]
+  float* dq32;      // [NFB][BH][n][D]
+  float* rowstat;   // [BH][n][2]: 1/(Z+eps), dZ
+  int H, n, w, nch, BH, seg_steps;
+  float eps;
+};
+
+static constexpr float kLn2 = 0.6931471805599453f;
+
+// ---------------------------------------------------------------------------
+// prep: row scalars and zeroed float32 accumulators
+// ---------------------------------------------------------------------------
+template <typename T, int DV>
+__global__ __launch_bounds__(256) void k_bwd_rowprep(BwdArgs a) {
+  const size_t rows = (size_t)a.BH * a.n;
+  const size_t row = (size_t)blockIdx.x * 8 + (threadIdx.x >> 5);
+  const int lane = threadIdx.x & 31;
+  if (row >= rows) return;
+  const T* g = (const T*)a.dout + row * DV;
+  const T* o = (const T*)a.out + row * DV;
+  float s = 0.0f;
+  for (int d = lane; d < DV; d += 32) s += tof(g[d]) * tof(o[d]);
+#pragma unroll
+  for (int off = 16; off >= 1; off >>= 1) s += __shfl_xor(s, off, 32);
+  const float inv = 1.0f / (a.stats[row * 2 + 1] + a.eps);
+  if (lane == 0) {
+    a.rowstat[row * 2 + 0] = inv;
+    a.rowstat[row * 2 + 1] = -s * inv;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_fill_zero(float* p, size_t n4) {
+  size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n4) ((f32x4*)p)[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// ---------------------------------------------------------------------------
+// Query sweeps
+// ---------------------------------------------------------------------------
+template <typename T, int D, int DV, int M, int NA>
+struct QCfg {
+  static constexpr int PAD = MF<T>::PAD;
+  static constexpr int NW = 4;                       // waves
+  static constexpr int BS = 16;                      // rows per step
+  static constexpr int RPW = BS / NW;                // rows per wave per step
+  static constexpr int FB = M < 128 ? M : 128;       // feature block
+  static constexpr int NFB = M / FB;
+  static constexpr int RING = 16 * ((32 * NA - 1 + BS + 15) / 16);   // anchor ring rows (>= window)
+  static constexpr int DVA = DV + 16;                // augmented width (column DV)
+  static constexpr int ES = sizeof(T);
+  static constexpr int a16(int x) { return (x + 15) & ~15; }
+};
+
+// Shared per-step state loading: the chunk's key features, values and boundary
+// state (only when the step starts a chunk), then the newest BS anchor rows.
+// ---------------------------------------------------------------------------
+// k_bwd_du: du_c = sum_i dN_i (*) A_ic and the intra-chunk value gradient
+//   dv_j += sum_{(i,c): j<=i} 2^(R_j-R_i) (psi_ic . chi_j) dA_ic
+// ---------------------------------------------------------------------------
+template <typename T, int D, int DV, int M, int NA>
+struct DuCfg : QCfg<T, D, DV, M, NA> {
+  using Q = QCfg<T, D, DV, M, NA>;
+  static constexpr int oOm = 0;
+  static constexpr int oMp = oOm + Q::a16(Q::FB * (D + Q::PAD) * Q::ES);
+  static constexpr int oA = oMp + Q::a16(Q::FB * (DV + Q::PAD) * Q::ES);
+  static constexpr int oChi = oA + Q::a16(Q::FB * 4);
+  static constexpr int oV = oChi + Q::a16(32 * (Q::FB + Q::PAD) * Q::ES);
+  static constexpr int szV = Q::a16(32 * (DV + Q::PAD) * Q::ES);
+  // chi + V double as the scratch that reduces the waves' intra-chunk dv
+  static constexpr int oU = (oV + szV > oChi + 32 * DV * 4) ? oV + szV : oChi + 32 * DV * 4;
+  static constexpr int oRj = oU + Q::a16(Q::RING * (DV + Q::PAD) * Q::ES);
+  static constexpr int oWin = oRj + Q::a16(32 * 4);
+  static constexpr int BYTES = oWin + Q::a16(Q::RING * DV * 4);
+};
+
+template <typename T, int D, int DV, int M, int NA>
+__global__ __launch_bounds__(256) void k_bwd_du(BwdArgs a) {
+  using F = MF<T>;
+  using C = DuCfg<T, D, DV, M, NA>;
+  constexpr int PAD = C::PAD, FB = C::FB, RING = C::RING, NW = C::NW, BS = C::BS;
+  static_assert(C::BYTES <= 160 * 1024, "du LDS budget");
+  __shared__ __align__(16) char smem[C::BYTES];
+  T* sOm = (T*)(smem + C::oOm);
+  T* sMp = (T*)(smem + C::oMp);
+  float* sA = (float*)(smem + C::oA);
+  T* sChi = (T*)(smem + C::oChi);
+  T* sV = (T*)(smem + C::oV);
+  T* sU = (T*)(smem + C::oU);
+  float* sRj = (float*)(smem + C::oRj);
+  float* sWin = (float*)(smem + C::oWin);
+  float* sRed = (float*)(smem + C::oChi);     // reused at chunk ends (dv reduction)
+
+  const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
+  const int bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
+  const int nsteps_tot = (n + BS - 1) / BS;
+  const int st0 = blockIdx.x * a.seg_steps;
+  const int st1 = min(nsteps_tot, st0 + a.seg_steps);
+  if (st0 >= st1) return;
+  const int S0 = st0 * BS, S1 = min(n, st1 * BS);      // segment rows [S0, S1)
+  constexpr int S = M * DV + M;
+  const size_t seq = (size_t)bh * n;
+  const T* qs = (const T*)a.q + seq * D;
+  const T* ks = (const T*)a.k + seq * D;
+  const T* vs = (const T*)a.v + seq * DV;
+  const T* rs_ = (const T*)a.r + seq * D;
+  const T* us = (const T*)a.u + seq * DV;
+  const T* gs = (const T*)a.dout + seq * DV;
+  const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
+  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
+  const float* rx = a.rex + (size_t)bh * (nch + 1);
+  float* du32 = a.du32 + ((size_t)fb * a.BH + bh) * n * DV;
+  float* dvin = a.dvin + ((size_t)fb * a.BH + bh) * n * DV;
+  const int w = a.w;
+  auto ringrow = [&](int c) { return ((c % RING) + RING) % RING; };
+
+  // Omega block (resident for the whole segment)
+  copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, 256);
+  // anchor ring: rows S0 - (32NA-1) .. S0-1 (the first step adds its own rows)
+  for (int idx = tid; idx < RING * DV; idx += 256) sWin[idx] = 0.0f;
+  for (int idx = tid; idx < (32 * NA - 1) * (DV / 4); idx += 256) {
+    int rr = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
+    int c = S0 - (32 * NA - 1) + rr;
+    T* dst = sU + ringrow(c) * (DV + PAD) + d0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) dst[e] = (c >= 0 && c < n) ? us[(size_t)c * DV + d0 + e] : (T)0.0f;
+  }
+
+  f32x16 dvacc[DV / 32];
+#pragma unroll
+  for (int dt = 0; dt < DV / 32; ++dt) dvacc[dt] = zero16();
+
+  for (int st = st0; st < st1; ++st) {
+    const int i0 = st * BS;
+    const int cb = i0 / 32;
+    const int s0 = cb * 32;
+    const bool chunk_start = (i0 == s0) || (st == st0);
+    const float Rexb = rx[cb];
+    const bool has_bnd = cb > 0;
+    __syncthreads();
+    // flush anchors that left the window: c in [i0 - RING, i0 - RING + BS)
+    for (int idx = tid; idx < BS * DV; idx += 256) {
+      int rr = idx / DV, d = idx % DV;
+      int c = i0 - RING + rr;
+      float* slot = sWin + ringrow(c) * DV + d;
+      if (c >= 0 && c < n && c >= S0 - (32 * NA - 1)) {
+        float x = *slot;
+        bool edge = (c < S0) || (c + w - 1 >= S1 && S1 < n);
+        if (edge) atomicAdd(du32 + (size_t)c * DV + d, x);
+        else du32[(size_t)c * DV + d] = x;
+      }
+      *slot = 0.0f;
+    }
+    // newest anchor rows [i0, i0 + BS)
+    for (int idx = tid; idx < BS * (DV / 4); idx += 256) {
+      int rr = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
+      int c = i0 + rr;
+      T* dst = sU + ringrow(c) * (DV + PAD) + d0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dst[e] = (c < n) ? us[(size_t)c * DV + d0 + e] : (T)0.0f;
+    }
+    if (chunk_start) {
+      if (st != st0) {
+        // chunk end: reduce the waves' intra-chunk dv over LDS, then write it
+        const int pcb = (i0 - 1) / 32;
+        for (int idx = tid; idx < 32 * DV; idx += 256) sRed[idx] = 0.0f;
+        __syncthreads();
+        for (int ww = 0; ww < NW; ++ww) {
+          if (wv == ww) {
+#pragma unroll
+            for (int dt = 0; dt < DV / 32; ++dt)
+#pragma unroll
+              for (int v = 0; v < 16; ++v) sRed[crow(v, h) * DV + dt * 32 + col] += dvacc[dt][v];
+          }
+          __syncthreads();
+        }
+        for (int idx = tid; idx < 32 * DV; idx += 256) {
+          int j = pcb * 32 + idx / DV;
+          if (j < n) atomicAdd(dvin + (size_t)j * DV + idx % DV, sRed[idx]);
+        }
+#pragma unroll
+        for (int dt = 0; dt < DV / 32; ++dt) dvacc[dt] = zero16();
+        __syncthreads();
+      }
+      if (wv == 0) chunk_key_features<T, D, M>(ks, s0, n, omk_h, Rexb, sChi, FB + PAD, sRj, fb * FB, fb * FB + FB);
+      const float* bst = a.states + ((size_t)bh * nch + cb) * S;
+      for (int idx = tid; idx < FB * (DV / 4); idx += 256) {
+        int p = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
+        f32x4 x = has_bnd ? *(const f32x4*)(bst + (size_t)(fb * FB + p) * DV + d0) : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sMp[p * (DV + PAD) + d0 + e] = (T)x[e];
+      }
+      for (int p = tid; p < FB; p += 256) sA[p] = has_bnd ? bst[(size_t)M * DV + fb * FB + p] : 0.0f;
+      copy_rows<T>(sV, DV + PAD, vs, DV, 32, DV, s0, 0, n, tid, 256);
+    }
+    __syncthreads();
+
+#pragma unroll 1
+    for (int rr = 0; rr < C::RPW; ++rr) {
+      const int t = (i0 - s0) + wv + NW * rr;      // row within the chunk
+      const int i = s0 + t;
+      if (i >= n) continue;
+      const float Li = uniform(a.stats[(seq + i) * 2]);
+      const float inv = uniform(a.rowstat[(seq + i) * 2]);
+      const float Ri = uniform(sRj[t]);
+      const float sb = uniform(has_bnd ? fast_exp2(Rexb - Ri) : 0.0f);
+      float sj[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int j = crow(v, h);
+        sj[v] = (j <= t) ? fast_exp2(sRj[j] - Ri) : 0.0f;
+      }
+      const float sjl = (col <= t) ? fast_exp2(sRj[col] - Ri) : 0.0f;
+      float dN[DV / 32];
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt) dN[dt] = tof(gs[(size_t)i * DV + dt * 32 + col]) * inv;
+      const T* qrow = qs + (size_t)i * D;
+#pragma unroll 1
+      for (int an = 0; an < NA; ++an) {
+        no_hoist();
+        const int c = i - 32 * an - col;
+        const bool valid = (32 * an + col < w) && (c >= 0);
+        const T* rrow = rs_ + (size_t)(valid ? c : 0) * D;
+        f32x16 accL[FB / 32];
+#pragma unroll
+        for (int pt = 0; pt < FB / 32; ++pt) accL[pt] = zero16();
+        float nz = 0.0f;
+#pragma unroll 2
+        for (int s = 0; s < D / F::KS; ++s) {
+          const int k0 = s * F::KS + h * F::KPL;
+          typename F::frag qf = F::ld(qrow, k0), rf = F::ld(rrow, k0), zf;
+          if constexpr (sizeof(T) == 2) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              float p = valid ? fel(qf, e) * fel(rf, e) : 0.0f;
+              nz += p * p;
+              zf[e] = (bf16)p;
+            }
+          } else {
+            float p = valid ? qf * rf : 0.0f;
+            nz += p * p;
+            zf = p;
+          }
+#pragma unroll
+          for (int pt = 0; pt < FB / 32; ++pt)
+            accL[pt] = F::mma(F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), zf, accL[pt]);
+        }
+        nz = half_swap_add(nz);
+        const float off = valid ? -0.5f * kLog2e * nz - Li : kNegInf;
+        typename F::frag pf[FB / 32][F::CSTEPS];
+#pragma unroll
+        for (int pt = 0; pt < FB / 32; ++pt) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) accL[pt][v] = fast_exp2(accL[pt][v] + off);
+#pragma unroll
+          for (int sp = 0; sp < F::CSTEPS; ++sp) pf[pt][sp] = F::cfrag(accL[pt], sp);
+        }
+        // P^T[j, c] (lanes <-> anchor) and P[c, j] (lanes <-> token j), masked and framed
+        f32x16 accP = zero16(), accPn = zero16();
+        const T* chirow = sChi + col * (FB + PAD);
+#pragma unroll
+        for (int pt = 0; pt < FB / 32; ++pt)
+#pragma unroll
+          for (int sp = 0; sp < F::CSTEPS; ++sp) {
+            typename F::frag cf = F::ldc(chirow, pt * 32, sp, h);
+            accP = F::mma(cf, pf[pt][sp], accP);
+            accPn = F::mma(pf[pt][sp], cf, accPn);
+          }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          accP[v] *= sj[v];
+          accPn[v] *= sjl;
+        }
+        typename F::frag ppf[F::CSTEPS], pnf[F::CSTEPS];
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp) {
+          ppf[sp] = F::cfrag(accP, sp);
+          pnf[sp] = F::cfrag(accPn, sp);
+        }
+        // ring row of anchor register index ar (anchor c = i - 32an - ar)
+        auto rmap = [&](int ar) { return ringrow(i - 32 * an - ar); };
+#pragma unroll 1
+        for (int dt = 0; dt < DV / 32; ++dt) {
+          no_hoist();
+          f32x16 accA = zero16();
+          if (has_bnd) {
+#pragma unroll
+            for (int pt = 0; pt < FB / 32; ++pt)
+#pragma unroll
+              for (int sp = 0; sp < F::CSTEPS; ++sp)
+                accA = F::mma(pf[pt][sp], F::tld_crow(sMp, DV + PAD, pt * 32, sp, dt * 32), accA);
+            if (sb != 1.0f) accA *= sb;
+          }
+#pragma unroll
+          for (int sp = 0; sp < F::CSTEPS; ++sp)
+            accA = F::mma(ppf[sp], F::tld_crow(sV, DV + PAD, 0, sp, dt * 32), accA);
+          // du_c[d] += dN[d] A[c, d]  (lanes <-> d, regs <-> anchor)
+          const float dn = dN[dt];
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int ar = crow(v, h);
+            if (32 * an + ar < w && i - 32 * an - ar >= 0)
+              atomicAdd(sWin + rmap(ar) * DV + dt * 32 + col, dn * accA[v]);
+          }
+          // intra-chunk dv: dvacc[j, d] += sum_c P[c, j] dA[c, d], dA = dN (*) u_c
+#pragma unroll
+          for (int sp = 0; sp < F::CSTEPS; ++sp) {
+            typename F::frag uf = F::tld_crow_map(sU, DV + PAD, sp, dt * 32, rmap), daf;
+            if constexpr (sizeof(T) == 2) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) daf[e] = (bf16)(fel(uf, e) * dn);
+            } else {
+              daf = uf * dn;
+            }
+            dvacc[dt] = F::mma(pnf[sp], daf, dvacc[dt]);
+          }
+        }
+      }
+    }
+  }
+  // ---- segment end: remaining anchors and the last chunk's intra dv ----
+  __syncthreads();
+  for (int idx = tid; idx < RING * DV; idx += 256) {
+    int rr = idx / DV, d = idx % DV;
+    int c = st1 * BS - RING + rr;
+    if (c >= 0 && c < n && c >= S0 - (32 * NA - 1) && c < S1) {
+      float x = sWin[ringrow(c) * DV + d];
+      bool edge = (c < S0) || (c + w - 1 >= S1 && S1 < n);
+      if (edge) atomicAdd(du32 + (size_t)c * DV + d, x);
+      else du32[(size_t)c * DV + d] = x;
+    }
+  }
+  __syncthreads();
+  {
+    const int pcb = (S1 - 1) / 32;
+    for (int idx = tid; idx < 32 * DV; idx += 256) sRed[idx] = 0.0f;
+    __syncthreads();
+    for (int ww = 0; ww < NW; ++ww) {
+      if (wv == ww) {
+#pragma unroll
+        for (int dt = 0; dt < DV / 32; ++dt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) sRed[crow(v, h) * DV + dt * 32 + col] += dvacc[dt][v];
+      }
+      __syncthreads();
+    }
+    for (int idx = tid; idx < 32 * DV; idx += 256) {
+      int j = pcb * 32 + idx / DV;
+      if (j < n) atomicAdd(dvin + (size_t)j * DV + idx % DV, sRed[idx]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// k_bwd_dqdr: dq (row side, complete per row) and dr (anchor side, ring)
+// ---------------------------------------------------------------------------
+template <typename T, int D, int DV, int M, int NA>
+struct DqCfg : QCfg<T, D, DV, M, NA> {
+  using Q = QCfg<T, D, DV, M, NA>;
+  static constexpr int oOm = 0;
+  static constexpr int oMp = oOm + Q::a16(Q::FB * (D + Q::PAD) * Q::ES);
+  static constexpr int oChi = oMp + Q::a16(Q::FB * (Q::DVA + Q::PAD) * Q::ES);
+  static constexpr int oV = oChi + Q::a16(32 * (Q::FB + Q::PAD) * Q::ES);
+  static constexpr int oR = oV + Q::a16(32 * (Q::DVA + Q::PAD) * Q::ES);
+  static constexpr int oRj = oR + Q::a16(Q::RING * (D + Q::PAD) * Q::ES);
+  static constexpr int oScr = oRj + Q::a16(32 * 4);
+  static constexpr int SCR = Q::DVA + 32;                 // per wave: dN/dZ (DVA) + s_c (32)
+  static constexpr int oWin = oScr + Q::a16(Q::NW * SCR * 4);
+  static constexpr int BYTES = oWin + Q::a16(Q::RING * D * 4);
+};
+
+template <typename T, int D, int DV, int M, int NA>
+__global__ __launch_bounds__(256) void k_bwd_dqdr(BwdArgs a) {
+  using F = MF<T>;
+  using C = DqCfg<T, D, DV, M, NA>;
+  constexpr int PAD = C::PAD, FB = C::FB, RING = C::RING, NW = C::NW, BS = C::BS, DVA = C::DVA;
+  static_assert(C::BYTES <= 160 * 1024, "dqdr LDS budget");
+  __shared__ __align__(16) char smem[C::BYTES];
+  T* sOm = (T*)(smem + C::oOm);
+  T* sMp = (T*)(smem + C::oMp);
+  T* sChi = (T*)(smem + C::oChi);
+  T* sV = (T*)(smem + C::oV);
+  T* sR = (T*)(smem + C::oR);
+  float* sRj = (float*)(smem + C::oRj);
+  float* sWin = (float*)(smem + C::oWin);
+
+  const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
+  float* sScr = (float*)(smem + C::oScr) + wv * C::SCR;
+  const int bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
+  const int nsteps_tot = (n + BS - 1) / BS;
+  const int st0 = blockIdx.x * a.seg_steps;
+  const int st1 = min(nsteps_tot, st0 + a.seg_steps);
+  if (st0 >= st1) return;
+  const int S0 = st0 * BS, S1 = min(n, st1 * BS);
+  constexpr int S = M * DV + M;
+  const size_t seq = (size_t)bh * n;
+  const T* qs = (const T*)a.q + seq * D;
+  const T* ks = (const T*)a.k + seq * D;
+  const T* vs = (const T*)a.v + seq * DV;
+  const T* rs_ = (const T*)a.r + seq * D;
+  const T* us = (const T*)a.u + seq * DV;
+  const T* gs = (const T*)a.dout + seq * DV;
+  const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
+  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
+  const float* rx = a.rex + (size_t)bh * (nch + 1);
+  float* dr32 = a.dr32 + ((size_t)fb * a.BH + bh) * n * D;
+  float* dq32 = a.dq32 + ((size_t)fb * a.BH + bh) * n * D;
+  const int w = a.w;
+  auto ringrow = [&](int c) { return ((c % RING) + RING) % RING; };
+
+  copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, 256);
+  for (int idx = tid; idx < RING * D; idx += 256) sWin[idx] = 0.0f;
+  for (int idx = tid; idx < (32 * NA - 1) * (D / 4); idx += 256) {
+    int rr = idx / (D / 4), d0 = (idx % (D / 4)) * 4;
+    int c = S0 - (32 * NA - 1) + rr;
+    T* dst = sR + ringrow(c) * (D + PAD) + d0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) dst[e] = (c >= 0 && c < n) ? rs_[(size_t)c * D + d0 + e] : (T)0.0f;
+  }
+
+  for (int st = st0; st < st1; ++st) {
+    const int i0 = st * BS;
+    const int cb = i0 / 32;
+    const int s0 = cb * 32;
+    const bool chunk_start = (i0 == s0) || (st == st0);
+    const float Rexb = rx[cb];
+    const bool has_bnd = cb > 0;
+    __syncthreads();
+    for (int idx = tid; idx < BS * D; idx += 256) {
+      int rr = idx / D, d = idx % D;
+      int c = i0 - RING + rr;
+      float* slot = sWin + ringrow(c) * D + d;
+      if (c >= 0 && c < n && c >= S0 - (32 * NA - 1)) {
+        float x = *slot;
+        bool edge = (c < S0) || (c + w - 1 >= S1 && S1 < n);
+        if (edge) atomicAdd(dr32 + (size_t)c * D + d, x);
+        else dr32[(size_t)c * D + d] = x;
+      }
+      *slot = 0.0f;
+    }
+    for (int idx = tid; idx < BS * (D / 4); idx += 256) {
+      int rr = idx / (D / 4), d0 = (idx % (D / 4)) * 4;
+      int c = i0 + rr;
+      T* dst = sR + ringrow(c) * (D + PAD) + d0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dst[e] = (c < n) ? rs_[(size_t)c * D + d0 + e] : (T)0.0f;
+    }
+    if (chunk_start) {
+      if (wv == 0) chunk_key_features<T, D, M>(ks, s0, n, omk_h, Rexb, sChi, FB + PAD, sRj, fb * FB, fb * FB + FB);
+      const float* bst = a.states + ((size_t)bh * nch + cb) * S;
+      // boundary M with column DV = boundary a (augmented), zero-padded to DVA
+      for (int idx = tid; idx < FB * (DVA / 4); idx += 256) {
+        int p = idx / (DVA / 4), d0 = (idx % (DVA / 4)) * 4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          int d = d0 + e;
+          float x = 0.0f;
+          if (has_bnd) {
+            if (d < DV) x = bst[(size_t)(fb * FB + p) * DV + d];
+            else if (d == DV) x = bst[(size_t)M * DV + fb * FB + p];
+          }
+          sMp[p * (DVA + PAD) + d] = (T)x;
+        }
+      }
+      // values with column DV = 1 (so the contraction with dA also carries dZ)
+      for (int idx = tid; idx < 32 * (DVA / 4); idx += 256) {
+        int j = idx / (DVA / 4), d0 = (idx % (DVA / 4)) * 4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          int d = d0 + e;
+          T x = (T)0.0f;
+          if (s0 + j < n) x = (d < DV) ? vs[(size_t)(s0 + j) * DV + d] : (d == DV ? (T)1.0f : (T)0.0f);
+          sV[j * (DVA + PAD) + d] = x;
+        }
+      }
+    }
+    __syncthreads();
+
+#pragma unroll 1
+    for (int rr = 0; rr < C::RPW; ++rr) {
+      const int t = (i0 - s0) + wv + NW * rr;
+      const int i = s0 + t;
+      if (i >= n) continue;
+      const float Li = uniform(a.stats[(seq + i) * 2]);
+      const float inv = uniform(a.rowstat[(seq + i) * 2]);
+      const float dZ = uniform(a.rowstat[(seq + i) * 2 + 1]);
+      const float Ri = uniform(sRj[t]);
+      const float sb = uniform(has_bnd ? fast_exp2(Rexb - Ri) : 0.0f);
+      float sj[16];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int j = crow(v, h);
+        sj[v] = (j <= t) ? fast_exp2(sRj[j] - Ri) : 0.0f;
+      }
+      // per-wave scratch: dN (with dZ at column DV) as floats
+      for (int d = l; d < DVA; d += 64)
+        sScr[d] = (d < DV) ? tof(gs[(size_t)i * DV + d]) * inv : (d == DV ? dZ : 0.0f);
+      wave_lds_sync();
+      const T* qrow = qs + (size_t)i * D;
+      float qD[D / 32];
+#pragma unroll
+      for (int Dt = 0; Dt < D / 32; ++Dt) qD[Dt] = tof(qrow[Dt * 32 + col]);
+      float dqacc[D / 32];
+#pragma unroll
+      for (int Dt = 0; Dt < D / 32; ++Dt) dqacc[Dt] = 0.0f;
+#pragma unroll 1
+      for (int an = 0; an < NA; ++an) {
+        no_hoist();
+        const int c = i - 32 * an - col;
+        const bool valid = (32 * an + col < w) && (c >= 0);
+        const T* rrow = sR + ringrow(c) * (D + PAD);
+        f32x16 accL[FB / 32];
+#pragma unroll
+        for (int pt = 0; pt < FB / 32; ++pt) accL[pt] = zero16();
+        float nz = 0.0f;
+#pragma unroll 2
+        for (int s = 0; s < D / F::KS; ++s) {
+          const int k0 = s * F::KS + h * F::KPL;
+          typename F::frag qf = F::ld(qrow, k0), rf = F::ld(rrow, k0), zf;
+          if constexpr (sizeof(T) == 2) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              float p = valid ? fel(qf, e) * fel(rf, e) : 0.0f;
+              nz += p * p;
+              zf[e] = (bf16)p;
+            }
+          } else {
+            float p = valid ? qf * rf : 0.0f;
+            nz += p * p;
+            zf = p;
+          }
+#pragma unroll
+          for (int pt = 0; pt < FB / 32; ++pt)
+            accL[pt] = F::mma(F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), zf, accL[pt]);
+        }
+        nz = half_swap_add(nz);
+        const float off = valid ? -0.5f * kLog2e * nz - Li : kNegInf;
+#pragma unroll
+        for (int pt = 0; pt < FB / 32; ++pt)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) accL[pt][v] = fast_exp2(accL[pt][v] + off);
+        // dA^T fragments (lanes <-> anchor, natural d order, column DV carries dZ)
+        const T* urow = us + (size_t)(valid ? c : 0) * DV;
+        typename F::frag daf[DVA / F::KS];
+#pragma unroll
+        for (int s = 0; s < DVA / F::KS; ++s) {
+          const int k0 = s * F::KS + h * F::KPL;
+          if constexpr (sizeof(T) == 2) {
+            bf16x8 uf = (k0 < DV && valid) ? F::ld(urow, k0) : F::zero();
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              float uu = (k0 + e < DV) ? fel(uf, e) : (k0 + e == DV && valid ? 1.0f : 0.0f);
+              daf[s][e] = (bf16)(uu * sScr[k0 + e]);
+            }
+          } else {
+            float uu = (k0 < DV) ? (valid ? urow[k0] : 0.0f) : (k0 == DV && valid ? 1.0f : 0.0f);
+            daf[s] = uu * sScr[k0];
+          }
+        }
+        // Q^T[j, c] = v_j . dA_c + dZ   (lanes <-> anchor, regs <-> j), framed and masked
+        f32x16 accQ = zero16();
+#pragma unroll
+        for (int s = 0; s < DVA / F::KS; ++s)
+          accQ = F::mma(F::ld(sV + col * (DVA + PAD), s * F::KS + h * F::KPL), daf[s], accQ);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) accQ[v] *= sj[v];
+        typename F::frag qqf[F::CSTEPS];
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp) qqf[sp] = F::cfrag(accQ, sp);
+        // dpsi^T[p, c] = sb * (M_b | a_b)[p, :] dA^T + chi^T Q^T ; dell = dpsi * psi
+        typename F::frag dlf[FB / 32][F::CSTEPS];
+        float sc = 0.0f;
+#pragma unroll 1
+        for (int pt = 0; pt < FB / 32; ++pt) {
+          no_hoist();
+          f32x16 dps = zero16();
+          if (has_bnd) {
+#pragma unroll
+            for (int s = 0; s < DVA / F::KS; ++s)
+              dps = F::mma(F::ld(sMp + (pt * 32 + col) * (DVA + PAD), s * F::KS + h * F::KPL), daf[s], dps);
+            dps *= sb;
+          }
+          // tail: rows p of chi^T with k = token j in crow order (chi stored [j][sigma(p)])
+#pragma unroll
+          for (int sp = 0; sp < F::CSTEPS; ++sp) {
+            typename F::frag cf;
+            if constexpr (sizeof(T) == 2) {
+              const int L = l, g = L >> 4, s4 = L & 15;
+              const int pcol = F::sigma(pt * 32 + 16 * (g & 1) + 4 * (s4 & 3));
+              bf16x4 x0 = lds_tr4(sChi + (16 * sp + 4 * h + (s4 >> 2)) * (FB + PAD) + pcol);
+              bf16x4 x1 = lds_tr4(sChi + (16 * sp + 8 + 4 * h + (s4 >> 2)) * (FB + PAD) + pcol);
+              cf = cat44(x0, x1);
+            } else {
+              cf = sChi[crow(sp, h) * (FB + PAD) + pt * 32 + col];
+            }
+            dps = F::mma(cf, qqf[sp], dps);
+          }
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            float dl = dps[v] * accL[pt][v];
+            sc += dl;
+            dps[v] = dl * kLn2;      // paired with Omega * log2(e) below
+          }
+#pragma unroll
+          for (int sp = 0; sp < F::CSTEPS; ++sp) dlf[pt][sp] = F::cfrag(dps, sp);
+        }
+        sc = half_swap_add(sc);                      // sum_p dell_cp for anchor col
+        if (h == 0) sScr[DVA + col] = valid ? sc : 0.0f;
+        wave_lds_sync();
+        // dz[c, D] = Omega^T dell_c - s_c z_c  (lanes <-> D, regs <-> anchor)
+        auto rmap = [&](int ar) { return ringrow(i - 32 * an - ar); };
+#pragma unroll 1
+        for (int Dt = 0; Dt < D / 32; ++Dt) {
+          no_hoist();
+          f32x16 dz = zero16();
+#pragma unroll
+          for (int pt = 0; pt < FB / 32; ++pt)
+#pragma unroll
+            for (int sp = 0; sp < F::CSTEPS; ++sp)
+              dz = F::mma(dlf[pt][sp], F::tld_crow(sOm, D + PAD, pt * 32, sp, Dt * 32), dz);
+          // r[c][D] for the registers' anchors, via the same transposed read
+          float rv[16];
+#pragma unroll
+          for (int sp = 0; sp < F::CSTEPS; ++sp) {
+            typename F::frag rf = F::tld_crow_map(sR, D + PAD, sp, Dt * 32, rmap);
+            if constexpr (sizeof(T) == 2) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) rv[8 * sp + e] = fel(rf, e);
+            } else {
+              rv[sp] = rf;
+            }
+          }
+          const float qd = qD[Dt];
+          const float* sch = sScr + DVA + 4 * h;
+          float dqs = 0.0f;
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const f32x4 s4 = *(const f32x4*)(sch + 8 * g);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int v = 4 * g + e;
+              const int ar = 8 * g + 4 * h + e;
+              float dzz = dz[v] - s4[e] * qd * rv[v];
+              dqs += dzz * rv[v];
+              if (32 * an + ar < w && i - 32 * an - ar >= 0)
+                atomicAdd(sWin + rmap(ar) * D + Dt * 32 + col, dzz * qd);
+            }
+          }
+          dqacc[Dt] += dqs;
+        }
+      }
+#pragma unroll
+      for (int Dt = 0; Dt < D / 32; ++Dt) {
+        float dq = half_swap_add(dqacc[Dt]);
+        if (h == 0) dq32[(size_t)i * D + Dt * 32 + col] = dq;
+      }
+    }
+  }
+  __syncthreads();
+  for (int idx = tid; idx < RING * D; idx += 256) {
+    int rr = idx / D, d = idx % D;
+    int c = st1 * BS - RING + rr;
+    if (c >= 0 && c < n && c >= S0 - (32 * NA - 1) && c < S1) {
+      float x = sWin[ringrow(c) * D + d];
+      bool edge = (c < S0) || (c + w - 1 >= S1 && S1 < n);
+      if (edge) atomicAdd(dr32 + (size_t)c * D + d, x);
+      else dr32[(size_t)c * D + d] = x;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// k_bwd_state: per chunk and feature tile (one wave per 32 features):
+//   GB[p, d]   = sum_(i,c) sb_i psi_icp dA_ic[d]          (boundary gradient)
+//   gb[p]      = sum_(i,c) sb_i psi_icp dZ_i
+//   dchi[p, j] = sum_(i,c), j<=i  2^(R_j-R_i) psi_icp (v_j . dA_ic + dZ_i)
+// The contraction runs over (row, anchor) pairs, so psi is formed with the
+// pair index in registers (lanes <-> feature p).
+// ---------------------------------------------------------------------------
+template <typename T, int D, int DV, int M, int NA>
+struct StCfg {
+  static constexpr int PAD = MF<T>::PAD;
+  static constexpr int FB = M < 128 ? M : 128;
+  static constexpr int NFB = M / FB;
+  static constexpr int NW = FB / 32;
+  static constexpr int WIN = 32 + 32 * NA - 1;
+  static constexpr int DVA = DV + 16;
+  static constexpr int ES = sizeof(T);
+  static constexpr int a16(int x) { return (x + 15) & ~15; }
+  static constexpr int oOm = 0;
+  static constexpr int oR = oOm + a16(FB * (D + PAD) * ES);
+  static constexpr int oU = oR + a16(WIN * (D + PAD) * ES);
+  static constexpr int oV = oU + a16(WIN * (DV + PAD) * ES);
+  static constexpr int oQ = oV + a16(32 * (DVA + PAD) * ES);
+  static constexpr int oRow = oQ + a16(32 * (D + PAD) * ES);
+  static constexpr int oDN = oRow + a16(32 * 8 * 4);
+  static constexpr int oBias = oDN + a16(DVA * 4);
+  static constexpr int BYTES = oBias + a16(NW * 32 * 4);
+};
+
+template <typename T, int D, int DV, int M, int NA>
+__global__ __launch_bounds__(256) void k_bwd_state(BwdArgs a) {
+  using F = MF<T>;
+  using C = StCfg<T, D, DV, M, NA>;
+  constexpr int PAD = C::PAD, FB = C::FB, WIN = C::WIN, NW = C::NW, DVA = C::DVA;
+  constexpr int NT = 64 * NW;
+  static_assert(C::BYTES <= 160 * 1024, "state LDS budget");
+  __shared__ __align__(16) char smem[C::BYTES];
+  T* sOm = (T*)(smem + C::oOm);
+  T* sR = (T*)(smem + C::oR);
+  T* sU = (T*)(smem + C::oU);
+  T* sV = (T*)(smem + C::oV);
+  T* sQ = (T*)(smem + C::oQ);
+  float* sRow = (float*)(smem + C::oRow);      // per row t: L, inv, dZ, sb, R
+  float* sDN = (float*)(smem + C::oDN);        // dN of the current row (column DV = dZ)
+
+  const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
+  float* sBias = (float*)(smem + C::oBias) + wv * 32;
+  const int cb = blockIdx.x, bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
+  const int s0 = cb * 32;
+  const int wb = s0 - (32 * NA - 1);
+  const size_t seq = (size_t)bh * n;
+  const T* qs = (const T*)a.q + seq * D;
+  const T* ks = (const T*)a.k + seq * D;
+  const T* vs = (const T*)a.v + seq * DV;
+  const T* rs_ = (const T*)a.r + seq * D;
+  const T* us = (const T*)a.u + seq * DV;
+  const T* gs = (const T*)a.dout + seq * DV;
+  const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
+  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
+  const float Rexb = a.rex[(size_t)bh * (nch + 1) + cb];
+  const bool has_bnd = cb > 0;
+  const int w = a.w;
+
+  copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
+  copy_rows<T>(sR, D + PAD, rs_, D, WIN, D, wb, 0, n, tid, NT);
+  copy_rows<T>(sU, DV + PAD, us, DV, WIN, DV, wb, 0, n, tid, NT);
+  copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
+  for (int idx = tid; idx < 32 * (DVA / 4); idx += NT) {
+    int j = idx / (DVA / 4), d0 = (idx % (DVA / 4)) * 4;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      int d = d0 + e;
+      T x = (T)0.0f;
+      if (s0 + j < n) x = (d < DV) ? vs[(size_t)(s0 + j) * DV + d] : (d == DV ? (T)1.0f : (T)0.0f);
+      sV[j * (DVA + PAD) + d] = x;
+    }
+  }
+  // per-row scalars; the running key frame R_t of each row comes from the key map
+  if (wv == 0) {
+    f32x16 acc[M / 32];
+    float nk;
+    key_logits<T, D, M, true>(acc, nk, ks, s0, n, omk_h);
+    const bool vt = s0 + col < n;
+    float mx = kNegInf;
+#pragma unroll
+    for (int pt = 0; pt < M / 32; ++pt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, vt ? acc[pt][v] - 0.5f * kLog2e * nk : kNegInf);
+    mx = half_swap_max(mx);
+    float R = mx;
+#pragma unroll
+    for (int o = 1; o < 32; o <<= 1) {
+      float tt = __shfl_up(R, o, 32);
+      if (col >= o) R = fmaxf(R, tt);
+    }
+    R = fmaxf(R, Rexb);
+    if (h == 0) {
+      const int i = s0 + col;
+      float L = 0.f, inv = 0.f, dZ = 0.f;
+      if (i < n) {
+        L = a.stats[(seq + i) * 2];
+        inv = a.rowstat[(seq + i) * 2];
+        dZ = a.rowstat[(seq + i) * 2 + 1];
+      }
+      sRow[col * 8 + 0] = L;
+      sRow[col * 8 + 1] = inv;
+      sRow[col * 8 + 2] = dZ;
+      sRow[col * 8 + 3] = has_bnd ? fast_exp2(Rexb - R) : 0.0f;
+      sRow[col * 8 + 4] = R;
+    }
+  }
+  __syncthreads();
+
+  const int pt = wv;                 // this wave's feature tile within the block
+  f32x16 gB[DV / 32];
+#pragma unroll
+  for (int dt = 0; dt < DV / 32; ++dt) gB[dt] = zero16();
+  f32x16 dchi = zero16();
+  float gbacc = 0.0f;
+
+#pragma unroll 1
+  for (int t = 0; t < 32; ++t) {
+    const int i = s0 + t;
+    if (i >= n) break;
+    __syncthreads();
+    const float Li = uniform(sRow[t * 8 + 0]);
+    const float inv = uniform(sRow[t * 8 + 1]);
+    const float dZ = uniform(sRow[t * 8 + 2]);
+    const float sb = uniform(sRow[t * 8 + 3]);
+    const float Ri = uniform(sRow[t * 8 + 4]);
+    for (int d = tid; d < DVA; d += NT)
+      sDN[d] = (d < DV) ? tof(gs[(size_t)i * DV + d]) * inv : (d == DV ? dZ : 0.0f);
+    __syncthreads();
+    // frame ratio of token col (for the intra-chunk terms), zero beyond row i
+    const float sjl = (col <= t) ? fast_exp2(sRow[col * 8 + 4] - Ri) : 0.0f;
+    const T* qrow = sQ + t * (D + PAD);
+#pragma unroll 1
+    for (int an = 0; an < NA; ++an) {
+      no_hoist();
+      const int c = i - 32 * an - col;                 // anchor of pair lane col
+      const bool valid = (32 * an + col < w) && (c >= 0);
+      const int wi = c - wb;
+      const T* rrow = sR + wi * (D + PAD);
+      const T* urow = sU + wi * (DV + PAD);
+      // G1 with pairs as rows: L[pair, p], lanes <-> p, regs <-> pair
+      f32x16 acc = zero16();
+      float nz = 0.0f;
+#pragma unroll 2
+      for (int s = 0; s < D / F::KS; ++s) {
+        const int k0 = s * F::KS + h * F::KPL;
+        typename F::frag qf = F::ld(qrow, k0), rf = F::ld(rrow, k0), zf;
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            float p = valid ? fel(qf, e) * fel(rf, e) : 0.0f;
+            nz += p * p;
+            zf[e] = (bf16)p;
+          }
+        } else {
+          float p = valid ? qf * rf : 0.0f;
+          nz += p * p;
+          zf = p;
+        }
+        acc = F::mma(zf, F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), acc);
+      }
+      nz = half_swap_add(nz);
+      if (h == 0) sBias[col] = valid ? -0.5f * kLog2e * nz - Li : kNegInf;
+      wave_lds_sync();
+      // dA as an A operand (rows = pairs, natural d, column DV carries dZ)
+      typename F::frag daA[DVA / F::KS];
+#pragma unroll
+      for (int s = 0; s < DVA / F::KS; ++s) {
+        const int k0 = s * F::KS + h * F::KPL;
+        if constexpr (sizeof(T) == 2) {
+          bf16x8 uf = (k0 < DV && valid) ? F::ld(urow, k0) : F::zero();
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            float uu = (k0 + e < DV) ? fel(uf, e) : (k0 + e == DV && valid ? 1.0f : 0.0f);
+            daA[s][e] = (bf16)(uu * sDN[k0 + e]);
+          }
+        } else {
+          float uu = (k0 < DV) ? (valid ? urow[k0] : 0.0f) : (k0 == DV && valid ? 1.0f : 0.0f);
+          daA[s] = uu * sDN[k0];
+        }
+      }
+      // Q[pair, j] = dA_pair . v_j + dZ  (lanes <-> j, regs <-> pair)
+      f32x16 accQ = zero16();
+#pragma unroll
+      for (int s = 0; s < DVA / F::KS; ++s)
+        accQ = F::mma(daA[s], F::ld(sV + col * (DVA + PAD), s * F::KS + h * F::KPL), accQ);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) accQ[v] *= sjl;
+      // psi with the pair's bias (registers <-> pair)
+      const float* bh4 = sBias + 4 * h;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 b4 = *(const f32x4*)(bh4 + 8 * g);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[4 * g + e] = fast_exp2(acc[4 * g + e] + b4[e]);
+      }
+      float ps = 0.0f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) ps += acc[v];
+      gbacc += ps * (dZ * sb);
+      typename F::frag pf[F::CSTEPS];
+#pragma unroll
+      for (int sp = 0; sp < F::CSTEPS; ++sp) pf[sp] = F::cfrag(acc, sp);
+      // dchi[p, j] += psi^T Q
+#pragma unroll
+      for (int sp = 0; sp < F::CSTEPS; ++sp) dchi = F::mma(pf[sp], F::cfrag(accQ, sp), dchi);
+      // GB[p, d] += psi^T (sb dN (*) u): B operand rows = pairs (crow), via transposed reads
+      if (has_bnd) {
+        auto rmap = [&](int ar) { return (i - 32 * an - ar) - wb; };
+#pragma unroll 1
+        for (int dt = 0; dt < DV / 32; ++dt) {
+          no_hoist();
+          const float dn = sDN[dt * 32 + col] * sb;
+#pragma unroll
+          for (int sp = 0; sp < F::CSTEPS; ++sp) {
+            typename F::frag uf = F::tld_crow_map(sU, DV + PAD, sp, dt * 32, rmap), bf;
+            if constexpr (sizeof(T) == 2) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                // pairs whose anchor is invalid carry psi = 0; keep their operand finite
+                bf[e] = (bf16)(fel(uf, e) * dn);
+              }
+            } else {
+              bf = uf * dn;
+            }
+            gB[dt] = F::mma(pf[sp], bf, gB[dt]);
+          }
+        }
+      }
+    }
+  }
+  // ---- write GB (frame Rex_b), gb and the intra-chunk dchi ----
+  constexpr int S = M * DV + M;
+  float* g = a.gst + ((size_t)bh * nch + cb) * S;
+  const int p0 = fb * FB + pt * 32;
+#pragma unroll
+  for (int dt = 0; dt < DV / 32; ++dt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) g[(size_t)(p0 + crow(v, h)) * DV + dt * 32 + col] = gB[dt][v];
+  gbacc = half_swap_add(gbacc);
+  if (h == 0) g[(size_t)M * DV + p0 + col] = gbacc;
+  // dchi: lanes <-> token j (col), regs <-> p
+  if (s0 + col < n) {
+    float* dc = a.dchi + (seq + s0 + col) * M + p0;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) dc[crow(v, h)] = dchi[v];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// reverse exclusive scan:  Ghat_b = GB_{b+1} + 2^(Rex_{b+1} - Rex_{b+2}) Ghat_{b+1},
+// Ghat_{nch-1} = 0  (frame of Ghat_b: Rex_{b+1}, the running key max at the end
+// of chunk b).  In place, element-parallel, sequential over chunks.
+// ---------------------------------------------------------------------------
+template <int S>
+__global__ __launch_bounds__(256) void k_bwd_revscan(BwdArgs a) {
+  constexpr int PF = 8;
+  const int bh = blockIdx.y;
+  const int i4 = (blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i4 >= S) return;
+  const int nch = a.nch;
+  float* g = a.gst + (size_t)bh * nch * S;
+  const float* rx = a.rex + (size_t)bh * (nch + 1);
+  f32x4 run = {0.f, 0.f, 0.f, 0.f};
+  for (int b1 = nch - 1; b1 >= 0; b1 -= PF) {
+    f32x4 x[PF];
+#pragma unroll
+    for (int e = 0; e < PF; ++e) {
+      int b = b1 - e;
+      x[e] = (b >= 0) ? *(const f32x4*)(g + (size_t)b * S + i4) : run * 0.0f;
+    }
+#pragma unroll
+    for (int e = 0; e < PF; ++e) {
+      int b = b1 - e;
+      if (b < 0) break;
+      *(f32x4*)(g + (size_t)b * S + i4) = run;           // Ghat_b
+      const float f = fast_exp2(rx[b] - rx[b + 1]);       // 0 for b = 0 (Rex_0 = -inf)
+      run = x[e] + run * f;                               // Ghat_{b-1}
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// key side: per chunk (one wave), tokens j:
+//   dchi_j = 2^(R_j - Rex_{b+1}) (Ghat_b v_j + ghat_b) + dchi_intra_j
+//   dv_j   = 2^(R_j - Rex_{b+1}) Ghat_b^T chi_j + dv_intra_j
+//   dlambda = dchi (*) chi;  dk_j = Omega^T dlambda_j - (sum_p dlambda_jp) k_j
+// ---------------------------------------------------------------------------
+template <typename T, int D, int DV, int M>
+__global__ __launch_bounds__(256) void k_bwd_keys(BwdArgs a, int nfb) {
+  using F = MF<T>;
+  constexpr int PAD = F::PAD;
+  constexpr int S = M * DV + M;
+  __shared__ __align__(16) T sOm[M * (D + PAD)];
+  __shared__ float sSk[4][32];
+  const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
+  const int bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch;
+  const int cb = blockIdx.x * 4 + wv;
+  const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
+  copy_rows<T>(sOm, D + PAD, omq_h, D, M, D, 0, 0, M, tid, 256);
+  __syncthreads();
+  const bool active = cb < nch;
+  const int s0 = (active ? cb : nch - 1) * 32;
+  const size_t seq = (size_t)bh * n;
+  const T* ks = (const T*)a.k + seq * D;
+  const T* vs = (const T*)a.v + seq * DV;
+  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
+  const float* rx = a.rex + (size_t)bh * (nch + 1);
+  const int cbx = active ? cb : nch - 1;
+  const float* G = a.gst + ((size_t)bh * nch + cbx) * S;    // Ghat_b [p][d], ghat [p]
+  const bool has_after = cbx < nch - 1;
+  // key features (lanes <-> token, regs <-> p)
+  f32x16 acc[M / 32];
+  float nk;
+  key_logits<T, D, M, true>(acc, nk, ks, s0, n, omk_h);
+  const int j = s0 + col;
+  const bool vt = j < n;
+  float mx = kNegInf;
+#pragma unroll
+  for (int pt = 0; pt < M / 32; ++pt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      float x = vt ? acc[pt][v] - 0.5f * kLog2e * nk : kNegInf;
+      acc[pt][v] = x;
+      mx = fmaxf(mx, x);
+    }
+  mx = half_swap_max(mx);
+  float R = mx;
+#pragma unroll
+  for (int o = 1; o < 32; o <<= 1) {
+    float tt = __shfl_up(R, o, 32);
+    if (col >= o) R = fmaxf(R, tt);
+  }
+  R = fmaxf(R, rx[cbx]);
+  const float eps_j = has_after ? fast_exp2(R - rx[cbx + 1]) : 0.0f;
+  const float rsm = rsqrtf((float)M);
+#pragma unroll
+  for (int pt = 0; pt < M / 32; ++pt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[pt][v] = vt ? fast_exp2(acc[pt][v] - R) * rsm : 0.0f;
+  // dchi (lanes <-> token, regs <-> p)
+  float sk = 0.0f;
+  typename F::frag dlf[M / 32][F::CSTEPS];
+  typename F::frag chf[M / 32][F::CSTEPS];
+#pragma unroll 1
+  for (int pt = 0; pt < M / 32; ++pt) {
+    no_hoist();
+    f32x16 X = zero16();
+    if (has_after) {
+      // X[p, j] = Ghat[p, :] . v_j  (Ghat split hi + lo for accuracy)
+#pragma unroll 2
+      for (int s = 0; s < DV / F::KS; ++s) {
+        const int k0 = s * F::KS + h * F::KPL;
+        typename F::frag vf = vt ? F::ld(vs + (size_t)j * DV, k0) : F::zero();
+        const float* gr = G + (size_t)(pt * 32 + col) * DV + k0;
+        if constexpr (sizeof(T) == 2) {
+          bf16x8 hi, lo;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            float x = gr[e];
+            hi[e] = (bf16)x;
+            lo[e] = (bf16)(x - (float)hi[e]);
+          }
+          X = F::mma(hi, vf, X);
+          X = F::mma(lo, vf, X);
+        } else {
+          X = F::mma(gr[0], vf, X);
+        }
+      }
+    }
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int p = pt * 32 + crow(v, h);
+      float dc = 0.0f;
+      if (vt) dc = eps_j * (X[v] + (has_after ? G[(size_t)M * DV + p] : 0.0f)) + a.dchi[(seq + j) * M + p];
+      const float dl = dc * acc[pt][v];
+      sk += dl;
+      X[v] = dl * kLn2;
+    }
+#pragma unroll
+    for (int sp = 0; sp < F::CSTEPS; ++sp) {
+      dlf[pt][sp] = F::cfrag(X, sp);
+      f32x16 cs = acc[pt] * eps_j;
+      chf[pt][sp] = F::cfrag(cs, sp);
+    }
+  }
+  sk = half_swap_add(sk);
+  if (h == 0) sSk[wv][col] = sk;
+  __syncthreads();
+  // dk[j, D] = sum_p dlambda[j, p] Omega[p, D] - sk_j k_j   (lanes <-> D, regs <-> j)
+#pragma unroll 1
+  for (int Dt = 0; Dt < D / 32; ++Dt) {
+    no_hoist();
+    f32x16 dk = zero16();
+#pragma unroll
+    for (int pt = 0; pt < M / 32; ++pt)
+#pragma unroll
+      for (int sp = 0; sp < F::CSTEPS; ++sp)
+        dk = F::mma(dlf[pt][sp], F::tld_crow(sOm, D + PAD, pt * 32, sp, Dt * 32), dk);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int jj = s0 + crow(v, h);
+      if (active && jj < n) {
+        const int d = Dt * 32 + col;
+        float x = dk[v] - sSk[wv][crow(v, h)] * tof(ks[(size_t)jj * D + d]);
+        ((T*)a.dk)[(seq + jj) * D + d] = (T)x;
+      }
+    }
+  }
+  // dv[j, d] = sum_p (eps_j chi[j, p]) Ghat[p, d] + dv_intra  (lanes <-> d, regs <-> j)
+#pragma unroll 1
+  for (int dt = 0; dt < DV / 32; ++dt) {
+    no_hoist();
+    f32x16 dv = zero16();
+    if (has_after) {
+#pragma unroll
+      for (int pt = 0; pt < M / 32; ++pt)
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp) {
+          if constexpr (sizeof(T) == 2) {
+            bf16x8 hi, lo;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const int p = pt * 32 + 16 * sp + 8 * (e >> 2) + 4 * h + (e & 3);
+              float x = G[(size_t)p * DV + dt * 32 + col];
+              hi[e] = (bf16)x;
+              lo[e] = (bf16)(x - (float)hi[e]);
+            }
+            dv = F::mma(chf[pt][sp], hi, dv);
+            dv = F::mma(chf[pt][sp], lo, dv);
+          } else {
+            const int p = pt * 32 + crow(sp, h);
+            dv = F::mma(chf[pt][sp], G[(size_t)p * DV + dt * 32 + col], dv);
+          }
+        }
+    }
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int jj = s0 + crow(v, h);
+      if (active && jj < n) {
+        const int d = dt * 32 + col;
+        float x = dv[v];
+        for (int b = 0; b < nfb; ++b) x += a.dvin[(((size_t)b * a.BH + bh) * n + jj) * DV + d];
+        ((T*)a.dv)[(seq + jj) * DV + d] = (T)x;
+      }
+    }
+  }
+}
+
+// float32 accumulators (summed over feature blocks) -> output dtype
+template <typename T>
+__global__ __launch_bounds__(256) void k_bwd_final(const float* __restrict__ src, T* __restrict__ dst,
+                                                   size_t count, int nfb) {
+  size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= count) return;
+  float x = 0.0f;
+  for (int b = 0; b < nfb; ++b) x += src[(size_t)b * count + i];
+  dst[i] = (T)x;
+}
+
+// ---------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------
+static int launch_err(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) {
+    set_error("backward %s launch failed: %s", what, hipGetErrorString(e));
+    return -4;
+  }
+  return 0;
+}
+
+template <typename T, int D, int DV, int M, int NA>
+static int run_bwd(const Shape& s, BwdArgs a, hipStream_t st) {
+  using Q = QCfg<T, D, DV, M, NA>;
+  constexpr int NFB = Q::NFB;
+  const int BH = (int)s.BH();
+  const size_t rows = (size_t)BH * s.n;
+  {
+    size_t z4 = (rows * (DV + DV + D + D) * NFB) / 4;     // du32, dvin, dr32, dq32 are contiguous
+    k_fill_zero<<<(unsigned)((z4 + 255) / 256), 256, 0, st>>>(a.du32, z4);
+    k_bwd_rowprep<T, DV><<<(unsigned)((rows + 7) / 8), 256, 0, st>>>(a);
+  }
+  // query sweeps over segments of seg_steps 16-row steps
+  const int nsteps = (int)((s.n + Q::BS - 1) / Q::BS);
+  const long target = 1024;
+  int seg = (int)(((long)nsteps * BH * NFB + target - 1) / target);
+  if (seg < 4) seg = 4;
+  if (seg > nsteps) seg = nsteps;
+  a.seg_steps = seg;
+  const int nseg = (nsteps + seg - 1) / seg;
+  k_bwd_du<T, D, DV, M, NA><<<dim3(nseg, BH, NFB), 256, 0, st>>>(a);
+  if (int rc = launch_err("du")) return rc;
+  k_bwd_dqdr<T, D, DV, M, NA><<<dim3(nseg, BH, NFB), 256, 0, st>>>(a);
+  if (int rc = launch_err("dqdr")) return rc;
+  const int nch = (int)s.nch();
+  k_bwd_state<T, D, DV, M, NA><<<dim3(nch, BH, NFB), 64 * StCfg<T, D, DV, M, NA>::NW, 0, st>>>(a);
+  if (int rc = launch_err("state")) return rc;
+  constexpr int S = M * DV + M;
+  k_bwd_revscan<S><<<dim3((S / 4 + 255) / 256, BH), 256, 0, st>>>(a);
+  k_bwd_keys<T, D, DV, M><<<dim3((nch + 3) / 4, BH), 256, 0, st>>>(a, NFB);
+  if (int rc = launch_err("keys")) return rc;
+  k_bwd_final<T><<<(unsigned)((rows * DV + 255) / 256), 256, 0, st>>>(a.du32, (T*)a.du, rows * DV, NFB);
+  k_bwd_final<T><<<(unsigned)((rows * D + 255) / 256), 256, 0, st>>>(a.dr32, (T*)a.dr, rows * D, NFB);
+  k_bwd_final<T><<<(unsigned)((rows * D + 255) / 256), 256, 0, st>>>(a.dq32, (T*)a.dq, rows * D, NFB);
+  return launch_err("final");
+}
+
+#define LS_BWD_CASES(X)   \
+  X(bf16, 32, 32, 32)     \
+  X(bf16, 64, 64, 64)     \
+  X(bf16, 64, 64, 128)    \
+  X(bf16, 128, 128, 64)   \
+  X(bf16, 128, 128, 128)  \
+  X(bf16, 128, 128, 256)  \
+  X(float, 32, 32, 32)    \
+  X(float, 32, 32, 64)    \
+  X(float, 64, 64, 32)    \
+  X(float, 64, 64, 64)
+
+int launch_backward(const Shape& s, const void* q, const void* k, const void* v, const void* r,
+                    const void* u, const float* omega, const void* out, const float* stats,
+                    const void* dout, void* dq, void* dk, void* dv, void* dr, void* du,
+                    const Workspace& ws, hipStream_t st) {
+  // recompute the forward's prefix states (boundary states and frames)
+  int rc = launch_forward(s, q, k, v, r, u, omega, nullptr, nullptr, nullptr, nullptr, nullptr, ws, st);
+  if (rc) return rc;
+  BwdArgs a;
+  a.q = q; a.k = k; a.v = v; a.r = r; a.u = u; a.omega = omega; a.out = out; a.stats = stats;
+  a.dout = dout; a.dq = dq; a.dk = dk; a.dv = dv; a.dr = dr; a.du = du;
+  a.omq = ws.omq; a.omk = ws.omk; a.states = ws.states; a.rex = ws.rex;
+  a.gst = ws.gstates; a.dchi = ws.dchi; a.dvin = ws.dvin; a.du32 = ws.du32; a.dr32 = ws.dr32;
+  a.dq32 = ws.dq32; a.rowstat = ws.rowstat;
+  a.H = (int)s.H; a.n = (int)s.n; a.w = s.w; a.nch = (int)s.nch(); a.BH = (int)s.BH();
+  a.seg_steps = 1; a.eps = s.eps;
+  const int NA = (s.w + 31) / 32;
+#define X(T, D_, DV_, M_)                                                            \
+  if (s.dtype == (sizeof(T) == 2 ? 1 : 0) && s.D == D_ && s.Dv == DV_ && s.m == M_) { \
+    if (NA == 1) return run_bwd<T, D_, DV_, M_, 1>(s, a, st);                        \
+    return run_bwd<T, D_, DV_, M_, 2>(s, a, st);                                     \
+  }
+  LS_BWD_CASES(X)
+#undef X
+  set_error("backward: unsupported shape (dtype=%d D=%d Dv=%d m=%d)", s.dtype, s.D, s.Dv, s.m);
   return -2;
 }
 

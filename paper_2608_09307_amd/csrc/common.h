@@ -58,6 +58,13 @@ template <> struct MF<bf16> {
     return f;
   }
   static constexpr int CSTEPS = 2;   // k-steps per 32-row C tile
+  // ---- fragments from K-major storage mat[k][n] (n contiguous), column n0 + (lane & 31) ----
+  // natural k order: rows kbase + 8h + 0..7
+  LS_DEV static frag tld_nat(const bf16* mat, int ld, int kbase, int n0);
+  // crow order of k-step sp of a C-derived partner: rows kbase + 16sp + 8(e>>2) + 4h + (e&3)
+  LS_DEV static frag tld_crow(const bf16* mat, int ld, int kbase, int sp, int n0);
+  // crow order with an arbitrary logical-row -> storage-row map (ring buffers)
+  template <class RowMap> LS_DEV static frag tld_crow_map(const bf16* mat, int ld, int sp, int n0, RowMap rm);
   // storage position of contraction index k for permuted operands
   LS_DEV static int sigma(int k) {
     int g = (k >> 2) & 3;
@@ -81,8 +88,63 @@ template <> struct MF<float> {
   }
   LS_DEV static frag cfrag(const f32x16& acc, int sp) { return acc[sp]; }
   static constexpr int CSTEPS = 16;
+  LS_DEV static frag tld_nat(const float* mat, int ld, int kbase, int n0) {
+    const int l = threadIdx.x & 63;
+    return mat[(kbase + (l >> 5)) * ld + n0 + (l & 31)];
+  }
+  LS_DEV static frag tld_crow(const float* mat, int ld, int kbase, int sp, int n0) {
+    const int l = threadIdx.x & 63;
+    return mat[(kbase + 8 * (sp >> 2) + 4 * (l >> 5) + (sp & 3)) * ld + n0 + (l & 31)];
+  }
+  template <class RowMap> LS_DEV static frag tld_crow_map(const float* mat, int ld, int sp, int n0, RowMap rm) {
+    const int l = threadIdx.x & 63;
+    return mat[rm(8 * (sp >> 2) + 4 * (l >> 5) + (sp & 3)) * ld + n0 + (l & 31)];
+  }
   LS_DEV static int sigma(int k) { return k; }
 };
+
+// ---- transposing LDS reads (ds_read_b64_tr_b16) ----
+// Within each 16-lane group, lane i receives column i of the 4 x 16 block whose
+// row j is the 64-bit chunk addressed by lane 4j + i/4 (element i%4).  With
+// lane L = 16*g + s addressing row k0 + (s>>2) and columns
+// n0 + 16*(g&1) + 4*(s&3) of a row-major [k][n] matrix, lane L receives
+// M[k0 .. k0+3][n0 + (L & 31)]: an MFMA operand fragment read from storage
+// whose contiguous axis is the operand's M/N index.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+LS_DEV bf16x4 lds_tr4(const bf16* p) {
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  s16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
+  return __builtin_bit_cast(bf16x4, r);
+}
+// address of this lane's 64-bit chunk for rows k0..k0+3 of a [k][n] matrix
+LS_DEV const bf16* tr_addr(const bf16* mat, int ld, int k0, int n0) {
+  const int L = threadIdx.x & 63, g = L >> 4, s = L & 15;
+  return mat + (k0 + (s >> 2)) * ld + n0 + 16 * (g & 1) + 4 * (s & 3);
+}
+LS_DEV bf16x8 cat44(bf16x4 a, bf16x4 b) {
+  bf16x8 r;
+  r[0] = a[0]; r[1] = a[1]; r[2] = a[2]; r[3] = a[3];
+  r[4] = b[0]; r[5] = b[1]; r[6] = b[2]; r[7] = b[3];
+  return r;
+}
+
+LS_DEV bf16x8 MF<bf16>::tld_nat(const bf16* mat, int ld, int kbase, int n0) {
+  const int h = (threadIdx.x & 63) >> 5;
+  return cat44(lds_tr4(tr_addr(mat, ld, kbase + 8 * h, n0)), lds_tr4(tr_addr(mat, ld, kbase + 8 * h + 4, n0)));
+}
+LS_DEV bf16x8 MF<bf16>::tld_crow(const bf16* mat, int ld, int kbase, int sp, int n0) {
+  const int h = (threadIdx.x & 63) >> 5;
+  return cat44(lds_tr4(tr_addr(mat, ld, kbase + 16 * sp + 4 * h, n0)),
+               lds_tr4(tr_addr(mat, ld, kbase + 16 * sp + 8 + 4 * h, n0)));
+}
+template <class RowMap>
+LS_DEV bf16x8 MF<bf16>::tld_crow_map(const bf16* mat, int ld, int sp, int n0, RowMap rm) {
+  const int L = threadIdx.x & 63, g = L >> 4, s = L & 15, h = L >> 5;
+  const int col = n0 + 16 * (g & 1) + 4 * (s & 3);
+  bf16x4 a = lds_tr4(mat + rm(16 * sp + 4 * h + (s >> 2)) * ld + col);
+  bf16x4 b = lds_tr4(mat + rm(16 * sp + 8 + 4 * h + (s >> 2)) * ld + col);
+  return cat44(a, b);
+}
 
 // row index of accumulator register v in a 32x32 tile
 LS_DEV int crow(int v, int h) { return 8 * (v >> 2) + 4 * h + (v & 3); }
@@ -108,6 +170,9 @@ LS_DEV float uniform(float x) {
   return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
 }
 LS_DEV int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// LDS writes by some lanes of a wave, then reads by other lanes of that wave
+LS_DEV void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 // compiler-only barrier: memory reads after it cannot be hoisted above it
 LS_DEV void no_hoist() { asm volatile("" ::: "memory"); }

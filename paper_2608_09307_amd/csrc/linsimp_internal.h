@@ -33,10 +33,11 @@ struct Workspace {
   // backward-only regions (null in forward)
   float* gstates;   // [BH][nch][m*Dv + m]  per-chunk state gradients, then reverse-scanned
   float* dchi;      // [BH][n][m]           intra-chunk key-feature gradient (frame R_j)
-  float* dvin;      // [BH][n][Dv]          intra-chunk value gradient
-  float* du32;      // [BH][nch][WIN][Dv]   per-chunk anchor-gradient partials (du)
-  float* dr32;      // [BH][nch][WIN][D]    per-chunk anchor-gradient partials (dr)
-  float* rowstat;   // [BH][n][4]           per-row backward scalars
+  float* dvin;      // [nfb][BH][n][Dv]     intra-chunk value gradient
+  float* du32;      // [nfb][BH][n][Dv]     float32 accumulators of du, dr, dq
+  float* dr32;      // [nfb][BH][n][D]
+  float* dq32;      // [nfb][BH][n][D]
+  float* rowstat;   // [BH][n][2]           per-row 1/(Z+eps) and dZ
 };
 
 size_t workspace_bytes(const Shape& s, bool backward);
