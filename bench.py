@@ -1,0 +1,217 @@
+#!/usr/bin/env python3
+"""LinSimp forward + backward throughput on one MI355X.
+
+Workload: the 16k-context layer (B=2, H=16, n=16384, d=m=128, w=64; bf16
+inputs, float32 state), synthetic seeded inputs resident in HBM.  One step is
+the whole hot path: forward (key feature map, chunk states, chunk scan,
+anchor-window readout) and backward (query sweeps, state sweep, reverse scan,
+key side) on the same batch.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1]
+
+Prints one JSON line.  `value` is tokens/s (B*n per step time).  `roofline`
+reports the dominant kernel (largest share of the timed region) against the
+bf16 matrix-core peak, from HIP events recorded around every library kernel
+on its stream during the timed steps.  `cpu_baseline` times the float64 oracle
+on host cores on a causal prefix of one (batch, head) sequence.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+WORKLOAD = "layer16k_bf16"
+PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 matrix-core peak
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer16k_bf16.json")
+
+
+def anchor_rows(n, w):
+    """sum_i min(i+1, w): (row, anchor) pairs of one sequence."""
+    if n <= w:
+        return n * (n + 1) // 2
+    return w * (w + 1) // 2 + (n - w) * w
+
+
+def kernel_flops(wl):
+    """Algorithmic matrix-core flops per launch of each hot kernel (2 flops per
+    multiply-add).  Forward readout: logits (D) + readout (Dv + 1 for the
+    normaliser) per (row, anchor) pair and feature; backward: the five anchor
+    contractions (logits, readout, dpsi, dz, dM) = 2D + 3Dv, split across the
+    kernels that perform them."""
+    ar = wl.B * wl.H * anchor_rows(wl.n, wl.w)
+    f = 2 * wl.m * ar
+    return {
+        "fwd_readout": f * (wl.D + wl.Dv + 1),
+        "bwd_du": f * (wl.D + wl.Dv),
+        "bwd_dqdr": f * (wl.Dv + wl.D),
+        "bwd_state": f * wl.Dv,
+    }
+
+
+def src_digest():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2608_09307_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h", ".cpp")):
+            with open(os.path.join(csrc, name), "rb") as fh:
+                h.update(name.encode())
+                h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(kernel):
+    """HBM bytes per launch from the committed counter runs, if they were taken
+    on the current kernel sources; else None."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel") != kernel or t.get("src_sha") != src_digest():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(x, wl, budget_s):
+    """Time the float64 oracle (forward + backward) on host cores on the first
+    rows of one (batch, head) sequence: rows are causal, so a prefix is a
+    complete sub-problem.  Scaled to the full job: tokens/s = rows/s / H."""
+    import numpy as np
+    from oracle import linsimp as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([int(p.get("num_threads", 1)) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count() or 1
+
+    def f64(t):
+        return t.detach().float().cpu().double().numpy()
+
+    b, h = 0, 0
+    q, k, v, r, u = (f64(x[nm][b, h]) for nm in ("q", "k", "v", "r", "u"))
+    om, dO = f64(x["omega"][h]), f64(x["dO"][b, h])
+
+    def run(rows):
+        t0 = time.perf_counter()
+        O.forward_recurrent(q[:rows], k[:rows], v[:rows], r[:rows], u[:rows], om, wl.w)
+        O.backward(q[:rows], k[:rows], v[:rows], r[:rows], u[:rows], om, wl.w, dO[:rows])
+        return time.perf_counter() - t0
+
+    cal_rows = 256
+    t_cal = run(cal_rows)
+    rows = int(min(wl.n, max(cal_rows, cal_rows * budget_s / max(t_cal, 1e-6))))
+    rows = max(cal_rows, rows)
+    t = run(rows) if rows != cal_rows else t_cal
+    rate = rows / t / wl.H
+    return {"value": rate, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": (f"float64 oracle forward+backward of the first {rows} rows of one "
+                       f"(batch, head) of the {wl.n}-token layer in {t:.1f} s; full-job "
+                       f"tokens/s = rows/s / H (H={wl.H})")}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="budget of the oracle timing on host cores")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
+              "(the LinSimp core here runs on a single MI355X)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_09307_amd import linsimp as L
+    from paper_2608_09307_amd.workloads import WORKLOADS, make_inputs
+
+    wl = WORKLOADS[WORKLOAD]
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    x = make_inputs(wl, device=dev, with_grad=True)
+    d = L.dims_of(x["q"], x["v"], x["omega"], wl.w)
+    ws_f = L.alloc_workspace(d, False, dev)
+    ws_b = L.alloc_workspace(d, True, dev)
+    out = torch.empty_like(x["v"])
+    stats = torch.empty(x["q"].shape[:3] + (2,), dtype=torch.float32, device=dev)
+    grads = tuple(torch.empty_like(x[nm]) for nm in ("q", "k", "v", "r", "u"))
+
+    def step():
+        L.fwd(x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w, out=out, stats=stats,
+              workspace=ws_f)
+        L.bwd(x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w, out, stats, x["dO"],
+              grads=grads, workspace=ws_b)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    L.timing_enable(True)
+    L.timing_read()
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    L.timing_enable(False)
+    kt = L.timing_read()
+    ms = e0.elapsed_time(e1) / args.steps
+
+    tokens = wl.B * wl.n
+    kf = kernel_flops(wl)
+    total_flops = sum(kf.values()) + 0 * 1
+    fwd_flops = kf["fwd_readout"]
+    bwd_flops = kf["bwd_du"] + kf["bwd_dqdr"] + kf["bwd_state"]
+    step_tflops = (fwd_flops + bwd_flops) / (ms * 1e-3) / 1e12
+    dominant = max(kt, key=lambda k: kt[k][0]) if kt else None
+    kernels_ms = {k: round(v[0] / max(v[1], 1), 4) for k, v in sorted(kt.items(), key=lambda kv: -kv[1][0])}
+    roofline = None
+    if dominant is not None:
+        tot, cnt = kt[dominant]
+        avg_s = tot / cnt * 1e-3
+        if dominant in kf:
+            achieved = kf[dominant] / avg_s / 1e12
+            roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                        "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                        "traffic": traffic_for(dominant), "kernel": dominant,
+                        "avg_ms": round(tot / cnt, 4)}
+    line = {
+        "metric": "LinSimp fwd+bwd tokens/s at n=16k; % of MI355X bf16 MFMA peak",
+        "value": round(tokens / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1)*d^-1/4 streams, N(0,1) feature bank and dO)",
+        "config": {"workload": WORKLOAD, "B": wl.B, "H": wl.H, "n": wl.n, "d": wl.D, "m": wl.m,
+                   "w": wl.w},
+        "mfma_frac_step": round(step_tflops / PEAK_BF16_TFLOPS, 4),
+        "algorithmic_tflops_step": round(step_tflops, 2),
+        "roofline": roofline,
+        "kernels_avg_ms": kernels_ms,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(x, wl, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

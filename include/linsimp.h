@@ -130,6 +130,20 @@ int linsimp_decode_step(int64_t S, int32_t H, int32_t D, int32_t Dv, int32_t m, 
                         float* rho, void* ring_r, void* ring_u, int64_t* pos, void* out,
                         void* stream);
 
+/* Per-kernel timing, for tuning and roofline reports.  While enabled
+ * (on != 0), every kernel the library launches is bracketed by two HIP events
+ * recorded on its stream; enabling costs two event records per launch and
+ * changes nothing else.  Process-wide; returns LINSIMP_OK. */
+int linsimp_timing_enable(int on);
+
+/* Waits for the events recorded since the previous read, sums them per kernel
+ * name and clears them.  Writes up to max_kernels entries: names (a
+ * newline-separated list, NUL-terminated, into names[names_len]), total_ms[i]
+ * (summed milliseconds) and counts[i] (launches).  Returns the number of
+ * kernels written (>= 0) or a negative linsimp_status. */
+int linsimp_timing_read(char* names, int names_len, float* total_ms, int* counts,
+                        int max_kernels);
+
 /* Message for the last non-OK status returned on this thread ("" if none). */
 const char* linsimp_last_error(void);
 

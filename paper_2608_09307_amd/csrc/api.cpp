@@ -7,6 +7,11 @@
 #include <string.h>
 
 #include "linsimp_internal.h"
+#include "prof.h"
+
+#include <mutex>
+#include <string>
+#include <vector>
 
 namespace linsimp {
 
@@ -64,6 +69,48 @@ void carve(const Shape& s, void* base, bool backward, Workspace* ws) {
     ws->dr32 = ws->dvin + nfb * BH * n * s.Dv;
     ws->dq32 = ws->dr32 + nfb * BH * n * s.D;
     ws->rowstat = (float*)p; p += al(BH * n * 2 * 4);
+  }
+}
+
+// ---- per-kernel timing ----
+struct TimedLaunch {
+  std::string name;
+  hipEvent_t ev0, ev1;
+};
+static std::mutex g_tmu;
+static bool g_timing = false;
+static std::vector<TimedLaunch> g_launches;
+static std::vector<hipEvent_t> g_free;
+
+bool timing_on() { return g_timing; }
+
+static hipEvent_t take_event() {
+  if (!g_free.empty()) {
+    hipEvent_t e = g_free.back();
+    g_free.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+void timing_mark(const char* name, hipStream_t st, bool begin) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  if (begin) {
+    TimedLaunch t;
+    t.name = name;
+    t.ev0 = take_event();
+    t.ev1 = take_event();
+    if (t.ev0 == nullptr || t.ev1 == nullptr) return;
+    hipEventRecord(t.ev0, st);
+    g_launches.push_back(t);
+  } else {
+    for (auto it = g_launches.rbegin(); it != g_launches.rend(); ++it)
+      if (it->name == name) {
+        hipEventRecord(it->ev1, st);
+        break;
+      }
   }
 }
 
@@ -205,6 +252,47 @@ int linsimp_decode_step(int64_t S, int32_t H, int32_t D, int32_t Dv, int32_t m, 
   if ((rc = check_ptrs("q,k,v,r,u,omega,M,a,rho,ring_r,ring_u,pos,out", ps, 13))) return rc;
   return launch_decode(S, H, D, Dv, m, w, dtype, eps, q, k, v, r, u, omega, M, a, rho, ring_r,
                        ring_u, pos, out, (hipStream_t)stream);
+}
+
+int linsimp_timing_enable(int on) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  g_timing = on != 0;
+  return LINSIMP_OK;
+}
+
+int linsimp_timing_read(char* names, int names_len, float* total_ms, int* counts, int max_kernels) {
+  std::lock_guard<std::mutex> lk(g_tmu);
+  if (names == nullptr || total_ms == nullptr || counts == nullptr || names_len < 1 || max_kernels < 1) {
+    set_error("timing_read: bad output buffers");
+    return LINSIMP_E_INVALID_ARG;
+  }
+  std::vector<std::string> keys;
+  std::vector<double> tot;
+  std::vector<int> cnt;
+  int rc = LINSIMP_OK;
+  for (auto& t : g_launches) {
+    if (hipEventSynchronize(t.ev1) != hipSuccess) { rc = LINSIMP_E_HIP; continue; }
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, t.ev0, t.ev1) != hipSuccess) { rc = LINSIMP_E_HIP; continue; }
+    size_t k = 0;
+    while (k < keys.size() && keys[k] != t.name) ++k;
+    if (k == keys.size()) { keys.push_back(t.name); tot.push_back(0.0); cnt.push_back(0); }
+    tot[k] += ms;
+    cnt[k] += 1;
+  }
+  for (auto& t : g_launches) { g_free.push_back(t.ev0); g_free.push_back(t.ev1); }
+  g_launches.clear();
+  std::string all;
+  int nk = 0;
+  for (size_t k = 0; k < keys.size() && nk < max_kernels; ++k, ++nk) {
+    all += keys[k];
+    all += '\n';
+    total_ms[nk] = (float)tot[k];
+    counts[nk] = cnt[k];
+  }
+  snprintf(names, (size_t)names_len, "%s", all.c_str());
+  if (rc != LINSIMP_OK) set_error("timing_read: a HIP event query failed");
+  return rc < 0 ? rc : nk;
 }
 
 const char* linsimp_last_error(void) { return g_err; }

@@ -32,6 +32,7 @@
 #include "common.h"
 #include "keyfeat.h"
 #include "linsimp_internal.h"
+#include "prof.h"
 
 namespace linsimp {
 
@@ -1204,6 +1205,7 @@ static int run_bwd(const Shape& s, BwdArgs a, hipStream_t st) {
   const size_t rows = (size_t)BH * s.n;
   {
     size_t z4 = (rows * (DV + DV + D + D) * NFB) / 4;     // du32, dvin, dr32, dq32 are contiguous
+    ProfScope ps("bwd_prep", st);
     k_fill_zero<<<(unsigned)((z4 + 255) / 256), 256, 0, st>>>(a.du32, z4);
     k_bwd_rowprep<T, DV><<<(unsigned)((rows + 7) / 8), 256, 0, st>>>(a);
   }
@@ -1215,17 +1217,28 @@ static int run_bwd(const Shape& s, BwdArgs a, hipStream_t st) {
   if (seg > nsteps) seg = nsteps;
   a.seg_steps = seg;
   const int nseg = (nsteps + seg - 1) / seg;
+  { ProfScope ps("bwd_du", st);
   k_bwd_du<T, D, DV, M, NA><<<dim3(nseg, BH, NFB), 256, 0, st>>>(a);
+  }
   if (int rc = launch_err("du")) return rc;
+  { ProfScope ps("bwd_dqdr", st);
   k_bwd_dqdr<T, D, DV, M, NA><<<dim3(nseg, BH, NFB), 256, 0, st>>>(a);
+  }
   if (int rc = launch_err("dqdr")) return rc;
   const int nch = (int)s.nch();
+  { ProfScope ps("bwd_state", st);
   k_bwd_state<T, D, DV, M, NA><<<dim3(nch, BH, NFB), 64 * StCfg<T, D, DV, M, NA>::NW, 0, st>>>(a);
+  }
   if (int rc = launch_err("state")) return rc;
   constexpr int S = M * DV + M;
+  { ProfScope ps("bwd_revscan", st);
   k_bwd_revscan<S><<<dim3((S / 4 + 255) / 256, BH), 256, 0, st>>>(a);
+  }
+  { ProfScope ps("bwd_keys", st);
   k_bwd_keys<T, D, DV, M><<<dim3((nch + 3) / 4, BH), 256, 0, st>>>(a, NFB);
+  }
   if (int rc = launch_err("keys")) return rc;
+  ProfScope psf("bwd_final", st);
   k_bwd_final<T><<<(unsigned)((rows * DV + 255) / 256), 256, 0, st>>>(a.du32, (T*)a.du, rows * DV, NFB);
   k_bwd_final<T><<<(unsigned)((rows * D + 255) / 256), 256, 0, st>>>(a.dr32, (T*)a.dr, rows * D, NFB);
   k_bwd_final<T><<<(unsigned)((rows * D + 255) / 256), 256, 0, st>>>(a.dq32, (T*)a.dq, rows * D, NFB);

@@ -12,6 +12,7 @@
 // every float32 state element is read once and written once.
 #include "common.h"
 #include "linsimp_internal.h"
+#include "prof.h"
 
 namespace linsimp {
 
@@ -255,7 +256,8 @@ __global__ __launch_bounds__(256) void k_decode_advance(int64_t* pos, int64_t S)
 
 template <typename T, int D, int DV, int M, int NA>
 static int run_decode(int64_t S, DecArgs a, hipStream_t st) {
-  k_decode<T, D, DV, M, NA><<<(unsigned)(S * a.H), 256, 0, st>>>(a);
+  { ProfScope ps("decode", st);
+  k_decode<T, D, DV, M, NA><<<(unsigned)(S * a.H), 256, 0, st>>>(a); }
   k_decode_advance<<<(unsigned)((S + 255) / 256), 256, 0, st>>>(a.pos, S);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) {

@@ -17,6 +17,7 @@
 // cancels in the ratio, App. A "Feature scaling").
 #include "common.h"
 #include "linsimp_internal.h"
+#include "prof.h"
 #include "keyfeat.h"
 
 namespace linsimp {
@@ -475,17 +476,22 @@ static int run_fwd(const Shape& s, FwdArgs a, hipStream_t st) {
   const int nch = (int)s.nch();
   {
     int tot = (int)s.H * M * D;
+    ProfScope ps("prep_omega", st);
     k_prep_omega<T><<<(tot + 255) / 256, 256, 0, st>>>(a.omega, (T*)a.omq, (T*)a.omk, (int)s.H, M * D);
   }
-  k_chunk_state<T, D, DV, M><<<dim3((nch + 3) / 4, BH), 256, 0, st>>>(a);
+  { ProfScope ps("chunk_state", st);
+  k_chunk_state<T, D, DV, M><<<dim3((nch + 3) / 4, BH), 256, 0, st>>>(a); }
   {
     constexpr int S = M * DV + M;
+    ProfScope ps("state_scan", st);
     k_state_scan<M, DV><<<dim3((S / 4 + 255) / 256, BH), 256, 0, st>>>(a);
   }
   if (a.out != nullptr) {
     constexpr int NFB = RCfg<T, D, DV, M, NW, NA>::NFB;
-    k_readout<T, D, DV, M, NW, NA><<<dim3(nch, BH, NFB), 64 * NW, 0, st>>>(a);
+    { ProfScope ps("fwd_readout", st);
+    k_readout<T, D, DV, M, NW, NA><<<dim3(nch, BH, NFB), 64 * NW, 0, st>>>(a); }
     if constexpr (NFB > 1) {
+      ProfScope ps("fwd_merge", st);
       size_t rows = (size_t)BH * s.n;
       k_merge_blocks<T, DV, NFB><<<(unsigned)((rows + 7) / 8), 256, 0, st>>>(a);
     }

@@ -34,7 +34,8 @@ class Dims(ctypes.Structure):
 
 
 EXPORTS = ("linsimp_workspace_size", "linsimp_fwd", "linsimp_bwd", "linsimp_prefill",
-           "linsimp_decode_step", "linsimp_last_error", "linsimp_version")
+           "linsimp_decode_step", "linsimp_timing_enable", "linsimp_timing_read",
+           "linsimp_last_error", "linsimp_version")
 
 
 def lib_path() -> str:
@@ -61,6 +62,11 @@ def lib():
     L.linsimp_prefill.restype = ctypes.c_int
     L.linsimp_decode_step.argtypes = [i64, i32, i32, i32, i32, i32, i32, f32] + [vp] * 13 + [vp]
     L.linsimp_decode_step.restype = ctypes.c_int
+    L.linsimp_timing_enable.argtypes = [ctypes.c_int]
+    L.linsimp_timing_enable.restype = ctypes.c_int
+    L.linsimp_timing_read.argtypes = [ctypes.c_char_p, ctypes.c_int, ctypes.POINTER(ctypes.c_float),
+                                      ctypes.POINTER(ctypes.c_int), ctypes.c_int]
+    L.linsimp_timing_read.restype = ctypes.c_int
     L.linsimp_last_error.argtypes = []
     L.linsimp_last_error.restype = ctypes.c_char_p
     L.linsimp_version.argtypes = []
@@ -149,6 +155,23 @@ def bwd(q, k, v, r, u, omega, w, out, stats, dout, eps=EPS, grads=None, workspac
                              _ptr(dk, "dk"), _ptr(dv, "dv"), _ptr(dr, "dr"), _ptr(du, "du"),
                              _ptr(workspace, "workspace"), workspace.numel(), _stream()))
     return dq, dk, dv, dr, du
+
+
+def timing_enable(on: bool = True):
+    """Bracket every library kernel launch with HIP events (see linsimp_timing_enable)."""
+    _check(lib().linsimp_timing_enable(1 if on else 0))
+
+
+def timing_read(max_kernels: int = 64):
+    """Per-kernel {name: (total_ms, launches)} since the previous read."""
+    names = ctypes.create_string_buffer(4096)
+    tot = (ctypes.c_float * max_kernels)()
+    cnt = (ctypes.c_int * max_kernels)()
+    nk = lib().linsimp_timing_read(names, 4096, tot, cnt, max_kernels)
+    if nk < 0:
+        _check(nk)
+    keys = names.value.decode().split("\n")[:nk]
+    return {k: (float(tot[i]), int(cnt[i])) for i, k in enumerate(keys)}
 
 
 def prefill(k, v, r, u, omega, w, eps=EPS, workspace=None):
