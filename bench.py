@@ -117,6 +117,17 @@ def cpu_baseline(x, wl, budget_s):
                        f"tokens/s = rows/s / H (H={wl.H})")}
 
 
+def copy_calibration(torch, dev, nbytes=1 << 30, reps=3):
+    """A plain device-to-device copy of `nbytes` (read nbytes, write nbytes) run
+    `reps` times: the reference for scaling FETCH_SIZE / WRITE_SIZE counters."""
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "reps": reps}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -125,6 +136,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="budget of the oracle timing on host cores")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain device copy of known size (for scaling HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
@@ -135,9 +148,12 @@ def main():
     from paper_2608_09307_amd import linsimp as L
     from paper_2608_09307_amd.workloads import WORKLOADS, make_inputs
 
-    wl = WORKLOADS[WORKLOAD]
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        copy_calibration(torch, dev)
+        return
+    wl = WORKLOADS[WORKLOAD]
     x = make_inputs(wl, device=dev, with_grad=True)
     d = L.dims_of(x["q"], x["v"], x["omega"], wl.w)
     ws_f = L.alloc_workspace(d, False, dev)
@@ -172,7 +188,6 @@ def main():
 
     tokens = wl.B * wl.n
     kf = kernel_flops(wl)
-    total_flops = sum(kf.values()) + 0 * 1
     fwd_flops = kf["fwd_readout"]
     bwd_flops = kf["bwd_du"] + kf["bwd_dqdr"] + kf["bwd_state"]
     step_tflops = (fwd_flops + bwd_flops) / (ms * 1e-3) / 1e12

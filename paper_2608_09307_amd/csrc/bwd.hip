@@ -93,7 +93,7 @@ __global__ __launch_bounds__(256) void k_fill_zero(float* p, size_t n4) {
 template <typename T, int D, int DV, int M, int NA>
 struct QCfg {
   static constexpr int PAD = MF<T>::PAD;
-  static constexpr int NW = 4;                       // waves
+  static constexpr int NW = 8;                       // waves (two per SIMD)
   static constexpr int BS = 16;                      // rows per step
   static constexpr int RPW = BS / NW;                // rows per wave per step
   static constexpr int FB = M < 128 ? M : 128;       // feature block
@@ -107,43 +107,41 @@ struct QCfg {
 // Shared per-step state loading: the chunk's key features, values and boundary
 // state (only when the step starts a chunk), then the newest BS anchor rows.
 // ---------------------------------------------------------------------------
-// k_bwd_du: du_c = sum_i dN_i (*) A_ic and the intra-chunk value gradient
-//   dv_j += sum_{(i,c): j<=i} 2^(R_j-R_i) (psi_ic . chi_j) dA_ic
+// k_bwd_du: du_c = sum_i dN_i (*) A_ic, A_ic = psi_ic^T M^(i)
+// (the intra-chunk value gradient comes from the state sweep)
 // ---------------------------------------------------------------------------
 template <typename T, int D, int DV, int M, int NA>
 struct DuCfg : QCfg<T, D, DV, M, NA> {
   using Q = QCfg<T, D, DV, M, NA>;
   static constexpr int oOm = 0;
   static constexpr int oMp = oOm + Q::a16(Q::FB * (D + Q::PAD) * Q::ES);
-  static constexpr int oA = oMp + Q::a16(Q::FB * (DV + Q::PAD) * Q::ES);
-  static constexpr int oChi = oA + Q::a16(Q::FB * 4);
+  static constexpr int oChi = oMp + Q::a16(Q::FB * (DV + Q::PAD) * Q::ES);
   static constexpr int oV = oChi + Q::a16(32 * (Q::FB + Q::PAD) * Q::ES);
-  static constexpr int szV = Q::a16(32 * (DV + Q::PAD) * Q::ES);
-  // chi + V double as the scratch that reduces the waves' intra-chunk dv
-  static constexpr int oU = (oV + szV > oChi + 32 * DV * 4) ? oV + szV : oChi + 32 * DV * 4;
+  static constexpr int oU = oV + Q::a16(32 * (DV + Q::PAD) * Q::ES);
   static constexpr int oRj = oU + Q::a16(Q::RING * (DV + Q::PAD) * Q::ES);
-  static constexpr int oWin = oRj + Q::a16(32 * 4);
+  static constexpr int oDN = oRj + Q::a16(32 * 4);
+  static constexpr int oWin = oDN + Q::a16(Q::NW * DV * 4);
   static constexpr int BYTES = oWin + Q::a16(Q::RING * DV * 4);
 };
 
 template <typename T, int D, int DV, int M, int NA>
-__global__ __launch_bounds__(256) void k_bwd_du(BwdArgs a) {
+__global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
   using F = MF<T>;
   using C = DuCfg<T, D, DV, M, NA>;
   constexpr int PAD = C::PAD, FB = C::FB, RING = C::RING, NW = C::NW, BS = C::BS;
+  constexpr int NT = 64 * NW;
   static_assert(C::BYTES <= 160 * 1024, "du LDS budget");
   __shared__ __align__(16) char smem[C::BYTES];
   T* sOm = (T*)(smem + C::oOm);
   T* sMp = (T*)(smem + C::oMp);
-  float* sA = (float*)(smem + C::oA);
   T* sChi = (T*)(smem + C::oChi);
   T* sV = (T*)(smem + C::oV);
   T* sU = (T*)(smem + C::oU);
   float* sRj = (float*)(smem + C::oRj);
   float* sWin = (float*)(smem + C::oWin);
-  float* sRed = (float*)(smem + C::oChi);     // reused at chunk ends (dv reduction)
 
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
+  float* sDN = (float*)(smem + C::oDN) + wv * DV;
   const int bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
   const int nsteps_tot = (n + BS - 1) / BS;
   const int st0 = blockIdx.x * a.seg_steps;
@@ -162,25 +160,20 @@ __global__ __launch_bounds__(256) void k_bwd_du(BwdArgs a) {
   const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
   const float* rx = a.rex + (size_t)bh * (nch + 1);
   float* du32 = a.du32 + ((size_t)fb * a.BH + bh) * n * DV;
-  float* dvin = a.dvin + ((size_t)fb * a.BH + bh) * n * DV;
   const int w = a.w;
   auto ringrow = [&](int c) { return ((c % RING) + RING) % RING; };
 
   // Omega block (resident for the whole segment)
-  copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, 256);
+  copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
   // anchor ring: rows S0 - (32NA-1) .. S0-1 (the first step adds its own rows)
-  for (int idx = tid; idx < RING * DV; idx += 256) sWin[idx] = 0.0f;
-  for (int idx = tid; idx < (32 * NA - 1) * (DV / 4); idx += 256) {
+  for (int idx = tid; idx < RING * DV; idx += NT) sWin[idx] = 0.0f;
+  for (int idx = tid; idx < (32 * NA - 1) * (DV / 4); idx += NT) {
     int rr = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
     int c = S0 - (32 * NA - 1) + rr;
     T* dst = sU + ringrow(c) * (DV + PAD) + d0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) dst[e] = (c >= 0 && c < n) ? us[(size_t)c * DV + d0 + e] : (T)0.0f;
   }
-
-  f32x16 dvacc[DV / 32];
-#pragma unroll
-  for (int dt = 0; dt < DV / 32; ++dt) dvacc[dt] = zero16();
 
   for (int st = st0; st < st1; ++st) {
     const int i0 = st * BS;
@@ -191,7 +184,7 @@ __global__ __launch_bounds__(256) void k_bwd_du(BwdArgs a) {
     const bool has_bnd = cb > 0;
     __syncthreads();
     // flush anchors that left the window: c in [i0 - RING, i0 - RING + BS)
-    for (int idx = tid; idx < BS * DV; idx += 256) {
+    for (int idx = tid; idx < BS * DV; idx += NT) {
       int rr = idx / DV, d = idx % DV;
       int c = i0 - RING + rr;
       float* slot = sWin + ringrow(c) * DV + d;
@@ -204,7 +197,7 @@ __global__ __launch_bounds__(256) void k_bwd_du(BwdArgs a) {
       *slot = 0.0f;
     }
     // newest anchor rows [i0, i0 + BS)
-    for (int idx = tid; idx < BS * (DV / 4); idx += 256) {
+    for (int idx = tid; idx < BS * (DV / 4); idx += NT) {
       int rr = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
       int c = i0 + rr;
       T* dst = sU + ringrow(c) * (DV + PAD) + d0;
@@ -212,38 +205,15 @@ __global__ __launch_bounds__(256) void k_bwd_du(BwdArgs a) {
       for (int e = 0; e < 4; ++e) dst[e] = (c < n) ? us[(size_t)c * DV + d0 + e] : (T)0.0f;
     }
     if (chunk_start) {
-      if (st != st0) {
-        // chunk end: reduce the waves' intra-chunk dv over LDS, then write it
-        const int pcb = (i0 - 1) / 32;
-        for (int idx = tid; idx < 32 * DV; idx += 256) sRed[idx] = 0.0f;
-        __syncthreads();
-        for (int ww = 0; ww < NW; ++ww) {
-          if (wv == ww) {
-#pragma unroll
-            for (int dt = 0; dt < DV / 32; ++dt)
-#pragma unroll
-              for (int v = 0; v < 16; ++v) sRed[crow(v, h) * DV + dt * 32 + col] += dvacc[dt][v];
-          }
-          __syncthreads();
-        }
-        for (int idx = tid; idx < 32 * DV; idx += 256) {
-          int j = pcb * 32 + idx / DV;
-          if (j < n) atomicAdd(dvin + (size_t)j * DV + idx % DV, sRed[idx]);
-        }
-#pragma unroll
-        for (int dt = 0; dt < DV / 32; ++dt) dvacc[dt] = zero16();
-        __syncthreads();
-      }
       if (wv == 0) chunk_key_features<T, D, M>(ks, s0, n, omk_h, Rexb, sChi, FB + PAD, sRj, fb * FB, fb * FB + FB);
       const float* bst = a.states + ((size_t)bh * nch + cb) * S;
-      for (int idx = tid; idx < FB * (DV / 4); idx += 256) {
+      for (int idx = tid; idx < FB * (DV / 4); idx += NT) {
         int p = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
         f32x4 x = has_bnd ? *(const f32x4*)(bst + (size_t)(fb * FB + p) * DV + d0) : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int e = 0; e < 4; ++e) sMp[p * (DV + PAD) + d0 + e] = (T)x[e];
       }
-      for (int p = tid; p < FB; p += 256) sA[p] = has_bnd ? bst[(size_t)M * DV + fb * FB + p] : 0.0f;
-      copy_rows<T>(sV, DV + PAD, vs, DV, 32, DV, s0, 0, n, tid, 256);
+      copy_rows<T>(sV, DV + PAD, vs, DV, 32, DV, s0, 0, n, tid, NT);
     }
     __syncthreads();
 
@@ -262,10 +232,9 @@ __global__ __launch_bounds__(256) void k_bwd_du(BwdArgs a) {
         const int j = crow(v, h);
         sj[v] = (j <= t) ? fast_exp2(sRj[j] - Ri) : 0.0f;
       }
-      const float sjl = (col <= t) ? fast_exp2(sRj[col] - Ri) : 0.0f;
-      float dN[DV / 32];
-#pragma unroll
-      for (int dt = 0; dt < DV / 32; ++dt) dN[dt] = tof(gs[(size_t)i * DV + dt * 32 + col]) * inv;
+      // dN of this row, per wave (read back per d tile)
+      for (int d = l; d < DV; d += 64) sDN[d] = tof(gs[(size_t)i * DV + d]) * inv;
+      wave_lds_sync();
       const T* qrow = qs + (size_t)i * D;
 #pragma unroll 1
       for (int an = 0; an < NA; ++an) {
@@ -307,28 +276,19 @@ __global__ __launch_bounds__(256) void k_bwd_du(BwdArgs a) {
 #pragma unroll
           for (int sp = 0; sp < F::CSTEPS; ++sp) pf[pt][sp] = F::cfrag(accL[pt], sp);
         }
-        // P^T[j, c] (lanes <-> anchor) and P[c, j] (lanes <-> token j), masked and framed
-        f32x16 accP = zero16(), accPn = zero16();
+        // P^T[j, c] = chi_j . psi_c (lanes <-> anchor), masked and framed
+        f32x16 accP = zero16();
         const T* chirow = sChi + col * (FB + PAD);
 #pragma unroll
         for (int pt = 0; pt < FB / 32; ++pt)
 #pragma unroll
-          for (int sp = 0; sp < F::CSTEPS; ++sp) {
-            typename F::frag cf = F::ldc(chirow, pt * 32, sp, h);
-            accP = F::mma(cf, pf[pt][sp], accP);
-            accPn = F::mma(pf[pt][sp], cf, accPn);
-          }
+          for (int sp = 0; sp < F::CSTEPS; ++sp)
+            accP = F::mma(F::ldc(chirow, pt * 32, sp, h), pf[pt][sp], accP);
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          accP[v] *= sj[v];
-          accPn[v] *= sjl;
-        }
-        typename F::frag ppf[F::CSTEPS], pnf[F::CSTEPS];
+        for (int v = 0; v < 16; ++v) accP[v] *= sj[v];
+        typename F::frag ppf[F::CSTEPS];
 #pragma unroll
-        for (int sp = 0; sp < F::CSTEPS; ++sp) {
-          ppf[sp] = F::cfrag(accP, sp);
-          pnf[sp] = F::cfrag(accPn, sp);
-        }
+        for (int sp = 0; sp < F::CSTEPS; ++sp) ppf[sp] = F::cfrag(accP, sp);
         // ring row of anchor register index ar (anchor c = i - 32an - ar)
         auto rmap = [&](int ar) { return ringrow(i - 32 * an - ar); };
 #pragma unroll 1
@@ -347,32 +307,20 @@ __global__ __launch_bounds__(256) void k_bwd_du(BwdArgs a) {
           for (int sp = 0; sp < F::CSTEPS; ++sp)
             accA = F::mma(ppf[sp], F::tld_crow(sV, DV + PAD, 0, sp, dt * 32), accA);
           // du_c[d] += dN[d] A[c, d]  (lanes <-> d, regs <-> anchor)
-          const float dn = dN[dt];
+          const float dn = sDN[dt * 32 + col];
 #pragma unroll
           for (int v = 0; v < 16; ++v) {
             const int ar = crow(v, h);
             if (32 * an + ar < w && i - 32 * an - ar >= 0)
               atomicAdd(sWin + rmap(ar) * DV + dt * 32 + col, dn * accA[v]);
           }
-          // intra-chunk dv: dvacc[j, d] += sum_c P[c, j] dA[c, d], dA = dN (*) u_c
-#pragma unroll
-          for (int sp = 0; sp < F::CSTEPS; ++sp) {
-            typename F::frag uf = F::tld_crow_map(sU, DV + PAD, sp, dt * 32, rmap), daf;
-            if constexpr (sizeof(T) == 2) {
-#pragma unroll
-              for (int e = 0; e < 8; ++e) daf[e] = (bf16)(fel(uf, e) * dn);
-            } else {
-              daf = uf * dn;
-            }
-            dvacc[dt] = F::mma(pnf[sp], daf, dvacc[dt]);
-          }
         }
       }
     }
   }
-  // ---- segment end: remaining anchors and the last chunk's intra dv ----
+  // ---- segment end: remaining anchors ----
   __syncthreads();
-  for (int idx = tid; idx < RING * DV; idx += 256) {
+  for (int idx = tid; idx < RING * DV; idx += NT) {
     int rr = idx / DV, d = idx % DV;
     int c = st1 * BS - RING + rr;
     if (c >= 0 && c < n && c >= S0 - (32 * NA - 1) && c < S1) {
@@ -380,25 +328,6 @@ __global__ __launch_bounds__(256) void k_bwd_du(BwdArgs a) {
       bool edge = (c < S0) || (c + w - 1 >= S1 && S1 < n);
       if (edge) atomicAdd(du32 + (size_t)c * DV + d, x);
       else du32[(size_t)c * DV + d] = x;
-    }
-  }
-  __syncthreads();
-  {
-    const int pcb = (S1 - 1) / 32;
-    for (int idx = tid; idx < 32 * DV; idx += 256) sRed[idx] = 0.0f;
-    __syncthreads();
-    for (int ww = 0; ww < NW; ++ww) {
-      if (wv == ww) {
-#pragma unroll
-        for (int dt = 0; dt < DV / 32; ++dt)
-#pragma unroll
-          for (int v = 0; v < 16; ++v) sRed[crow(v, h) * DV + dt * 32 + col] += dvacc[dt][v];
-      }
-      __syncthreads();
-    }
-    for (int idx = tid; idx < 32 * DV; idx += 256) {
-      int j = pcb * 32 + idx / DV;
-      if (j < n) atomicAdd(dvin + (size_t)j * DV + idx % DV, sRed[idx]);
     }
   }
 }
@@ -422,10 +351,11 @@ struct DqCfg : QCfg<T, D, DV, M, NA> {
 };
 
 template <typename T, int D, int DV, int M, int NA>
-__global__ __launch_bounds__(256) void k_bwd_dqdr(BwdArgs a) {
+__global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
   using F = MF<T>;
   using C = DqCfg<T, D, DV, M, NA>;
   constexpr int PAD = C::PAD, FB = C::FB, RING = C::RING, NW = C::NW, BS = C::BS, DVA = C::DVA;
+  constexpr int NT = 64 * NW;
   static_assert(C::BYTES <= 160 * 1024, "dqdr LDS budget");
   __shared__ __align__(16) char smem[C::BYTES];
   T* sOm = (T*)(smem + C::oOm);
@@ -460,9 +390,9 @@ __global__ __launch_bounds__(256) void k_bwd_dqdr(BwdArgs a) {
   const int w = a.w;
   auto ringrow = [&](int c) { return ((c % RING) + RING) % RING; };
 
-  copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, 256);
-  for (int idx = tid; idx < RING * D; idx += 256) sWin[idx] = 0.0f;
-  for (int idx = tid; idx < (32 * NA - 1) * (D / 4); idx += 256) {
+  copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
+  for (int idx = tid; idx < RING * D; idx += NT) sWin[idx] = 0.0f;
+  for (int idx = tid; idx < (32 * NA - 1) * (D / 4); idx += NT) {
     int rr = idx / (D / 4), d0 = (idx % (D / 4)) * 4;
     int c = S0 - (32 * NA - 1) + rr;
     T* dst = sR + ringrow(c) * (D + PAD) + d0;
@@ -478,7 +408,7 @@ __global__ __launch_bounds__(256) void k_bwd_dqdr(BwdArgs a) {
     const float Rexb = rx[cb];
     const bool has_bnd = cb > 0;
     __syncthreads();
-    for (int idx = tid; idx < BS * D; idx += 256) {
+    for (int idx = tid; idx < BS * D; idx += NT) {
       int rr = idx / D, d = idx % D;
       int c = i0 - RING + rr;
       float* slot = sWin + ringrow(c) * D + d;
@@ -490,7 +420,7 @@ __global__ __launch_bounds__(256) void k_bwd_dqdr(BwdArgs a) {
       }
       *slot = 0.0f;
     }
-    for (int idx = tid; idx < BS * (D / 4); idx += 256) {
+    for (int idx = tid; idx < BS * (D / 4); idx += NT) {
       int rr = idx / (D / 4), d0 = (idx % (D / 4)) * 4;
       int c = i0 + rr;
       T* dst = sR + ringrow(c) * (D + PAD) + d0;
@@ -501,7 +431,7 @@ __global__ __launch_bounds__(256) void k_bwd_dqdr(BwdArgs a) {
       if (wv == 0) chunk_key_features<T, D, M>(ks, s0, n, omk_h, Rexb, sChi, FB + PAD, sRj, fb * FB, fb * FB + FB);
       const float* bst = a.states + ((size_t)bh * nch + cb) * S;
       // boundary M with column DV = boundary a (augmented), zero-padded to DVA
-      for (int idx = tid; idx < FB * (DVA / 4); idx += 256) {
+      for (int idx = tid; idx < FB * (DVA / 4); idx += NT) {
         int p = idx / (DVA / 4), d0 = (idx % (DVA / 4)) * 4;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -515,7 +445,7 @@ __global__ __launch_bounds__(256) void k_bwd_dqdr(BwdArgs a) {
         }
       }
       // values with column DV = 1 (so the contraction with dA also carries dZ)
-      for (int idx = tid; idx < 32 * (DVA / 4); idx += 256) {
+      for (int idx = tid; idx < 32 * (DVA / 4); idx += NT) {
         int j = idx / (DVA / 4), d0 = (idx % (DVA / 4)) * 4;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -682,7 +612,7 @@ __global__ __launch_bounds__(256) void k_bwd_dqdr(BwdArgs a) {
               rv[sp] = rf;
             }
           }
-          const float qd = qD[Dt];
+          const float qd = pick(qD, Dt);
           const float* sch = sScr + DVA + 4 * h;
           float dqs = 0.0f;
 #pragma unroll
@@ -698,7 +628,7 @@ __global__ __launch_bounds__(256) void k_bwd_dqdr(BwdArgs a) {
                 atomicAdd(sWin + rmap(ar) * D + Dt * 32 + col, dzz * qd);
             }
           }
-          dqacc[Dt] += dqs;
+          add_at(dqacc, Dt, dqs);
         }
       }
 #pragma unroll
@@ -709,7 +639,7 @@ __global__ __launch_bounds__(256) void k_bwd_dqdr(BwdArgs a) {
     }
   }
   __syncthreads();
-  for (int idx = tid; idx < RING * D; idx += 256) {
+  for (int idx = tid; idx < RING * D; idx += NT) {
     int rr = idx / D, d = idx % D;
     int c = st1 * BS - RING + rr;
     if (c >= 0 && c < n && c >= S0 - (32 * NA - 1) && c < S1) {
@@ -722,12 +652,18 @@ __global__ __launch_bounds__(256) void k_bwd_dqdr(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// k_bwd_state: per chunk and feature tile (one wave per 32 features):
-//   GB[p, d]   = sum_(i,c) sb_i psi_icp dA_ic[d]          (boundary gradient)
-//   gb[p]      = sum_(i,c) sb_i psi_icp dZ_i
-//   dchi[p, j] = sum_(i,c), j<=i  2^(R_j-R_i) psi_icp (v_j . dA_ic + dZ_i)
-// The contraction runs over (row, anchor) pairs, so psi is formed with the
-// pair index in registers (lanes <-> feature p).
+// k_bwd_state: state sweep of one chunk b, one wave per 32-feature tile.
+// With dM^(i)[p, d] = sum_c psi_icp dA_ic[d] and da^(i)[p] = dZ_i sum_c psi_icp,
+// the rows are walked in reverse with the running (frame R_t) matrices
+//   F_t = dM^(t) + 2^(R_t - R_{t+1}) F_{t+1},   f_t likewise from da,
+// i.e. F_t = sum_{i >= t in the chunk} 2^(R_t - R_i) dM^(i).  They give
+//   intra dchi_t = F_t v_t + f_t      intra dv_t = F_t^T chi_t
+//   GB_b = sum_i sb_i dM^(i) = 2^(Rex_b - R_s0) F_s0,   gb_b = 2^(Rex_b - R_s0) f_s0.
+// The query features are formed with the (row, anchor) pair in registers
+// (lanes <-> feature p): L[c, p] = sum_D r_c[D] (q_i[D] Omega[p, D]), so the
+// wave's Omega tile is scaled by q_i once per row and multiplies the anchors'
+// r rows straight from LDS; |q_i (*) r_c|^2 comes from a per-chunk table built
+// with the matrix cores (q^2 against r^2, split hi + lo in bf16).
 // ---------------------------------------------------------------------------
 template <typename T, int D, int DV, int M, int NA>
 struct StCfg {
@@ -735,42 +671,72 @@ struct StCfg {
   static constexpr int FB = M < 128 ? M : 128;
   static constexpr int NFB = M / FB;
   static constexpr int NW = FB / 32;
-  static constexpr int WIN = 32 + 32 * NA - 1;
-  static constexpr int DVA = DV + 16;
+  static constexpr int AW = 32 * NA;                 // anchor offsets i - c per row
+  static constexpr int WIN = 32 + AW - 1;            // anchor window rows of a chunk
+  static constexpr int NT32 = (WIN + 31) / 32;
+  static constexpr int RB = 4;                       // rows per intra-dv flush
   static constexpr int ES = sizeof(T);
   static constexpr int a16(int x) { return (x + 15) & ~15; }
-  static constexpr int oOm = 0;
-  static constexpr int oR = oOm + a16(FB * (D + PAD) * ES);
-  static constexpr int oU = oR + a16(WIN * (D + PAD) * ES);
-  static constexpr int oV = oU + a16(WIN * (DV + PAD) * ES);
-  static constexpr int oQ = oV + a16(32 * (DVA + PAD) * ES);
-  static constexpr int oRow = oQ + a16(32 * (D + PAD) * ES);
-  static constexpr int oDN = oRow + a16(32 * 8 * 4);
-  static constexpr int oBias = oDN + a16(DVA * 4);
-  static constexpr int BYTES = oBias + a16(NW * 32 * 4);
+  static constexpr int oR = 0;
+  static constexpr int oU = oR + a16(32 * NT32 * (D + PAD) * ES);
+  static constexpr int oChi = oU + a16(WIN * (DV + PAD) * ES);
+  static constexpr int oNz = oChi + a16(32 * (FB + PAD) * ES);
+  static constexpr int oRj = oNz + a16(32 * AW * 4);
+  static constexpr int oL = oRj + a16(32 * 4);
+  static constexpr int oQ = oL + a16(32 * 4);
+  static constexpr int oDv = oQ + a16(NW * D * ES);
+  static constexpr int BYTES = oDv + a16(NW * RB * DV * 4);
 };
 
+template <typename T> LS_DEV void ld4f(const T* p, float (&x)[4]) {
+  if constexpr (sizeof(T) == 2) {
+    bf16x4 b = *(const bf16x4*)p;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = (float)b[e];
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = p[e];
+  }
+}
+
+// squared fragment, split into hi + lo parts of the operand type
+template <typename T> LS_DEV void sq_split(const typename MF<T>::frag& x, typename MF<T>::frag& hi,
+                                           typename MF<T>::frag& lo) {
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float s = fel(x, e) * fel(x, e);
+      hi[e] = (bf16)s;
+      lo[e] = (bf16)(s - (float)hi[e]);
+    }
+  } else {
+    hi = x * x;
+    lo = 0.0f;
+  }
+}
+
 template <typename T, int D, int DV, int M, int NA>
-__global__ __launch_bounds__(256) void k_bwd_state(BwdArgs a) {
+__global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
   using F = MF<T>;
   using C = StCfg<T, D, DV, M, NA>;
-  constexpr int PAD = C::PAD, FB = C::FB, WIN = C::WIN, NW = C::NW, DVA = C::DVA;
+  constexpr int PAD = C::PAD, FB = C::FB, WIN = C::WIN, NW = C::NW, AW = C::AW, RB = C::RB;
   constexpr int NT = 64 * NW;
-  static_assert(C::BYTES <= 160 * 1024, "state LDS budget");
+  static_assert(C::BYTES <= 80 * 1024, "state LDS budget (two groups per CU)");
   __shared__ __align__(16) char smem[C::BYTES];
-  T* sOm = (T*)(smem + C::oOm);
   T* sR = (T*)(smem + C::oR);
   T* sU = (T*)(smem + C::oU);
-  T* sV = (T*)(smem + C::oV);
-  T* sQ = (T*)(smem + C::oQ);
-  float* sRow = (float*)(smem + C::oRow);      // per row t: L, inv, dZ, sb, R
-  float* sDN = (float*)(smem + C::oDN);        // dN of the current row (column DV = dZ)
+  T* sChi = (T*)(smem + C::oChi);
+  float* sNz = (float*)(smem + C::oNz);        // [t][i - c]: -|z|^2 log2e / 2 - L_i, -inf if not a pair
+  float* sRj = (float*)(smem + C::oRj);
+  float* sL = (float*)(smem + C::oL);
+  float* sDv = (float*)(smem + C::oDv);        // [wave][row % RB][d] intra dv partials
 
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
-  float* sBias = (float*)(smem + C::oBias) + wv * 32;
+  T* sQ = (T*)(smem + C::oQ) + wv * D;
   const int cb = blockIdx.x, bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
   const int s0 = cb * 32;
-  const int wb = s0 - (32 * NA - 1);
+  const int wb = s0 - (AW - 1);                // window row 0 = anchor s0 - (AW - 1)
+  const int tlast = min(31, n - 1 - s0);
   const size_t seq = (size_t)bh * n;
   const T* qs = (const T*)a.q + seq * D;
   const T* ks = (const T*)a.k + seq * D;
@@ -781,197 +747,180 @@ __global__ __launch_bounds__(256) void k_bwd_state(BwdArgs a) {
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
   const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
   const float Rexb = a.rex[(size_t)bh * (nch + 1) + cb];
-  const bool has_bnd = cb > 0;
   const int w = a.w;
+  const int pw = fb * FB + wv * 32;            // first feature of this wave's tile
 
-  copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
-  copy_rows<T>(sR, D + PAD, rs_, D, WIN, D, wb, 0, n, tid, NT);
+  copy_rows<T>(sR, D + PAD, rs_, D, 32 * C::NT32, D, wb, 0, n, tid, NT);
   copy_rows<T>(sU, DV + PAD, us, DV, WIN, DV, wb, 0, n, tid, NT);
-  copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
-  for (int idx = tid; idx < 32 * (DVA / 4); idx += NT) {
-    int j = idx / (DVA / 4), d0 = (idx % (DVA / 4)) * 4;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      int d = d0 + e;
-      T x = (T)0.0f;
-      if (s0 + j < n) x = (d < DV) ? vs[(size_t)(s0 + j) * DV + d] : (d == DV ? (T)1.0f : (T)0.0f);
-      sV[j * (DVA + PAD) + d] = x;
-    }
-  }
-  // per-row scalars; the running key frame R_t of each row comes from the key map
-  if (wv == 0) {
-    f32x16 acc[M / 32];
-    float nk;
-    key_logits<T, D, M, true>(acc, nk, ks, s0, n, omk_h);
-    const bool vt = s0 + col < n;
-    float mx = kNegInf;
-#pragma unroll
-    for (int pt = 0; pt < M / 32; ++pt)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, vt ? acc[pt][v] - 0.5f * kLog2e * nk : kNegInf);
-    mx = half_swap_max(mx);
-    float R = mx;
-#pragma unroll
-    for (int o = 1; o < 32; o <<= 1) {
-      float tt = __shfl_up(R, o, 32);
-      if (col >= o) R = fmaxf(R, tt);
-    }
-    R = fmaxf(R, Rexb);
-    if (h == 0) {
-      const int i = s0 + col;
-      float L = 0.f, inv = 0.f, dZ = 0.f;
-      if (i < n) {
-        L = a.stats[(seq + i) * 2];
-        inv = a.rowstat[(seq + i) * 2];
-        dZ = a.rowstat[(seq + i) * 2 + 1];
-      }
-      sRow[col * 8 + 0] = L;
-      sRow[col * 8 + 1] = inv;
-      sRow[col * 8 + 2] = dZ;
-      sRow[col * 8 + 3] = has_bnd ? fast_exp2(Rexb - R) : 0.0f;
-      sRow[col * 8 + 4] = R;
-    }
-  }
+  if (tid < 32) sL[tid] = (s0 + tid < n) ? a.stats[(seq + s0 + tid) * 2] : 0.0f;
   __syncthreads();
-
-  const int pt = wv;                 // this wave's feature tile within the block
-  f32x16 gB[DV / 32];
-#pragma unroll
-  for (int dt = 0; dt < DV / 32; ++dt) gB[dt] = zero16();
-  f32x16 dchi = zero16();
-  float gbacc = 0.0f;
-
-#pragma unroll 1
-  for (int t = 0; t < 32; ++t) {
-    const int i = s0 + t;
-    if (i >= n) break;
-    __syncthreads();
-    const float Li = uniform(sRow[t * 8 + 0]);
-    const float inv = uniform(sRow[t * 8 + 1]);
-    const float dZ = uniform(sRow[t * 8 + 2]);
-    const float sb = uniform(sRow[t * 8 + 3]);
-    const float Ri = uniform(sRow[t * 8 + 4]);
-    for (int d = tid; d < DVA; d += NT)
-      sDN[d] = (d < DV) ? tof(gs[(size_t)i * DV + d]) * inv : (d == DV ? dZ : 0.0f);
-    __syncthreads();
-    // frame ratio of token col (for the intra-chunk terms), zero beyond row i
-    const float sjl = (col <= t) ? fast_exp2(sRow[col * 8 + 4] - Ri) : 0.0f;
-    const T* qrow = sQ + t * (D + PAD);
-#pragma unroll 1
-    for (int an = 0; an < NA; ++an) {
-      no_hoist();
-      const int c = i - 32 * an - col;                 // anchor of pair lane col
-      const bool valid = (32 * an + col < w) && (c >= 0);
-      const int wi = c - wb;
-      const T* rrow = sR + wi * (D + PAD);
-      const T* urow = sU + wi * (DV + PAD);
-      // G1 with pairs as rows: L[pair, p], lanes <-> p, regs <-> pair
+  // wave 0: chunk key features and frames; the others: the |z|^2 table
+  if (wv == 0)
+    chunk_key_features<T, D, M>(ks, s0, n, omk_h, Rexb, sChi, FB + PAD, sRj, fb * FB, fb * FB + FB);
+  if (NW == 1 || wv > 0) {
+    for (int kt = (NW == 1 ? 0 : wv - 1); kt < C::NT32; kt += (NW == 1 ? 1 : NW - 1)) {
+      // C[t][wi] = sum_D q_{s0+t}[D]^2 r_{wb+wi}[D]^2   (regs <-> t, lanes <-> window row)
       f32x16 acc = zero16();
-      float nz = 0.0f;
+      const bool vi = s0 + col < n;
+      const T* qrow = qs + (size_t)(vi ? s0 + col : 0) * D;
+      const T* rrow = sR + (32 * kt + col) * (D + PAD);
 #pragma unroll 2
       for (int s = 0; s < D / F::KS; ++s) {
         const int k0 = s * F::KS + h * F::KPL;
-        typename F::frag qf = F::ld(qrow, k0), rf = F::ld(rrow, k0), zf;
+        typename F::frag qf = vi ? F::ld(qrow, k0) : F::zero(), rf = F::ld(rrow, k0);
+        typename F::frag qh, ql, rh, rl;
+        sq_split<T>(qf, qh, ql);
+        sq_split<T>(rf, rh, rl);
+        acc = F::mma(qh, rh, acc);
         if constexpr (sizeof(T) == 2) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            float p = valid ? fel(qf, e) * fel(rf, e) : 0.0f;
-            nz += p * p;
-            zf[e] = (bf16)p;
-          }
-        } else {
-          float p = valid ? qf * rf : 0.0f;
-          nz += p * p;
-          zf = p;
-        }
-        acc = F::mma(zf, F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), acc);
-      }
-      nz = half_swap_add(nz);
-      if (h == 0) sBias[col] = valid ? -0.5f * kLog2e * nz - Li : kNegInf;
-      wave_lds_sync();
-      // dA as an A operand (rows = pairs, natural d, column DV carries dZ)
-      typename F::frag daA[DVA / F::KS];
-#pragma unroll
-      for (int s = 0; s < DVA / F::KS; ++s) {
-        const int k0 = s * F::KS + h * F::KPL;
-        if constexpr (sizeof(T) == 2) {
-          bf16x8 uf = (k0 < DV && valid) ? F::ld(urow, k0) : F::zero();
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            float uu = (k0 + e < DV) ? fel(uf, e) : (k0 + e == DV && valid ? 1.0f : 0.0f);
-            daA[s][e] = (bf16)(uu * sDN[k0 + e]);
-          }
-        } else {
-          float uu = (k0 < DV) ? (valid ? urow[k0] : 0.0f) : (k0 == DV && valid ? 1.0f : 0.0f);
-          daA[s] = uu * sDN[k0];
+          acc = F::mma(qh, rl, acc);
+          acc = F::mma(ql, rh, acc);
         }
       }
-      // Q[pair, j] = dA_pair . v_j + dZ  (lanes <-> j, regs <-> pair)
-      f32x16 accQ = zero16();
+      const int wi = 32 * kt + col;
 #pragma unroll
-      for (int s = 0; s < DVA / F::KS; ++s)
-        accQ = F::mma(daA[s], F::ld(sV + col * (DVA + PAD), s * F::KS + h * F::KPL), accQ);
-#pragma unroll
-      for (int v = 0; v < 16; ++v) accQ[v] *= sjl;
-      // psi with the pair's bias (registers <-> pair)
-      const float* bh4 = sBias + 4 * h;
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const f32x4 b4 = *(const f32x4*)(bh4 + 8 * g);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) acc[4 * g + e] = fast_exp2(acc[4 * g + e] + b4[e]);
-      }
-      float ps = 0.0f;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) ps += acc[v];
-      gbacc += ps * (dZ * sb);
-      typename F::frag pf[F::CSTEPS];
-#pragma unroll
-      for (int sp = 0; sp < F::CSTEPS; ++sp) pf[sp] = F::cfrag(acc, sp);
-      // dchi[p, j] += psi^T Q
-#pragma unroll
-      for (int sp = 0; sp < F::CSTEPS; ++sp) dchi = F::mma(pf[sp], F::cfrag(accQ, sp), dchi);
-      // GB[p, d] += psi^T (sb dN (*) u): B operand rows = pairs (crow), via transposed reads
-      if (has_bnd) {
-        auto rmap = [&](int ar) { return (i - 32 * an - ar) - wb; };
-#pragma unroll 1
-        for (int dt = 0; dt < DV / 32; ++dt) {
-          no_hoist();
-          const float dn = sDN[dt * 32 + col] * sb;
-#pragma unroll
-          for (int sp = 0; sp < F::CSTEPS; ++sp) {
-            typename F::frag uf = F::tld_crow_map(sU, DV + PAD, sp, dt * 32, rmap), bf;
-            if constexpr (sizeof(T) == 2) {
-#pragma unroll
-              for (int e = 0; e < 8; ++e) {
-                // pairs whose anchor is invalid carry psi = 0; keep their operand finite
-                bf[e] = (bf16)(fel(uf, e) * dn);
-              }
-            } else {
-              bf = uf * dn;
-            }
-            gB[dt] = F::mma(pf[sp], bf, gB[dt]);
-          }
+      for (int v = 0; v < 16; ++v) {
+        const int t = crow(v, h);
+        const int dl = t - wi + AW - 1;            // i - c
+        if (dl >= 0 && dl < AW) {
+          const bool ok = dl < w && wb + wi >= 0 && s0 + t < n;
+          sNz[t * AW + dl] = ok ? -0.5f * kLog2e * acc[v] - sL[t] : kNegInf;
         }
       }
     }
   }
-  // ---- write GB (frame Rex_b), gb and the intra-chunk dchi ----
+  // this wave's Omega tile (log2e-scaled) as B operands, resident in registers
+  typename F::frag omf[D / F::KS];
+#pragma unroll
+  for (int s = 0; s < D / F::KS; ++s) omf[s] = F::ld(omq_h + (size_t)(pw + col) * D, s * F::KS + h * F::KPL);
+  __syncthreads();
+
+  f32x16 Fm[DV / 32];
+#pragma unroll
+  for (int dt = 0; dt < DV / 32; ++dt) Fm[dt] = zero16();
+  float fpart = 0.0f;                          // f[p = col], partial over this half's anchors
+
+#pragma unroll 1
+  for (int t = tlast; t >= 0; --t) {
+    const int i = s0 + t;
+    const float inv = uniform(a.rowstat[(seq + i) * 2]);
+    const float dZ = uniform(a.rowstat[(seq + i) * 2 + 1]);
+    const float fr = uniform(t < tlast ? fast_exp2(sRj[t] - sRj[t + 1]) : 1.0f);
+    for (int e = l; e < D; e += 64) sQ[e] = qs[(size_t)i * D + e];
+    float dN[DV / 32], vv[DV / 32];
+#pragma unroll
+    for (int dt = 0; dt < DV / 32; ++dt) {
+      dN[dt] = tof(gs[(size_t)i * DV + dt * 32 + col]) * inv;
+      vv[dt] = tof(vs[(size_t)i * DV + dt * 32 + col]);
+    }
+    wave_lds_sync();
+    // logits L[c, p] of the row's anchor tiles (regs <-> anchor c = i - 32an - crow)
+    f32x16 acc[NA];
+#pragma unroll
+    for (int an = 0; an < NA; ++an) acc[an] = zero16();
+#pragma unroll
+    for (int s = 0; s < D / F::KS; ++s) {
+      const int k0 = s * F::KS + h * F::KPL;
+      typename F::frag qf = F::ld(sQ, k0), bq;
+      if constexpr (sizeof(T) == 2) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) bq[e] = (bf16)(fel(omf[s], e) * fel(qf, e));
+      } else {
+        bq = omf[s] * qf;
+      }
+#pragma unroll
+      for (int an = 0; an < NA; ++an)
+        acc[an] = F::mma(F::ld(sR + (t + AW - 1 - 32 * an - col) * (D + PAD), k0), bq, acc[an]);
+    }
+    // psi = 2^(L + bias); bias -inf outside the window
+    typename F::frag pf[NA][F::CSTEPS];
+    float ps = 0.0f;
+#pragma unroll
+    for (int an = 0; an < NA; ++an) {
+      const float* brow = sNz + t * AW + 32 * an + 4 * h;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 b4 = *(const f32x4*)(brow + 8 * g);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float x = fast_exp2(acc[an][4 * g + e] + b4[e]);
+          acc[an][4 * g + e] = x;
+          ps += x;
+        }
+      }
+#pragma unroll
+      for (int sp = 0; sp < F::CSTEPS; ++sp) pf[an][sp] = F::cfrag(acc[an], sp);
+    }
+    fpart = fpart * fr + dZ * ps;
+    // F <- 2^(R_t - R_{t+1}) F + (sum_c psi_c u_c^T) diag(dN)
+#pragma unroll
+    for (int dt = 0; dt < DV / 32; ++dt) {
+      f32x16 y = zero16();
+#pragma unroll
+      for (int an = 0; an < NA; ++an) {
+        auto rmap = [&](int ar) { return t + AW - 1 - 32 * an - ar; };
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp)
+          y = F::mma(pf[an][sp], F::tld_crow_map(sU, DV + PAD, sp, dt * 32, rmap), y);
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) Fm[dt][v] = Fm[dt][v] * fr + y[v] * dN[dt];
+    }
+    // intra dchi_t[p] = F_t[p, :] . v_t + f_t[p]  (p of register col >> 1)
+    float X[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      float x = 0.0f;
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt) x += Fm[dt][v] * vv[dt];
+      X[v] = x;
+    }
+    const float xs = half_reduce16(X);
+    const int pl = crow(col >> 1, h);
+    const float ft = __shfl(half_swap_add(fpart), pl);
+    if ((col & 1) == 0) a.dchi[(seq + i) * M + pw + pl] = xs + ft;
+    // intra dv_t[d] = sum_p chi_t[p] F_t[p, d]  (this wave's p tile; summed over waves below)
+    float chv[16];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      float c4[4];
+      ld4f<T>(sChi + t * (FB + PAD) + F::sigma(wv * 32 + 8 * g + 4 * h), c4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) chv[4 * g + e] = c4[e];
+    }
+#pragma unroll
+    for (int dt = 0; dt < DV / 32; ++dt) {
+      float x = 0.0f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) x += chv[v] * Fm[dt][v];
+      x = half_swap_add(x);
+      if ((dt & 1) == h) sDv[(wv * RB + t % RB) * DV + dt * 32 + col] = x;
+    }
+    if (t % RB == 0) {
+      __syncthreads();
+      float* dvin = a.dvin + ((size_t)fb * a.BH + bh) * n * DV;
+      for (int idx = tid; idx < RB * DV; idx += NT) {
+        const int rr = idx / DV, d = idx % DV;
+        if (t + rr <= tlast) {
+          float x = 0.0f;
+#pragma unroll
+          for (int ww = 0; ww < NW; ++ww) x += sDv[(ww * RB + rr) * DV + d];
+          dvin[(size_t)(s0 + t + rr) * DV + d] = x;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // ---- GB (frame Rex_b) and gb ----
   constexpr int S = M * DV + M;
   float* g = a.gst + ((size_t)bh * nch + cb) * S;
-  const int p0 = fb * FB + pt * 32;
+  const float fac = fast_exp2(Rexb - sRj[0]);  // 0 for the first chunk (Rex_0 = -inf)
 #pragma unroll
   for (int dt = 0; dt < DV / 32; ++dt)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) g[(size_t)(p0 + crow(v, h)) * DV + dt * 32 + col] = gB[dt][v];
-  gbacc = half_swap_add(gbacc);
-  if (h == 0) g[(size_t)M * DV + p0 + col] = gbacc;
-  // dchi: lanes <-> token j (col), regs <-> p
-  if (s0 + col < n) {
-    float* dc = a.dchi + (seq + s0 + col) * M + p0;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) dc[crow(v, h)] = dchi[v];
-  }
+    for (int v = 0; v < 16; ++v) g[(size_t)(pw + crow(v, h)) * DV + dt * 32 + col] = Fm[dt][v] * fac;
+  const float ft = half_swap_add(fpart);
+  if (h == 0) g[(size_t)M * DV + pw + col] = ft * fac;
 }
 
 // ---------------------------------------------------------------------------
@@ -1069,9 +1018,8 @@ __global__ __launch_bounds__(256) void k_bwd_keys(BwdArgs a, int nfb) {
   float sk = 0.0f;
   typename F::frag dlf[M / 32][F::CSTEPS];
   typename F::frag chf[M / 32][F::CSTEPS];
-#pragma unroll 1
+#pragma unroll
   for (int pt = 0; pt < M / 32; ++pt) {
-    no_hoist();
     f32x16 X = zero16();
     if (has_after) {
       // X[p, j] = Ghat[p, :] . v_j  (Ghat split hi + lo for accuracy)
@@ -1218,11 +1166,11 @@ static int run_bwd(const Shape& s, BwdArgs a, hipStream_t st) {
   a.seg_steps = seg;
   const int nseg = (nsteps + seg - 1) / seg;
   { ProfScope ps("bwd_du", st);
-  k_bwd_du<T, D, DV, M, NA><<<dim3(nseg, BH, NFB), 256, 0, st>>>(a);
+  k_bwd_du<T, D, DV, M, NA><<<dim3(nseg, BH, NFB), 64 * Q::NW, 0, st>>>(a);
   }
   if (int rc = launch_err("du")) return rc;
   { ProfScope ps("bwd_dqdr", st);
-  k_bwd_dqdr<T, D, DV, M, NA><<<dim3(nseg, BH, NFB), 256, 0, st>>>(a);
+  k_bwd_dqdr<T, D, DV, M, NA><<<dim3(nseg, BH, NFB), 64 * Q::NW, 0, st>>>(a);
   }
   if (int rc = launch_err("dqdr")) return rc;
   const int nch = (int)s.nch();

@@ -208,6 +208,44 @@ LS_DEV float half_swap_max(float x) {
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
+// Sixteen sums over the 32 lanes of each wave half at once (a reduce-scatter
+// butterfly that halves the live registers at every step).  On return, lane
+// (col, h) holds sum over the lanes col' of half h of x[col >> 1].
+//   lanes 16 apart: v_permlane16_swap pairs rows 0-1 and 2-3 of the wave
+//   lanes  8 apart: row_ror:8;  then row_half_mirror (l <-> 7 - l within 8),
+//   quad_perm [2,3,0,1] and [1,0,3,2], each keeping the half selected by
+//   lane bits 3, 2, 1.
+LS_DEV float half_reduce16(const float (&x)[16]) {
+  const int l = lane_id();
+  float y[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x[k]), __float_as_uint(x[k + 8]), false, false);
+    y[k] = __uint_as_float(r[0]) + __uint_as_float(r[1]);   // rows 0/2: x[k], rows 1/3: x[k+8]
+  }
+  const bool b3 = (l >> 3) & 1, b2 = (l >> 2) & 1, b1 = (l >> 1) & 1;
+  float z[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) z[k] = (b3 ? y[k + 4] : y[k]) + dpp<0x128>(b3 ? y[k] : y[k + 4]);
+  float u[2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) u[k] = (b2 ? z[k + 2] : z[k]) + dpp<0x141>(b2 ? z[k] : z[k + 2]);
+  float s = (b1 ? u[1] : u[0]) + dpp<0x4E>(b1 ? u[0] : u[1]);
+  return s + dpp<0xB1>(s);
+}
+
+// x[i] for a wave-uniform index i without dynamic register indexing
+template <int N> LS_DEV float pick(const float (&x)[N], int i) {
+  float r = x[0];
+#pragma unroll
+  for (int j = 1; j < N; ++j) r = (i == j) ? x[j] : r;
+  return r;
+}
+template <int N> LS_DEV void add_at(float (&x)[N], int i, float v) {
+#pragma unroll
+  for (int j = 0; j < N; ++j) x[j] += (i == j) ? v : 0.0f;
+}
+
 // ---- cooperative global -> LDS copies (block-wide) ----
 // 2D copy of a [rows][cols] T matrix (global row stride gstride) into LDS with
 // row stride lstride; rows >= valid_rows (or < 0 via row offset) become zero.
