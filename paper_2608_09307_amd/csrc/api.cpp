@@ -37,11 +37,16 @@ size_t workspace_bytes(const Shape& s, bool backward) {
   t += al(BH * (nch + 1) * 4);                 // rex
   if (s.m > 128) t += al((size_t)(s.m / 128) * BH * s.n * (s.Dv + 2) * 4);   // part
   if (backward) {
-    const size_t n = (size_t)s.n, nfb = s.m > 128 ? (size_t)s.m / 128 : 1;
+    const size_t n = (size_t)s.n, nfb = (size_t)bwd_nfb(s.m), ns = (size_t)bwd_slots(s.w);
     t += al(BH * nch * S * 4);                 // gstates
     t += al(BH * n * s.m * 4);                 // dchi
-    // du32, dvin, dr32, dq32 (contiguous): [nfb][BH][n][Dv | Dv | D | D]
-    t += al(nfb * BH * n * (2 * (size_t)s.Dv + 2 * (size_t)s.D) * 4);
+    const size_t nfp = nfb > 1 ? nfb : 0;      // float32 du / dr partials only when m > 128
+    t += al(nfb * BH * n * s.Dv * 4);          // dvin
+    t += al(nfp * BH * n * s.Dv * 4);          // du32
+    t += al(nfp * BH * n * s.D * 4);           // dr32
+    t += al(nfb * ns * BH * n * s.D * 4);      // dq32
+    t += al(BH * n * s.m * s.esize());         // chi
+    t += al(BH * n * 4);                       // rj
     t += al(BH * n * 2 * 4);                   // rowstat
   }
   return t;
@@ -59,15 +64,16 @@ void carve(const Shape& s, void* base, bool backward, Workspace* ws) {
   ws->rex = (float*)p; p += al(BH * (nch + 1) * 4);
   if (s.m > 128) { ws->part = (float*)p; p += al((size_t)(s.m / 128) * BH * s.n * (s.Dv + 2) * 4); }
   if (backward) {
-    const size_t n = (size_t)s.n, nfb = s.m > 128 ? (size_t)s.m / 128 : 1;
+    const size_t n = (size_t)s.n, nfb = (size_t)bwd_nfb(s.m), ns = (size_t)bwd_slots(s.w);
     ws->gstates = (float*)p; p += al(BH * nch * S * 4);
     ws->dchi = (float*)p; p += al(BH * n * s.m * 4);
-    float* acc = (float*)p;
-    p += al(nfb * BH * n * (2 * (size_t)s.Dv + 2 * (size_t)s.D) * 4);
-    ws->du32 = acc;
-    ws->dvin = ws->du32 + nfb * BH * n * s.Dv;
-    ws->dr32 = ws->dvin + nfb * BH * n * s.Dv;
-    ws->dq32 = ws->dr32 + nfb * BH * n * s.D;
+    const size_t nfp = nfb > 1 ? nfb : 0;
+    ws->dvin = (float*)p; p += al(nfb * BH * n * s.Dv * 4);
+    ws->du32 = nfp ? (float*)p : nullptr; p += al(nfp * BH * n * s.Dv * 4);
+    ws->dr32 = nfp ? (float*)p : nullptr; p += al(nfp * BH * n * s.D * 4);
+    ws->dq32 = (float*)p; p += al(nfb * ns * BH * n * s.D * 4);
+    ws->chi = p; p += al(BH * n * s.m * s.esize());
+    ws->rj = (float*)p; p += al(BH * n * 4);
     ws->rowstat = (float*)p; p += al(BH * n * 2 * 4);
   }
 }

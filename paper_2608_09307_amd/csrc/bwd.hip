@@ -18,17 +18,17 @@
 // dk = Omega^T dlambda - (sum_p dlambda_p) k.
 //
 // Kernels:
-//   k_bwd_prep     row scalars (1/(Z+eps), dZ) and zeroed accumulators
-//   k_bwd_du       query sweep 1: du (anchor side) and the intra-chunk dv
-//   k_bwd_dqdr     query sweep 2: dq (row side) and dr (anchor side)
-//   k_bwd_state    state sweep: GB_b, gb_b and the intra-chunk dchi (matrix cores,
-//                  contraction over (row, anchor) pairs)
+//   k_bwd_rowprep  row scalars 1/(Z+eps) and dZ
+//   k_bwd_keyfeat  key features chi_j and frames R_j of every token
+//   k_bwd_du       anchor sweep 1: du
+//   k_bwd_dqdr     anchor sweep 2: dr (anchor side) and per-tile partials of dq
+//   k_bwd_state    state sweep: GB_b, gb_b and the intra-chunk dchi, dv
 //   k_bwd_revscan  reverse exclusive scan of (GB, gb) with the frame monoid
 //   k_bwd_keys     key side: dk, dv
-//   k_bwd_final    float32 accumulators -> output dtype
-// The query sweeps walk a segment of rows in order, keeping the anchor-side
-// accumulators in an LDS ring that slides with the window: an anchor is written
-// once it has seen all of its rows; only anchors at segment edges use atomics.
+//   k_bwd_final*   float32 partials -> output dtype
+// The anchor sweeps are anchor-stationary: a workgroup owns 32 anchors and
+// walks the rows that see them, so du and dr are summed in registers (no
+// atomics anywhere); dq of a row is the sum of its anchor tiles' partials.
 #include "common.h"
 #include "keyfeat.h"
 #include "linsimp_internal.h"
@@ -50,11 +50,13 @@ struct BwdArgs {
   float* gst;       // [BH][nch][M*DV + M]  GB_b, then Ghat_b
   float* dchi;      // [BH][n][M]           intra-chunk key-feature gradient
   float* dvin;      // [NFB][BH][n][DV]     intra-chunk value gradient
-  float* du32;      // [NFB][BH][n][DV]
-  float* dr32;      // [NFB][BH][n][D]
-  float* dq32;      // [NFB][BH][n][D]
+  float* du32;      // [NFB][BH][n][DV]     per feature block (NFB > 1)
+  float* dr32;      // [NFB][BH][n][D]      per feature block (NFB > 1)
+  float* dq32;      // [NFB][NS][BH][n][D]  per anchor tile (slot = row chunk - tile)
+  void* chi;        // [BH][n][M]           key features, p permuted in 16-blocks
+  float* rj;        // [BH][n]              running key frame R_j
   float* rowstat;   // [BH][n][2]: 1/(Z+eps), dZ
-  int H, n, w, nch, BH, seg_steps;
+  int H, n, w, nch, BH;
   float eps;
 };
 
@@ -82,573 +84,535 @@ __global__ __launch_bounds__(256) void k_bwd_rowprep(BwdArgs a) {
   }
 }
 
-__global__ __launch_bounds__(256) void k_fill_zero(float* p, size_t n4) {
-  size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < n4) ((f32x4*)p)[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+// ---------------------------------------------------------------------------
+// Key features of every token in the running frame (one wave per chunk):
+//   R_j = max(Rex_b, max_{s0 <= j' <= j} max_p lambda_j'p),  chi_j = 2^(lambda_j - R_j)/sqrt(m)
+// stored with p permuted inside 16-blocks (the LDS layout of the sweeps).
+// ---------------------------------------------------------------------------
+template <typename T, int D, int M>
+__global__ __launch_bounds__(256) void k_bwd_keyfeat(BwdArgs a) {
+  using F = MF<T>;
+  const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
+  const int bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch;
+  const int cb = blockIdx.x * 4 + wv;
+  if (cb >= nch) return;
+  const int s0 = cb * 32;
+  const size_t seq = (size_t)bh * n;
+  const T* ks = (const T*)a.k + seq * D;
+  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
+  f32x16 acc[M / 32];
+  float nk;
+  key_logits<T, D, M, true>(acc, nk, ks, s0, n, omk_h);
+  const bool vt = s0 + col < n;
+  float mx = kNegInf;
+#pragma unroll
+  for (int pt = 0; pt < M / 32; ++pt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      float x = vt ? acc[pt][v] - 0.5f * kLog2e * nk : kNegInf;
+      acc[pt][v] = x;
+      mx = fmaxf(mx, x);
+    }
+  mx = half_swap_max(mx);
+  float R = mx;
+#pragma unroll
+  for (int o = 1; o < 32; o <<= 1) {
+    float t = __shfl_up(R, o, 32);
+    if (col >= o) R = fmaxf(R, t);
+  }
+  R = fmaxf(R, a.rex[(size_t)bh * (nch + 1) + cb]);
+  if (!vt) return;
+  if (h == 0) a.rj[seq + s0 + col] = R;
+  const float rsm = rsqrtf((float)M);
+  T* row = (T*)a.chi + (seq + s0 + col) * M;
+#pragma unroll
+  for (int pt = 0; pt < M / 32; ++pt)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      T x4[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x4[e] = (T)(fast_exp2(acc[pt][4 * g + e] - R) * rsm);
+      T* dst = row + F::sigma(pt * 32 + 8 * g + 4 * h);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dst[e] = x4[e];
+    }
 }
 
 // ---------------------------------------------------------------------------
-// Query sweeps
+// Anchor-stationary sweeps.  A workgroup owns the 32 anchors [c0, c0 + 32) of
+// one sequence and one feature block, and walks the row chunks that can see
+// them (rows c0 .. c0 + 31 + w - 1); each wave takes every eighth row of a
+// chunk.  Per (row, anchor tile) the query features psi[p, c] are formed with
+// lanes <-> anchor (registers <-> feature), exactly as in the forward readout,
+// and the anchor-side sums stay in registers; the waves' sums are added once
+// at the end.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int DV, int M, int NA>
-struct QCfg {
+struct AsCfg {
   static constexpr int PAD = MF<T>::PAD;
-  static constexpr int NW = 8;                       // waves (two per SIMD)
-  static constexpr int BS = 16;                      // rows per step
-  static constexpr int RPW = BS / NW;                // rows per wave per step
-  static constexpr int FB = M < 128 ? M : 128;       // feature block
+  static constexpr int FB = M < 128 ? M : 128;
   static constexpr int NFB = M / FB;
-  static constexpr int RING = 16 * ((32 * NA - 1 + BS + 15) / 16);   // anchor ring rows (>= window)
-  static constexpr int DVA = DV + 16;                // augmented width (column DV)
+  static constexpr int NW = 8;
   static constexpr int ES = sizeof(T);
   static constexpr int a16(int x) { return (x + 15) & ~15; }
+  static constexpr int mx(int x, int y) { return x > y ? x : y; }
+  static constexpr int oOm = 0;                                             // Omega block [p][D]
+  static constexpr int oM = oOm + a16(FB * (D + PAD) * ES);                 // boundary M ([d][sigma(p)] or [p][d])
+  static constexpr int oChi = oM + a16(mx(DV * (FB + PAD), FB * (DV + PAD)) * ES);   // chi [j][sigma(p)]
+  static constexpr int oV = oChi + a16(32 * (FB + PAD) * ES);               // V [j][d]
+  static constexpr int oQ = oV + a16(32 * (DV + PAD) * ES);                 // q rows of the chunk
+  static constexpr int oR = oQ + a16(32 * (D + PAD) * ES);                  // r of the anchor tile
+  static constexpr int oU = oR + a16(32 * (D + PAD) * ES);                  // u of the anchor tile
+  static constexpr int oRj = oU + a16(32 * (DV + PAD) * ES);                // R_j of the chunk
+  static constexpr int oA = oRj + a16(32 * 4);                              // boundary a
+  static constexpr int oW = oA + a16(FB * 4);                               // per wave: dN (DV), s_c (32)
+  static constexpr int BYTES0 = oW + a16(NW * (DV + 32) * 4);
+  static constexpr int RED = (NW / 2) * 32 * mx(DV, D) * 4;                 // end-of-sweep reduction
+  static constexpr int BYTES = mx(BYTES0, RED);
 };
 
-// Shared per-step state loading: the chunk's key features, values and boundary
-// state (only when the step starts a chunk), then the newest BS anchor rows.
-// ---------------------------------------------------------------------------
-// k_bwd_du: du_c = sum_i dN_i (*) A_ic, A_ic = psi_ic^T M^(i)
-// (the intra-chunk value gradient comes from the state sweep)
-// ---------------------------------------------------------------------------
-template <typename T, int D, int DV, int M, int NA>
-struct DuCfg : QCfg<T, D, DV, M, NA> {
-  using Q = QCfg<T, D, DV, M, NA>;
-  static constexpr int oOm = 0;
-  static constexpr int oMp = oOm + Q::a16(Q::FB * (D + Q::PAD) * Q::ES);
-  static constexpr int oChi = oMp + Q::a16(Q::FB * (DV + Q::PAD) * Q::ES);
-  static constexpr int oV = oChi + Q::a16(32 * (Q::FB + Q::PAD) * Q::ES);
-  static constexpr int oU = oV + Q::a16(32 * (DV + Q::PAD) * Q::ES);
-  static constexpr int oRj = oU + Q::a16(Q::RING * (DV + Q::PAD) * Q::ES);
-  static constexpr int oDN = oRj + Q::a16(32 * 4);
-  static constexpr int oWin = oDN + Q::a16(Q::NW * DV * 4);
-  static constexpr int BYTES = oWin + Q::a16(Q::RING * DV * 4);
-};
+// Sum the waves' 32 x (32 NT) accumulators into wave 0 through LDS (the
+// caller has finished with the other shared buffers).
+template <int NT>
+LS_DEV void reduce_waves(f32x16 (&acc)[NT], float* red, int wv, int NW) {
+  const int l = lane_id(), col = l & 31, h = l >> 5;
+  constexpr int W = 32 * NT;
+  for (int half = NW / 2; half >= 1; half >>= 1) {
+    __syncthreads();
+    if (wv >= half && wv < 2 * half) {
+      float* dst = red + (size_t)(wv - half) * 32 * W;
+#pragma unroll
+      for (int dt = 0; dt < NT; ++dt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) dst[crow(v, h) * W + dt * 32 + col] = acc[dt][v];
+    }
+    __syncthreads();
+    if (wv < half) {
+      const float* src = red + (size_t)wv * 32 * W;
+#pragma unroll
+      for (int dt = 0; dt < NT; ++dt)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[dt][v] += src[crow(v, h) * W + dt * 32 + col];
+    }
+  }
+}
 
+// psi[p, c] of one (row, anchor tile) pair: log2 features of z = q_i (*) r_c
+// against the block's Omega rows, shifted by L_i, masked anchors give 0.
+template <typename T, int D, int FB>
+LS_DEV void query_features(typename MF<T>::frag (&pf)[FB / 32][MF<T>::CSTEPS], const T* qrow,
+                           const T* rrow, const T* sOm, bool valid, float Li) {
+  using F = MF<T>;
+  constexpr int PAD = F::PAD;
+  const int l = lane_id(), col = l & 31, h = l >> 5;
+  f32x16 accL[FB / 32];
+#pragma unroll
+  for (int pt = 0; pt < FB / 32; ++pt) accL[pt] = zero16();
+  float nz = 0.0f;
+#pragma unroll 2
+  for (int s = 0; s < D / F::KS; ++s) {
+    const int k0 = s * F::KS + h * F::KPL;
+    typename F::frag qf = F::ld(qrow, k0), rf = F::ld(rrow, k0), zf;
+    if constexpr (sizeof(T) == 2) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float p = valid ? fel(qf, e) * fel(rf, e) : 0.0f;
+        nz += p * p;
+        zf[e] = (bf16)p;
+      }
+    } else {
+      float p = valid ? qf * rf : 0.0f;
+      nz += p * p;
+      zf = p;
+    }
+#pragma unroll
+    for (int pt = 0; pt < FB / 32; ++pt)
+      accL[pt] = F::mma(F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), zf, accL[pt]);
+  }
+  nz = half_swap_add(nz);
+  const float off = valid ? -0.5f * kLog2e * nz - Li : kNegInf;
+#pragma unroll
+  for (int pt = 0; pt < FB / 32; ++pt) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) accL[pt][v] = fast_exp2(accL[pt][v] + off);
+#pragma unroll
+    for (int sp = 0; sp < F::CSTEPS; ++sp) pf[pt][sp] = F::cfrag(accL[pt], sp);
+  }
+}
+
+// frame ratios 2^(R_j - R_i) of the chunk tokens j <= t for the registers' rows j
+LS_DEV void frame_ratios(float (&sj)[16], const float* sRj, int t, float Ri) {
+  const int h = lane_id() >> 5;
+  const float* sRjh = sRj + 4 * h;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int j = crow(v, h);
+    sj[v] = (j <= t) ? fast_exp2(sRjh[8 * (v >> 2) + (v & 3)] - Ri) : 0.0f;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// k_bwd_du: du_c = sum_i dN_i (*) A_ic,  A_ic = psi_ic^T M^(i)  (regs <-> anchor,
+// lanes <-> d).  M^(i) = sb_i M_b + sum_{j <= i in the chunk} 2^(R_j - R_i) chi_j v_j^T.
+// ---------------------------------------------------------------------------
 template <typename T, int D, int DV, int M, int NA>
 __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
   using F = MF<T>;
-  using C = DuCfg<T, D, DV, M, NA>;
-  constexpr int PAD = C::PAD, FB = C::FB, RING = C::RING, NW = C::NW, BS = C::BS;
+  using C = AsCfg<T, D, DV, M, NA>;
+  constexpr int PAD = C::PAD, FB = C::FB, NW = C::NW;
   constexpr int NT = 64 * NW;
+  constexpr int S = M * DV + M;
   static_assert(C::BYTES <= 160 * 1024, "du LDS budget");
   __shared__ __align__(16) char smem[C::BYTES];
   T* sOm = (T*)(smem + C::oOm);
-  T* sMp = (T*)(smem + C::oMp);
+  T* sMt = (T*)(smem + C::oM);
   T* sChi = (T*)(smem + C::oChi);
   T* sV = (T*)(smem + C::oV);
-  T* sU = (T*)(smem + C::oU);
+  T* sQ = (T*)(smem + C::oQ);
+  T* sR = (T*)(smem + C::oR);
   float* sRj = (float*)(smem + C::oRj);
-  float* sWin = (float*)(smem + C::oWin);
 
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
-  float* sDN = (float*)(smem + C::oDN) + wv * DV;
-  const int bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
-  const int nsteps_tot = (n + BS - 1) / BS;
-  const int st0 = blockIdx.x * a.seg_steps;
-  const int st1 = min(nsteps_tot, st0 + a.seg_steps);
-  if (st0 >= st1) return;
-  const int S0 = st0 * BS, S1 = min(n, st1 * BS);      // segment rows [S0, S1)
-  constexpr int S = M * DV + M;
+  const int kt = blockIdx.x, bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
+  const int c0 = kt * 32, w = a.w;
   const size_t seq = (size_t)bh * n;
   const T* qs = (const T*)a.q + seq * D;
-  const T* ks = (const T*)a.k + seq * D;
   const T* vs = (const T*)a.v + seq * DV;
   const T* rs_ = (const T*)a.r + seq * D;
-  const T* us = (const T*)a.u + seq * DV;
   const T* gs = (const T*)a.dout + seq * DV;
+  const T* chis = (const T*)a.chi + seq * M + fb * FB;
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
-  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
-  const float* rx = a.rex + (size_t)bh * (nch + 1);
-  float* du32 = a.du32 + ((size_t)fb * a.BH + bh) * n * DV;
-  const int w = a.w;
-  auto ringrow = [&](int c) { return ((c % RING) + RING) % RING; };
 
-  // Omega block (resident for the whole segment)
   copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
-  // anchor ring: rows S0 - (32NA-1) .. S0-1 (the first step adds its own rows)
-  for (int idx = tid; idx < RING * DV; idx += NT) sWin[idx] = 0.0f;
-  for (int idx = tid; idx < (32 * NA - 1) * (DV / 4); idx += NT) {
-    int rr = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
-    int c = S0 - (32 * NA - 1) + rr;
-    T* dst = sU + ringrow(c) * (DV + PAD) + d0;
+  copy_rows<T>(sR, D + PAD, rs_, D, 32, D, c0, 0, n, tid, NT);
+  f32x16 du[DV / 32];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) dst[e] = (c >= 0 && c < n) ? us[(size_t)c * DV + d0 + e] : (T)0.0f;
-  }
+  for (int dt = 0; dt < DV / 32; ++dt) du[dt] = zero16();
+  const int ch_end = min(nch - 1, (c0 + 30 + w) / 32);     // last chunk with a row that sees the tile
 
-  for (int st = st0; st < st1; ++st) {
-    const int i0 = st * BS;
-    const int cb = i0 / 32;
-    const int s0 = cb * 32;
-    const bool chunk_start = (i0 == s0) || (st == st0);
-    const float Rexb = rx[cb];
-    const bool has_bnd = cb > 0;
+#pragma unroll 1
+  for (int ch = kt; ch <= ch_end; ++ch) {
+    const int s0 = ch * 32;
+    const bool has_bnd = ch > 0;
+    const float Rexb = a.rex[(size_t)bh * (nch + 1) + ch];
     __syncthreads();
-    // flush anchors that left the window: c in [i0 - RING, i0 - RING + BS)
-    for (int idx = tid; idx < BS * DV; idx += NT) {
-      int rr = idx / DV, d = idx % DV;
-      int c = i0 - RING + rr;
-      float* slot = sWin + ringrow(c) * DV + d;
-      if (c >= 0 && c < n && c >= S0 - (32 * NA - 1)) {
-        float x = *slot;
-        bool edge = (c < S0) || (c + w - 1 >= S1 && S1 < n);
-        if (edge) atomicAdd(du32 + (size_t)c * DV + d, x);
-        else du32[(size_t)c * DV + d] = x;
-      }
-      *slot = 0.0f;
-    }
-    // newest anchor rows [i0, i0 + BS)
-    for (int idx = tid; idx < BS * (DV / 4); idx += NT) {
-      int rr = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
-      int c = i0 + rr;
-      T* dst = sU + ringrow(c) * (DV + PAD) + d0;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) dst[e] = (c < n) ? us[(size_t)c * DV + d0 + e] : (T)0.0f;
-    }
-    if (chunk_start) {
-      if (wv == 0) chunk_key_features<T, D, M>(ks, s0, n, omk_h, Rexb, sChi, FB + PAD, sRj, fb * FB, fb * FB + FB);
-      const float* bst = a.states + ((size_t)bh * nch + cb) * S;
+    if (has_bnd) {
+      const float* bst = a.states + ((size_t)bh * nch + ch) * S;
       for (int idx = tid; idx < FB * (DV / 4); idx += NT) {
         int p = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
-        f32x4 x = has_bnd ? *(const f32x4*)(bst + (size_t)(fb * FB + p) * DV + d0) : f32x4{0.f, 0.f, 0.f, 0.f};
+        f32x4 x = *(const f32x4*)(bst + (size_t)(fb * FB + p) * DV + d0);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) sMp[p * (DV + PAD) + d0 + e] = (T)x[e];
+        for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = (T)x[e];
       }
-      copy_rows<T>(sV, DV + PAD, vs, DV, 32, DV, s0, 0, n, tid, NT);
     }
+    copy_rows<T>(sChi, FB + PAD, chis, M, 32, FB, s0, 0, n, tid, NT);
+    copy_rows<T>(sV, DV + PAD, vs, DV, 32, DV, s0, 0, n, tid, NT);
+    copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
+    for (int j = tid; j < 32; j += NT) sRj[j] = (s0 + j < n) ? a.rj[seq + s0 + j] : 0.0f;
     __syncthreads();
 
 #pragma unroll 1
-    for (int rr = 0; rr < C::RPW; ++rr) {
-      const int t = (i0 - s0) + wv + NW * rr;      // row within the chunk
+    for (int t = wv; t < 32; t += NW) {
       const int i = s0 + t;
-      if (i >= n) continue;
+      if (i >= n || i < c0 || i - c0 > w + 30) continue;
       const float Li = uniform(a.stats[(seq + i) * 2]);
       const float inv = uniform(a.rowstat[(seq + i) * 2]);
       const float Ri = uniform(sRj[t]);
       const float sb = uniform(has_bnd ? fast_exp2(Rexb - Ri) : 0.0f);
+      float dN[DV / 32];
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt) dN[dt] = tof(gs[(size_t)i * DV + dt * 32 + col]) * inv;
+      const int c = c0 + col;
+      const bool valid = (i - c >= 0) && (i - c < w);
+      typename F::frag pf[FB / 32][F::CSTEPS];
+      query_features<T, D, FB>(pf, sQ + t * (D + PAD), sR + col * (D + PAD), sOm, valid, Li);
+      // intra-chunk part: P^T[j, c] = chi_j . psi_c, framed, j <= i
       float sj[16];
+      frame_ratios(sj, sRj, t, Ri);
+      f32x16 accP = zero16();
+      const T* chirow = sChi + col * (FB + PAD);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int j = crow(v, h);
-        sj[v] = (j <= t) ? fast_exp2(sRj[j] - Ri) : 0.0f;
-      }
-      // dN of this row, per wave (read back per d tile)
-      for (int d = l; d < DV; d += 64) sDN[d] = tof(gs[(size_t)i * DV + d]) * inv;
-      wave_lds_sync();
-      const T* qrow = qs + (size_t)i * D;
-#pragma unroll 1
-      for (int an = 0; an < NA; ++an) {
+      for (int pt = 0; pt < FB / 32; ++pt)
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp)
+          accP = F::mma(F::ldc(chirow, pt * 32, sp, h), pf[pt][sp], accP);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) accP[v] *= sj[v];
+      typename F::frag ppf[F::CSTEPS];
+#pragma unroll
+      for (int sp = 0; sp < F::CSTEPS; ++sp) ppf[sp] = F::cfrag(accP, sp);
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt) {
         no_hoist();
-        const int c = i - 32 * an - col;
-        const bool valid = (32 * an + col < w) && (c >= 0);
-        const T* rrow = rs_ + (size_t)(valid ? c : 0) * D;
-        f32x16 accL[FB / 32];
-#pragma unroll
-        for (int pt = 0; pt < FB / 32; ++pt) accL[pt] = zero16();
-        float nz = 0.0f;
-#pragma unroll 2
-        for (int s = 0; s < D / F::KS; ++s) {
-          const int k0 = s * F::KS + h * F::KPL;
-          typename F::frag qf = F::ld(qrow, k0), rf = F::ld(rrow, k0), zf;
-          if constexpr (sizeof(T) == 2) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              float p = valid ? fel(qf, e) * fel(rf, e) : 0.0f;
-              nz += p * p;
-              zf[e] = (bf16)p;
-            }
-          } else {
-            float p = valid ? qf * rf : 0.0f;
-            nz += p * p;
-            zf = p;
-          }
+        f32x16 accA = zero16();
+        if (has_bnd) {
+          const T* mrow = sMt + (dt * 32 + col) * (FB + PAD);
 #pragma unroll
           for (int pt = 0; pt < FB / 32; ++pt)
-            accL[pt] = F::mma(F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), zf, accL[pt]);
+#pragma unroll
+            for (int sp = 0; sp < F::CSTEPS; ++sp)
+              accA = F::mma(pf[pt][sp], F::ldc(mrow, pt * 32, sp, h), accA);
+          if (sb != 1.0f) accA *= sb;
         }
-        nz = half_swap_add(nz);
-        const float off = valid ? -0.5f * kLog2e * nz - Li : kNegInf;
-        typename F::frag pf[FB / 32][F::CSTEPS];
 #pragma unroll
-        for (int pt = 0; pt < FB / 32; ++pt) {
+        for (int sp = 0; sp < F::CSTEPS; ++sp)
+          accA = F::mma(ppf[sp], F::tld_crow(sV, DV + PAD, 0, sp, dt * 32), accA);
 #pragma unroll
-          for (int v = 0; v < 16; ++v) accL[pt][v] = fast_exp2(accL[pt][v] + off);
-#pragma unroll
-          for (int sp = 0; sp < F::CSTEPS; ++sp) pf[pt][sp] = F::cfrag(accL[pt], sp);
-        }
-        // P^T[j, c] = chi_j . psi_c (lanes <-> anchor), masked and framed
-        f32x16 accP = zero16();
-        const T* chirow = sChi + col * (FB + PAD);
-#pragma unroll
-        for (int pt = 0; pt < FB / 32; ++pt)
-#pragma unroll
-          for (int sp = 0; sp < F::CSTEPS; ++sp)
-            accP = F::mma(F::ldc(chirow, pt * 32, sp, h), pf[pt][sp], accP);
-#pragma unroll
-        for (int v = 0; v < 16; ++v) accP[v] *= sj[v];
-        typename F::frag ppf[F::CSTEPS];
-#pragma unroll
-        for (int sp = 0; sp < F::CSTEPS; ++sp) ppf[sp] = F::cfrag(accP, sp);
-        // ring row of anchor register index ar (anchor c = i - 32an - ar)
-        auto rmap = [&](int ar) { return ringrow(i - 32 * an - ar); };
-#pragma unroll 1
-        for (int dt = 0; dt < DV / 32; ++dt) {
-          no_hoist();
-          f32x16 accA = zero16();
-          if (has_bnd) {
-#pragma unroll
-            for (int pt = 0; pt < FB / 32; ++pt)
-#pragma unroll
-              for (int sp = 0; sp < F::CSTEPS; ++sp)
-                accA = F::mma(pf[pt][sp], F::tld_crow(sMp, DV + PAD, pt * 32, sp, dt * 32), accA);
-            if (sb != 1.0f) accA *= sb;
-          }
-#pragma unroll
-          for (int sp = 0; sp < F::CSTEPS; ++sp)
-            accA = F::mma(ppf[sp], F::tld_crow(sV, DV + PAD, 0, sp, dt * 32), accA);
-          // du_c[d] += dN[d] A[c, d]  (lanes <-> d, regs <-> anchor)
-          const float dn = sDN[dt * 32 + col];
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int ar = crow(v, h);
-            if (32 * an + ar < w && i - 32 * an - ar >= 0)
-              atomicAdd(sWin + rmap(ar) * DV + dt * 32 + col, dn * accA[v]);
-          }
-        }
+        for (int v = 0; v < 16; ++v) du[dt][v] += accA[v] * dN[dt];
       }
     }
   }
-  // ---- segment end: remaining anchors ----
-  __syncthreads();
-  for (int idx = tid; idx < RING * DV; idx += NT) {
-    int rr = idx / DV, d = idx % DV;
-    int c = st1 * BS - RING + rr;
-    if (c >= 0 && c < n && c >= S0 - (32 * NA - 1) && c < S1) {
-      float x = sWin[ringrow(c) * DV + d];
-      bool edge = (c < S0) || (c + w - 1 >= S1 && S1 < n);
-      if (edge) atomicAdd(du32 + (size_t)c * DV + d, x);
-      else du32[(size_t)c * DV + d] = x;
-    }
+  reduce_waves<DV / 32>(du, (float*)smem, wv, NW);
+  if (wv == 0) {
+#pragma unroll
+    for (int dt = 0; dt < DV / 32; ++dt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int c = c0 + crow(v, h);
+        if (c >= n) continue;
+        if constexpr (C::NFB == 1) ((T*)a.du)[(seq + c) * DV + dt * 32 + col] = (T)du[dt][v];
+        else a.du32[(((size_t)fb * a.BH + bh) * n + c) * DV + dt * 32 + col] = du[dt][v];
+      }
   }
 }
 
 // ---------------------------------------------------------------------------
-// k_bwd_dqdr: dq (row side, complete per row) and dr (anchor side, ring)
+// k_bwd_dqdr: per (row i, anchor c), dA = dN_i (*) u_c and
+//   dpsi[p, c] = sb_i (M_b dA_c + dZ_i a_b)[p] + sum_{j <= i} 2^(R_j - R_i) chi_j[p] (v_j . dA_c + dZ_i)
+//   dell = dpsi (*) psi,  s_c = sum_p dell[p, c]
+//   dz_c = Omega^T dell_c - s_c z_c  ->  dr_c += dz_c (*) q_i,  dq_i += dz_c (*) r_c
+// dr stays in registers (regs <-> anchor, lanes <-> D); each row's dq over this
+// tile is complete in one wave and goes to slot (chunk of i) - (tile) of dq32.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int DV, int M, int NA>
-struct DqCfg : QCfg<T, D, DV, M, NA> {
-  using Q = QCfg<T, D, DV, M, NA>;
-  static constexpr int oOm = 0;
-  static constexpr int oMp = oOm + Q::a16(Q::FB * (D + Q::PAD) * Q::ES);
-  static constexpr int oChi = oMp + Q::a16(Q::FB * (Q::DVA + Q::PAD) * Q::ES);
-  static constexpr int oV = oChi + Q::a16(32 * (Q::FB + Q::PAD) * Q::ES);
-  static constexpr int oR = oV + Q::a16(32 * (Q::DVA + Q::PAD) * Q::ES);
-  static constexpr int oRj = oR + Q::a16(Q::RING * (D + Q::PAD) * Q::ES);
-  static constexpr int oScr = oRj + Q::a16(32 * 4);
-  static constexpr int SCR = Q::DVA + 32;                 // per wave: dN/dZ (DVA) + s_c (32)
-  static constexpr int oWin = oScr + Q::a16(Q::NW * SCR * 4);
-  static constexpr int BYTES = oWin + Q::a16(Q::RING * D * 4);
-};
-
 template <typename T, int D, int DV, int M, int NA>
 __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
   using F = MF<T>;
-  using C = DqCfg<T, D, DV, M, NA>;
-  constexpr int PAD = C::PAD, FB = C::FB, RING = C::RING, NW = C::NW, BS = C::BS, DVA = C::DVA;
+  using C = AsCfg<T, D, DV, M, NA>;
+  constexpr int PAD = C::PAD, FB = C::FB, NW = C::NW;
   constexpr int NT = 64 * NW;
+  constexpr int S = M * DV + M;
+  constexpr int NS = NA + 1;
   static_assert(C::BYTES <= 160 * 1024, "dqdr LDS budget");
   __shared__ __align__(16) char smem[C::BYTES];
   T* sOm = (T*)(smem + C::oOm);
-  T* sMp = (T*)(smem + C::oMp);
+  T* sMp = (T*)(smem + C::oM);
   T* sChi = (T*)(smem + C::oChi);
   T* sV = (T*)(smem + C::oV);
+  T* sQ = (T*)(smem + C::oQ);
   T* sR = (T*)(smem + C::oR);
+  T* sU = (T*)(smem + C::oU);
   float* sRj = (float*)(smem + C::oRj);
-  float* sWin = (float*)(smem + C::oWin);
+  float* sA = (float*)(smem + C::oA);
 
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
-  float* sScr = (float*)(smem + C::oScr) + wv * C::SCR;
-  const int bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
-  const int nsteps_tot = (n + BS - 1) / BS;
-  const int st0 = blockIdx.x * a.seg_steps;
-  const int st1 = min(nsteps_tot, st0 + a.seg_steps);
-  if (st0 >= st1) return;
-  const int S0 = st0 * BS, S1 = min(n, st1 * BS);
-  constexpr int S = M * DV + M;
+  float* sDN = (float*)(smem + C::oW) + wv * (DV + 32);
+  float* sSc = sDN + DV;
+  const int kt = blockIdx.x, bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
+  const int c0 = kt * 32, w = a.w;
   const size_t seq = (size_t)bh * n;
   const T* qs = (const T*)a.q + seq * D;
-  const T* ks = (const T*)a.k + seq * D;
   const T* vs = (const T*)a.v + seq * DV;
   const T* rs_ = (const T*)a.r + seq * D;
   const T* us = (const T*)a.u + seq * DV;
   const T* gs = (const T*)a.dout + seq * DV;
+  const T* chis = (const T*)a.chi + seq * M + fb * FB;
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
-  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
-  const float* rx = a.rex + (size_t)bh * (nch + 1);
-  float* dr32 = a.dr32 + ((size_t)fb * a.BH + bh) * n * D;
-  float* dq32 = a.dq32 + ((size_t)fb * a.BH + bh) * n * D;
-  const int w = a.w;
-  auto ringrow = [&](int c) { return ((c % RING) + RING) % RING; };
 
   copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
-  for (int idx = tid; idx < RING * D; idx += NT) sWin[idx] = 0.0f;
-  for (int idx = tid; idx < (32 * NA - 1) * (D / 4); idx += NT) {
-    int rr = idx / (D / 4), d0 = (idx % (D / 4)) * 4;
-    int c = S0 - (32 * NA - 1) + rr;
-    T* dst = sR + ringrow(c) * (D + PAD) + d0;
+  copy_rows<T>(sR, D + PAD, rs_, D, 32, D, c0, 0, n, tid, NT);
+  copy_rows<T>(sU, DV + PAD, us, DV, 32, DV, c0, 0, n, tid, NT);
+  f32x16 dr[D / 32];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) dst[e] = (c >= 0 && c < n) ? rs_[(size_t)c * D + d0 + e] : (T)0.0f;
-  }
+  for (int Dt = 0; Dt < D / 32; ++Dt) dr[Dt] = zero16();
+  const int ch_end = min(nch - 1, (c0 + 30 + w) / 32);
 
-  for (int st = st0; st < st1; ++st) {
-    const int i0 = st * BS;
-    const int cb = i0 / 32;
-    const int s0 = cb * 32;
-    const bool chunk_start = (i0 == s0) || (st == st0);
-    const float Rexb = rx[cb];
-    const bool has_bnd = cb > 0;
+#pragma unroll 1
+  for (int ch = kt; ch <= ch_end; ++ch) {
+    const int s0 = ch * 32;
+    const bool has_bnd = ch > 0;
+    const float Rexb = a.rex[(size_t)bh * (nch + 1) + ch];
     __syncthreads();
-    for (int idx = tid; idx < BS * D; idx += NT) {
-      int rr = idx / D, d = idx % D;
-      int c = i0 - RING + rr;
-      float* slot = sWin + ringrow(c) * D + d;
-      if (c >= 0 && c < n && c >= S0 - (32 * NA - 1)) {
-        float x = *slot;
-        bool edge = (c < S0) || (c + w - 1 >= S1 && S1 < n);
-        if (edge) atomicAdd(dr32 + (size_t)c * D + d, x);
-        else dr32[(size_t)c * D + d] = x;
-      }
-      *slot = 0.0f;
-    }
-    for (int idx = tid; idx < BS * (D / 4); idx += NT) {
-      int rr = idx / (D / 4), d0 = (idx % (D / 4)) * 4;
-      int c = i0 + rr;
-      T* dst = sR + ringrow(c) * (D + PAD) + d0;
+    if (has_bnd) {
+      const float* bst = a.states + ((size_t)bh * nch + ch) * S;
+      for (int idx = tid; idx < FB * (DV / 4); idx += NT) {
+        int p = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
+        f32x4 x = *(const f32x4*)(bst + (size_t)(fb * FB + p) * DV + d0);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) dst[e] = (c < n) ? rs_[(size_t)c * D + d0 + e] : (T)0.0f;
-    }
-    if (chunk_start) {
-      if (wv == 0) chunk_key_features<T, D, M>(ks, s0, n, omk_h, Rexb, sChi, FB + PAD, sRj, fb * FB, fb * FB + FB);
-      const float* bst = a.states + ((size_t)bh * nch + cb) * S;
-      // boundary M with column DV = boundary a (augmented), zero-padded to DVA
-      for (int idx = tid; idx < FB * (DVA / 4); idx += NT) {
-        int p = idx / (DVA / 4), d0 = (idx % (DVA / 4)) * 4;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          int d = d0 + e;
-          float x = 0.0f;
-          if (has_bnd) {
-            if (d < DV) x = bst[(size_t)(fb * FB + p) * DV + d];
-            else if (d == DV) x = bst[(size_t)M * DV + fb * FB + p];
-          }
-          sMp[p * (DVA + PAD) + d] = (T)x;
-        }
+        for (int e = 0; e < 4; ++e) sMp[p * (DV + PAD) + d0 + e] = (T)x[e];
       }
-      // values with column DV = 1 (so the contraction with dA also carries dZ)
-      for (int idx = tid; idx < 32 * (DVA / 4); idx += NT) {
-        int j = idx / (DVA / 4), d0 = (idx % (DVA / 4)) * 4;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          int d = d0 + e;
-          T x = (T)0.0f;
-          if (s0 + j < n) x = (d < DV) ? vs[(size_t)(s0 + j) * DV + d] : (d == DV ? (T)1.0f : (T)0.0f);
-          sV[j * (DVA + PAD) + d] = x;
-        }
-      }
+      for (int p = tid; p < FB; p += NT) sA[p] = bst[(size_t)M * DV + fb * FB + p];
     }
+    copy_rows<T>(sChi, FB + PAD, chis, M, 32, FB, s0, 0, n, tid, NT);
+    copy_rows<T>(sV, DV + PAD, vs, DV, 32, DV, s0, 0, n, tid, NT);
+    copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
+    for (int j = tid; j < 32; j += NT) sRj[j] = (s0 + j < n) ? a.rj[seq + s0 + j] : 0.0f;
     __syncthreads();
 
 #pragma unroll 1
-    for (int rr = 0; rr < C::RPW; ++rr) {
-      const int t = (i0 - s0) + wv + NW * rr;
+    for (int t = wv; t < 32; t += NW) {
       const int i = s0 + t;
-      if (i >= n) continue;
+      if (i >= n || i < c0 || i - c0 > w + 30) continue;
       const float Li = uniform(a.stats[(seq + i) * 2]);
       const float inv = uniform(a.rowstat[(seq + i) * 2]);
       const float dZ = uniform(a.rowstat[(seq + i) * 2 + 1]);
       const float Ri = uniform(sRj[t]);
       const float sb = uniform(has_bnd ? fast_exp2(Rexb - Ri) : 0.0f);
-      float sj[16];
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int j = crow(v, h);
-        sj[v] = (j <= t) ? fast_exp2(sRj[j] - Ri) : 0.0f;
-      }
-      // per-wave scratch: dN (with dZ at column DV) as floats
-      for (int d = l; d < DVA; d += 64)
-        sScr[d] = (d < DV) ? tof(gs[(size_t)i * DV + d]) * inv : (d == DV ? dZ : 0.0f);
-      wave_lds_sync();
-      const T* qrow = qs + (size_t)i * D;
+      for (int d = l; d < DV; d += 64) sDN[d] = tof(gs[(size_t)i * DV + d]) * inv;
+      const T* qrow = sQ + t * (D + PAD);
       float qD[D / 32];
 #pragma unroll
       for (int Dt = 0; Dt < D / 32; ++Dt) qD[Dt] = tof(qrow[Dt * 32 + col]);
-      float dqacc[D / 32];
+      wave_lds_sync();
+      const int c = c0 + col;
+      const bool valid = (i - c >= 0) && (i - c < w);
+      typename F::frag pf[FB / 32][F::CSTEPS];
+      query_features<T, D, FB>(pf, qrow, sR + col * (D + PAD), sOm, valid, Li);
+      // dA^T fragments: lanes <-> anchor, natural d order
+      const T* urow = sU + col * (DV + PAD);
+      typename F::frag daf[DV / F::KS];
 #pragma unroll
-      for (int Dt = 0; Dt < D / 32; ++Dt) dqacc[Dt] = 0.0f;
-#pragma unroll 1
-      for (int an = 0; an < NA; ++an) {
-        no_hoist();
-        const int c = i - 32 * an - col;
-        const bool valid = (32 * an + col < w) && (c >= 0);
-        const T* rrow = sR + ringrow(c) * (D + PAD);
-        f32x16 accL[FB / 32];
+      for (int s = 0; s < DV / F::KS; ++s) {
+        const int k0 = s * F::KS + h * F::KPL;
+        typename F::frag uf = F::ld(urow, k0);
+        if constexpr (sizeof(T) == 2) {
+          const f32x4 d0 = *(const f32x4*)(sDN + k0), d1 = *(const f32x4*)(sDN + k0 + 4);
 #pragma unroll
-        for (int pt = 0; pt < FB / 32; ++pt) accL[pt] = zero16();
-        float nz = 0.0f;
-#pragma unroll 2
-        for (int s = 0; s < D / F::KS; ++s) {
-          const int k0 = s * F::KS + h * F::KPL;
-          typename F::frag qf = F::ld(qrow, k0), rf = F::ld(rrow, k0), zf;
-          if constexpr (sizeof(T) == 2) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              float p = valid ? fel(qf, e) * fel(rf, e) : 0.0f;
-              nz += p * p;
-              zf[e] = (bf16)p;
-            }
-          } else {
-            float p = valid ? qf * rf : 0.0f;
-            nz += p * p;
-            zf = p;
+          for (int e = 0; e < 4; ++e) {
+            daf[s][e] = (bf16)(fel(uf, e) * d0[e]);
+            daf[s][4 + e] = (bf16)(fel(uf, 4 + e) * d1[e]);
           }
-#pragma unroll
-          for (int pt = 0; pt < FB / 32; ++pt)
-            accL[pt] = F::mma(F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), zf, accL[pt]);
+        } else {
+          daf[s] = uf * sDN[k0];
         }
-        nz = half_swap_add(nz);
-        const float off = valid ? -0.5f * kLog2e * nz - Li : kNegInf;
+      }
+      // Q^T[j, c] = (v_j . dA_c + dZ_i) 2^(R_j - R_i), j <= i  (regs <-> j, lanes <-> anchor)
+      f32x16 accQ = zero16();
+#pragma unroll
+      for (int s = 0; s < DV / F::KS; ++s)
+        accQ = F::mma(F::ld(sV + col * (DV + PAD), s * F::KS + h * F::KPL), daf[s], accQ);
+      float sj[16];
+      frame_ratios(sj, sRj, t, Ri);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) accQ[v] = (accQ[v] + dZ) * sj[v];
+      typename F::frag qqf[F::CSTEPS];
+#pragma unroll
+      for (int sp = 0; sp < F::CSTEPS; ++sp) qqf[sp] = F::cfrag(accQ, sp);
+      // dell (natural-log derivative, times ln 2 to pair with Omega log2 e)
+      typename F::frag dlf[FB / 32][F::CSTEPS];
+      float sc = 0.0f;
+#pragma unroll
+      for (int pt = 0; pt < FB / 32; ++pt) {
+        no_hoist();
+        f32x16 dps = zero16();
+        if (has_bnd) {
+#pragma unroll
+          for (int s = 0; s < DV / F::KS; ++s)
+            dps = F::mma(F::ld(sMp + (pt * 32 + col) * (DV + PAD), s * F::KS + h * F::KPL), daf[s], dps);
+          const float* sAh = sA + pt * 32 + 4 * h;
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const f32x4 av = *(const f32x4*)(sAh + 8 * g);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) dps[4 * g + e] = (dps[4 * g + e] + dZ * av[e]) * sb;
+          }
+        }
+        // chi^T rows p, k = token j in crow order (chi stored [j][sigma(p)])
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp) {
+          typename F::frag cf;
+          if constexpr (sizeof(T) == 2) {
+            const int g = l >> 4, s4 = l & 15;
+            const int pcol = F::sigma(pt * 32 + 16 * (g & 1) + 4 * (s4 & 3));
+            bf16x4 x0 = lds_tr4(sChi + (16 * sp + 4 * h + (s4 >> 2)) * (FB + PAD) + pcol);
+            bf16x4 x1 = lds_tr4(sChi + (16 * sp + 8 + 4 * h + (s4 >> 2)) * (FB + PAD) + pcol);
+            cf = cat44(x0, x1);
+          } else {
+            cf = sChi[crow(sp, h) * (FB + PAD) + pt * 32 + col];
+          }
+          dps = F::mma(cf, qqf[sp], dps);
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float dl = dps[v] * fel(pf[pt][v / F::KPL], v % F::KPL);
+          sc += dl;
+          dps[v] = dl * kLn2;
+        }
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp) dlf[pt][sp] = F::cfrag(dps, sp);
+      }
+      sc = half_swap_add(sc);
+      if (h == 0) sSc[col] = valid ? sc : 0.0f;
+      wave_lds_sync();
+      // dz[c, D] (regs <-> anchor, lanes <-> D)
+      float* dqo = a.dq32 + ((((size_t)fb * NS + (ch - kt)) * a.BH + bh) * n + i) * D;
+#pragma unroll
+      for (int Dt = 0; Dt < D / 32; ++Dt) {
+        no_hoist();
+        f32x16 dz = zero16();
 #pragma unroll
         for (int pt = 0; pt < FB / 32; ++pt)
 #pragma unroll
-          for (int v = 0; v < 16; ++v) accL[pt][v] = fast_exp2(accL[pt][v] + off);
-        // dA^T fragments (lanes <-> anchor, natural d order, column DV carries dZ)
-        const T* urow = us + (size_t)(valid ? c : 0) * DV;
-        typename F::frag daf[DVA / F::KS];
+          for (int sp = 0; sp < F::CSTEPS; ++sp)
+            dz = F::mma(dlf[pt][sp], F::tld_crow(sOm, D + PAD, pt * 32, sp, Dt * 32), dz);
+        float rv[16];
 #pragma unroll
-        for (int s = 0; s < DVA / F::KS; ++s) {
-          const int k0 = s * F::KS + h * F::KPL;
-          if constexpr (sizeof(T) == 2) {
-            bf16x8 uf = (k0 < DV && valid) ? F::ld(urow, k0) : F::zero();
+        for (int sp = 0; sp < F::CSTEPS; ++sp) {
+          typename F::frag rf = F::tld_crow(sR, D + PAD, 0, sp, Dt * 32);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              float uu = (k0 + e < DV) ? fel(uf, e) : (k0 + e == DV && valid ? 1.0f : 0.0f);
-              daf[s][e] = (bf16)(uu * sScr[k0 + e]);
-            }
-          } else {
-            float uu = (k0 < DV) ? (valid ? urow[k0] : 0.0f) : (k0 == DV && valid ? 1.0f : 0.0f);
-            daf[s] = uu * sScr[k0];
+          for (int e = 0; e < F::KPL; ++e) rv[F::KPL * sp + e] = fel(rf, e);
+        }
+        const float qd = qD[Dt];
+        const float* sch = sSc + 4 * h;
+        float dqs = 0.0f;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 s4 = *(const f32x4*)(sch + 8 * g);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int v = 4 * g + e;
+            const float dzz = dz[v] - s4[e] * qd * rv[v];
+            dqs += dzz * rv[v];
+            dr[Dt][v] += dzz * qd;
           }
         }
-        // Q^T[j, c] = v_j . dA_c + dZ   (lanes <-> anchor, regs <-> j), framed and masked
-        f32x16 accQ = zero16();
-#pragma unroll
-        for (int s = 0; s < DVA / F::KS; ++s)
-          accQ = F::mma(F::ld(sV + col * (DVA + PAD), s * F::KS + h * F::KPL), daf[s], accQ);
-#pragma unroll
-        for (int v = 0; v < 16; ++v) accQ[v] *= sj[v];
-        typename F::frag qqf[F::CSTEPS];
-#pragma unroll
-        for (int sp = 0; sp < F::CSTEPS; ++sp) qqf[sp] = F::cfrag(accQ, sp);
-        // dpsi^T[p, c] = sb * (M_b | a_b)[p, :] dA^T + chi^T Q^T ; dell = dpsi * psi
-        typename F::frag dlf[FB / 32][F::CSTEPS];
-        float sc = 0.0f;
-#pragma unroll 1
-        for (int pt = 0; pt < FB / 32; ++pt) {
-          no_hoist();
-          f32x16 dps = zero16();
-          if (has_bnd) {
-#pragma unroll
-            for (int s = 0; s < DVA / F::KS; ++s)
-              dps = F::mma(F::ld(sMp + (pt * 32 + col) * (DVA + PAD), s * F::KS + h * F::KPL), daf[s], dps);
-            dps *= sb;
-          }
-          // tail: rows p of chi^T with k = token j in crow order (chi stored [j][sigma(p)])
-#pragma unroll
-          for (int sp = 0; sp < F::CSTEPS; ++sp) {
-            typename F::frag cf;
-            if constexpr (sizeof(T) == 2) {
-              const int L = l, g = L >> 4, s4 = L & 15;
-              const int pcol = F::sigma(pt * 32 + 16 * (g & 1) + 4 * (s4 & 3));
-              bf16x4 x0 = lds_tr4(sChi + (16 * sp + 4 * h + (s4 >> 2)) * (FB + PAD) + pcol);
-              bf16x4 x1 = lds_tr4(sChi + (16 * sp + 8 + 4 * h + (s4 >> 2)) * (FB + PAD) + pcol);
-              cf = cat44(x0, x1);
-            } else {
-              cf = sChi[crow(sp, h) * (FB + PAD) + pt * 32 + col];
-            }
-            dps = F::mma(cf, qqf[sp], dps);
-          }
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            float dl = dps[v] * accL[pt][v];
-            sc += dl;
-            dps[v] = dl * kLn2;      // paired with Omega * log2(e) below
-          }
-#pragma unroll
-          for (int sp = 0; sp < F::CSTEPS; ++sp) dlf[pt][sp] = F::cfrag(dps, sp);
-        }
-        sc = half_swap_add(sc);                      // sum_p dell_cp for anchor col
-        if (h == 0) sScr[DVA + col] = valid ? sc : 0.0f;
-        wave_lds_sync();
-        // dz[c, D] = Omega^T dell_c - s_c z_c  (lanes <-> D, regs <-> anchor)
-        auto rmap = [&](int ar) { return ringrow(i - 32 * an - ar); };
-#pragma unroll 1
-        for (int Dt = 0; Dt < D / 32; ++Dt) {
-          no_hoist();
-          f32x16 dz = zero16();
-#pragma unroll
-          for (int pt = 0; pt < FB / 32; ++pt)
-#pragma unroll
-            for (int sp = 0; sp < F::CSTEPS; ++sp)
-              dz = F::mma(dlf[pt][sp], F::tld_crow(sOm, D + PAD, pt * 32, sp, Dt * 32), dz);
-          // r[c][D] for the registers' anchors, via the same transposed read
-          float rv[16];
-#pragma unroll
-          for (int sp = 0; sp < F::CSTEPS; ++sp) {
-            typename F::frag rf = F::tld_crow_map(sR, D + PAD, sp, Dt * 32, rmap);
-            if constexpr (sizeof(T) == 2) {
-#pragma unroll
-              for (int e = 0; e < 8; ++e) rv[8 * sp + e] = fel(rf, e);
-            } else {
-              rv[sp] = rf;
-            }
-          }
-          const float qd = pick(qD, Dt);
-          const float* sch = sScr + DVA + 4 * h;
-          float dqs = 0.0f;
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const f32x4 s4 = *(const f32x4*)(sch + 8 * g);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const int v = 4 * g + e;
-              const int ar = 8 * g + 4 * h + e;
-              float dzz = dz[v] - s4[e] * qd * rv[v];
-              dqs += dzz * rv[v];
-              if (32 * an + ar < w && i - 32 * an - ar >= 0)
-                atomicAdd(sWin + rmap(ar) * D + Dt * 32 + col, dzz * qd);
-            }
-          }
-          add_at(dqacc, Dt, dqs);
-        }
-      }
-#pragma unroll
-      for (int Dt = 0; Dt < D / 32; ++Dt) {
-        float dq = half_swap_add(dqacc[Dt]);
-        if (h == 0) dq32[(size_t)i * D + Dt * 32 + col] = dq;
+        dqs = half_swap_add(dqs);
+        if (h == 0) dqo[Dt * 32 + col] = dqs;
       }
     }
   }
-  __syncthreads();
-  for (int idx = tid; idx < RING * D; idx += NT) {
-    int rr = idx / D, d = idx % D;
-    int c = st1 * BS - RING + rr;
-    if (c >= 0 && c < n && c >= S0 - (32 * NA - 1) && c < S1) {
-      float x = sWin[ringrow(c) * D + d];
-      bool edge = (c < S0) || (c + w - 1 >= S1 && S1 < n);
-      if (edge) atomicAdd(dr32 + (size_t)c * D + d, x);
-      else dr32[(size_t)c * D + d] = x;
-    }
+  reduce_waves<D / 32>(dr, (float*)smem, wv, NW);
+  if (wv == 0) {
+#pragma unroll
+    for (int Dt = 0; Dt < D / 32; ++Dt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int c = c0 + crow(v, h);
+        if (c >= n) continue;
+        if constexpr (C::NFB == 1) ((T*)a.dr)[(seq + c) * D + Dt * 32 + col] = (T)dr[Dt][v];
+        else a.dr32[(((size_t)fb * a.BH + bh) * n + c) * D + Dt * 32 + col] = dr[Dt][v];
+      }
   }
+}
+
+// dq of every row: sum over feature blocks and over the anchor tiles that
+// processed it (tile k = chunk(i) - slot, processed iff k >= 0 and i - 32k <= w + 30)
+template <typename T>
+__global__ __launch_bounds__(256) void k_bwd_final_dq(const float* __restrict__ src, T* __restrict__ dst,
+                                                      int BH, int n, int D, int nfb, int NS, int w) {
+  const size_t count = (size_t)BH * n * D;
+  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= count) return;
+  const int i = (int)((idx / D) % n);
+  const int bi = i >> 5;
+  float acc = 0.0f;
+  for (int fb = 0; fb < nfb; ++fb)
+    for (int s = 0; s < NS; ++s) {
+      const int k = bi - s;
+      if (k < 0 || i - 32 * k > w + 30) continue;
+      acc += src[((size_t)fb * NS + s) * count + idx];
+    }
+  dst[idx] = (T)acc;
 }
 
 // ---------------------------------------------------------------------------
@@ -1147,33 +1111,26 @@ static int launch_err(const char* what) {
 
 template <typename T, int D, int DV, int M, int NA>
 static int run_bwd(const Shape& s, BwdArgs a, hipStream_t st) {
-  using Q = QCfg<T, D, DV, M, NA>;
-  constexpr int NFB = Q::NFB;
+  using A = AsCfg<T, D, DV, M, NA>;
+  constexpr int NFB = A::NFB;
+  constexpr int NS = NA + 1;
   const int BH = (int)s.BH();
+  const int nch = (int)s.nch();
   const size_t rows = (size_t)BH * s.n;
   {
-    size_t z4 = (rows * (DV + DV + D + D) * NFB) / 4;     // du32, dvin, dr32, dq32 are contiguous
     ProfScope ps("bwd_prep", st);
-    k_fill_zero<<<(unsigned)((z4 + 255) / 256), 256, 0, st>>>(a.du32, z4);
     k_bwd_rowprep<T, DV><<<(unsigned)((rows + 7) / 8), 256, 0, st>>>(a);
+    k_bwd_keyfeat<T, D, M><<<dim3((nch + 3) / 4, BH), 256, 0, st>>>(a);
   }
-  // query sweeps over segments of seg_steps 16-row steps
-  const int nsteps = (int)((s.n + Q::BS - 1) / Q::BS);
-  const long target = 1024;
-  int seg = (int)(((long)nsteps * BH * NFB + target - 1) / target);
-  if (seg < 4) seg = 4;
-  if (seg > nsteps) seg = nsteps;
-  a.seg_steps = seg;
-  const int nseg = (nsteps + seg - 1) / seg;
+  if (int rc = launch_err("prep")) return rc;
   { ProfScope ps("bwd_du", st);
-  k_bwd_du<T, D, DV, M, NA><<<dim3(nseg, BH, NFB), 64 * Q::NW, 0, st>>>(a);
+  k_bwd_du<T, D, DV, M, NA><<<dim3(nch, BH, NFB), 64 * A::NW, 0, st>>>(a);
   }
   if (int rc = launch_err("du")) return rc;
   { ProfScope ps("bwd_dqdr", st);
-  k_bwd_dqdr<T, D, DV, M, NA><<<dim3(nseg, BH, NFB), 64 * Q::NW, 0, st>>>(a);
+  k_bwd_dqdr<T, D, DV, M, NA><<<dim3(nch, BH, NFB), 64 * A::NW, 0, st>>>(a);
   }
   if (int rc = launch_err("dqdr")) return rc;
-  const int nch = (int)s.nch();
   { ProfScope ps("bwd_state", st);
   k_bwd_state<T, D, DV, M, NA><<<dim3(nch, BH, NFB), 64 * StCfg<T, D, DV, M, NA>::NW, 0, st>>>(a);
   }
@@ -1187,9 +1144,11 @@ static int run_bwd(const Shape& s, BwdArgs a, hipStream_t st) {
   }
   if (int rc = launch_err("keys")) return rc;
   ProfScope psf("bwd_final", st);
-  k_bwd_final<T><<<(unsigned)((rows * DV + 255) / 256), 256, 0, st>>>(a.du32, (T*)a.du, rows * DV, NFB);
-  k_bwd_final<T><<<(unsigned)((rows * D + 255) / 256), 256, 0, st>>>(a.dr32, (T*)a.dr, rows * D, NFB);
-  k_bwd_final<T><<<(unsigned)((rows * D + 255) / 256), 256, 0, st>>>(a.dq32, (T*)a.dq, rows * D, NFB);
+  if constexpr (NFB > 1) {
+    k_bwd_final<T><<<(unsigned)((rows * DV + 255) / 256), 256, 0, st>>>(a.du32, (T*)a.du, rows * DV, NFB);
+    k_bwd_final<T><<<(unsigned)((rows * D + 255) / 256), 256, 0, st>>>(a.dr32, (T*)a.dr, rows * D, NFB);
+  }
+  k_bwd_final_dq<T><<<(unsigned)((rows * D + 255) / 256), 256, 0, st>>>(a.dq32, (T*)a.dq, BH, (int)s.n, D, NFB, NS, s.w);
   return launch_err("final");
 }
 
@@ -1217,9 +1176,9 @@ int launch_backward(const Shape& s, const void* q, const void* k, const void* v,
   a.dout = dout; a.dq = dq; a.dk = dk; a.dv = dv; a.dr = dr; a.du = du;
   a.omq = ws.omq; a.omk = ws.omk; a.states = ws.states; a.rex = ws.rex;
   a.gst = ws.gstates; a.dchi = ws.dchi; a.dvin = ws.dvin; a.du32 = ws.du32; a.dr32 = ws.dr32;
-  a.dq32 = ws.dq32; a.rowstat = ws.rowstat;
+  a.dq32 = ws.dq32; a.rowstat = ws.rowstat; a.chi = ws.chi; a.rj = ws.rj;
   a.H = (int)s.H; a.n = (int)s.n; a.w = s.w; a.nch = (int)s.nch(); a.BH = (int)s.BH();
-  a.seg_steps = 1; a.eps = s.eps;
+  a.eps = s.eps;
   const int NA = (s.w + 31) / 32;
 #define X(T, D_, DV_, M_)                                                            \
   if (s.dtype == (sizeof(T) == 2 ? 1 : 0) && s.D == D_ && s.Dv == DV_ && s.m == M_) { \

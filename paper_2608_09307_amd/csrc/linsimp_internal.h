@@ -34,11 +34,19 @@ struct Workspace {
   float* gstates;   // [BH][nch][m*Dv + m]  per-chunk state gradients, then reverse-scanned
   float* dchi;      // [BH][n][m]           intra-chunk key-feature gradient (frame R_j)
   float* dvin;      // [nfb][BH][n][Dv]     intra-chunk value gradient
-  float* du32;      // [nfb][BH][n][Dv]     float32 accumulators of du, dr, dq
-  float* dr32;      // [nfb][BH][n][D]
-  float* dq32;      // [nfb][BH][n][D]
+  float* du32;      // [nfb][BH][n][Dv]     du per feature block (m > 128 only)
+  float* dr32;      // [nfb][BH][n][D]      dr per feature block (m > 128 only)
+  float* dq32;      // [nfb][ns][BH][n][D]  dq partial of each anchor tile (slot = row chunk - anchor tile)
+  void* chi;        // [BH][n][m] operand type: key features 2^(lambda_j - R_j)/sqrt(m), p permuted in 16-blocks
+  float* rj;        // [BH][n]              running key frame R_j (log2)
   float* rowstat;   // [BH][n][2]           per-row 1/(Z+eps) and dZ
 };
+
+// Row-side dq is summed over the anchor tiles a row sees: row i receives from
+// tiles floor(i/32) - ns + 1 .. floor(i/32), ns = ceil(w/32) + 1.
+inline int bwd_slots(int w) { return (w + kChunk - 1) / kChunk + 1; }
+// feature blocks of the backward (128 features each, fewer for m < 128)
+inline int bwd_nfb(int m) { return m > 128 ? m / 128 : 1; }
 
 size_t workspace_bytes(const Shape& s, bool backward);
 void carve(const Shape& s, void* base, bool backward, Workspace* ws);
