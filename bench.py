@@ -67,17 +67,25 @@ def src_digest():
     return h.hexdigest()[:16]
 
 
+KERNEL_SYMBOLS = {"fwd_readout": "k_readout", "bwd_du": "k_bwd_du", "bwd_dqdr": "k_bwd_dqdr",
+                  "bwd_state": "k_bwd_state", "bwd_keys": "k_bwd_keys"}
+
+
 def traffic_for(kernel):
-    """HBM bytes per launch from the committed counter runs, if they were taken
-    on the current kernel sources; else None."""
+    """Calibrated HBM bytes (FETCH_SIZE + WRITE_SIZE) per launch of `kernel`
+    from the committed counter runs, if they were taken on the current kernel
+    sources; else None."""
     try:
         with open(TRAFFIC_FILE) as fh:
             t = json.load(fh)
     except (OSError, ValueError):
         return None
-    if t.get("kernel") != kernel or t.get("src_sha") != src_digest():
+    if t.get("src_sha") != src_digest():
         return None
-    return t.get("bytes_per_launch")
+    per = t.get("per_kernel", {}).get(KERNEL_SYMBOLS.get(kernel, ""))
+    if per is None:
+        return None
+    return per["fetch_bytes"] + per["write_bytes"]
 
 
 def cpu_baseline(x, wl, budget_s):

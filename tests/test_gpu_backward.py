@@ -66,3 +66,16 @@ def test_backward_layer16k_sampled_heads():
 
 def test_backward_stress64k_sampled_head():
     _run(WORKLOADS["stress64k_m256"], pairs=[(0, 21)])
+
+
+def test_backward_bitwise_deterministic():
+    """No atomics anywhere: two backward calls give identical bits."""
+    wl = Workload("bf16_det", 1, 2, 700, 128, 128, 128, 64, "bf16", "fwdbwd", seed=33)
+    x = make_inputs(wl, device=DEV, with_grad=True)
+    out, stats = L.fwd(x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w)
+    g1 = L.bwd(x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w, out, stats, x["dO"])
+    g1 = tuple(t.clone() for t in g1)
+    g2 = L.bwd(x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w, out, stats, x["dO"])
+    torch.cuda.synchronize()
+    for nm, a_, b_ in zip(NAMES, g1, g2):
+        assert torch.equal(a_, b_), nm
