@@ -62,6 +62,12 @@ struct BwdArgs {
 
 static constexpr float kLn2 = 0.6931471805599453f;
 
+// Row padding (elements) of LDS buffers read only with ds_read_b64_tr_b16:
+// a 288-byte bf16 row (72 dwords) puts the four rows of one transposed read
+// 8 banks apart, so each 16-lane group is conflict-free.  Buffers read with
+// 16-byte row reads keep MF<T>::PAD (272-byte rows).
+template <typename T> constexpr int tr_pad() { return sizeof(T) == 2 ? 16 : 1; }
+
 // ---------------------------------------------------------------------------
 // prep: row scalars and zeroed float32 accumulators
 // ---------------------------------------------------------------------------
@@ -159,9 +165,10 @@ struct AsCfg {
   static constexpr int mx(int x, int y) { return x > y ? x : y; }
   static constexpr int oOm = 0;                                             // Omega block [p][D]
   static constexpr int oM = oOm + a16(FB * (D + PAD) * ES);                 // boundary M ([d][sigma(p)] or [p][d])
+  static constexpr int TP = tr_pad<T>();
   static constexpr int oChi = oM + a16(mx(DV * (FB + PAD), FB * (DV + PAD)) * ES);   // chi [j][sigma(p)]
-  static constexpr int oV = oChi + a16(32 * (FB + PAD) * ES);               // V [j][d]
-  static constexpr int oQ = oV + a16(32 * (DV + PAD) * ES);                 // q rows of the chunk
+  static constexpr int oV = oChi + a16(32 * (FB + TP) * ES);                // V [j][d]
+  static constexpr int oQ = oV + a16(32 * (DV + TP) * ES);                  // q rows of the chunk
   static constexpr int oR = oQ + a16(32 * (D + PAD) * ES);                  // r of the anchor tile
   static constexpr int oU = oR + a16(32 * (D + PAD) * ES);                  // u of the anchor tile
   static constexpr int oRj = oU + a16(32 * (DV + PAD) * ES);                // R_j of the chunk
@@ -300,14 +307,14 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
     if (has_bnd) {
       const float* bst = a.states + ((size_t)bh * nch + ch) * S;
       for (int idx = tid; idx < FB * (DV / 4); idx += NT) {
-        int p = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
+        int p = idx % FB, d0 = (idx / FB) * 4;
         f32x4 x = *(const f32x4*)(bst + (size_t)(fb * FB + p) * DV + d0);
 #pragma unroll
         for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = (T)x[e];
       }
     }
     copy_rows<T>(sChi, FB + PAD, chis, M, 32, FB, s0, 0, n, tid, NT);
-    copy_rows<T>(sV, DV + PAD, vs, DV, 32, DV, s0, 0, n, tid, NT);
+    copy_rows<T>(sV, DV + C::TP, vs, DV, 32, DV, s0, 0, n, tid, NT);
     copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
     for (int j = tid; j < 32; j += NT) sRj[j] = (s0 + j < n) ? a.rj[seq + s0 + j] : 0.0f;
     __syncthreads();
@@ -357,7 +364,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
         }
 #pragma unroll
         for (int sp = 0; sp < F::CSTEPS; ++sp)
-          accA = F::mma(ppf[sp], F::tld_crow(sV, DV + PAD, 0, sp, dt * 32), accA);
+          accA = F::mma(ppf[sp], F::tld_crow(sV, DV + C::TP, 0, sp, dt * 32), accA);
 #pragma unroll
         for (int v = 0; v < 16; ++v) du[dt][v] += accA[v] * dN[dt];
       }
@@ -443,7 +450,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       }
       for (int p = tid; p < FB; p += NT) sA[p] = bst[(size_t)M * DV + fb * FB + p];
     }
-    copy_rows<T>(sChi, FB + PAD, chis, M, 32, FB, s0, 0, n, tid, NT);
+    copy_rows<T>(sChi, FB + C::TP, chis, M, 32, FB, s0, 0, n, tid, NT);
     copy_rows<T>(sV, DV + PAD, vs, DV, 32, DV, s0, 0, n, tid, NT);
     copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
     for (int j = tid; j < 32; j += NT) sRj[j] = (s0 + j < n) ? a.rj[seq + s0 + j] : 0.0f;
@@ -524,11 +531,11 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
           if constexpr (sizeof(T) == 2) {
             const int g = l >> 4, s4 = l & 15;
             const int pcol = F::sigma(pt * 32 + 16 * (g & 1) + 4 * (s4 & 3));
-            bf16x4 x0 = lds_tr4(sChi + (16 * sp + 4 * h + (s4 >> 2)) * (FB + PAD) + pcol);
-            bf16x4 x1 = lds_tr4(sChi + (16 * sp + 8 + 4 * h + (s4 >> 2)) * (FB + PAD) + pcol);
+            bf16x4 x0 = lds_tr4(sChi + (16 * sp + 4 * h + (s4 >> 2)) * (FB + C::TP) + pcol);
+            bf16x4 x1 = lds_tr4(sChi + (16 * sp + 8 + 4 * h + (s4 >> 2)) * (FB + C::TP) + pcol);
             cf = cat44(x0, x1);
           } else {
-            cf = sChi[crow(sp, h) * (FB + PAD) + pt * 32 + col];
+            cf = sChi[crow(sp, h) * (FB + C::TP) + pt * 32 + col];
           }
           dps = F::mma(cf, qqf[sp], dps);
         }
@@ -643,7 +650,8 @@ struct StCfg {
   static constexpr int a16(int x) { return (x + 15) & ~15; }
   static constexpr int oR = 0;
   static constexpr int oU = oR + a16(32 * NT32 * (D + PAD) * ES);
-  static constexpr int oChi = oU + a16(WIN * (DV + PAD) * ES);
+  static constexpr int TP = tr_pad<T>();
+  static constexpr int oChi = oU + a16(WIN * (DV + TP) * ES);
   static constexpr int oNz = oChi + a16(32 * (FB + PAD) * ES);
   static constexpr int oRj = oNz + a16(32 * AW * 4);
   static constexpr int oL = oRj + a16(32 * 4);
@@ -715,7 +723,7 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
   const int pw = fb * FB + wv * 32;            // first feature of this wave's tile
 
   copy_rows<T>(sR, D + PAD, rs_, D, 32 * C::NT32, D, wb, 0, n, tid, NT);
-  copy_rows<T>(sU, DV + PAD, us, DV, WIN, DV, wb, 0, n, tid, NT);
+  copy_rows<T>(sU, DV + C::TP, us, DV, WIN, DV, wb, 0, n, tid, NT);
   if (tid < 32) sL[tid] = (s0 + tid < n) ? a.stats[(seq + s0 + tid) * 2] : 0.0f;
   __syncthreads();
   // wave 0: chunk key features and frames; the others: the |z|^2 table
@@ -825,7 +833,7 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
         auto rmap = [&](int ar) { return t + AW - 1 - 32 * an - ar; };
 #pragma unroll
         for (int sp = 0; sp < F::CSTEPS; ++sp)
-          y = F::mma(pf[an][sp], F::tld_crow_map(sU, DV + PAD, sp, dt * 32, rmap), y);
+          y = F::mma(pf[an][sp], F::tld_crow_map(sU, DV + C::TP, sp, dt * 32, rmap), y);
       }
 #pragma unroll
       for (int v = 0; v < 16; ++v) Fm[dt][v] = Fm[dt][v] * fr + y[v] * dN[dt];
@@ -929,15 +937,15 @@ __global__ __launch_bounds__(256) void k_bwd_revscan(BwdArgs a) {
 template <typename T, int D, int DV, int M>
 __global__ __launch_bounds__(256) void k_bwd_keys(BwdArgs a, int nfb) {
   using F = MF<T>;
-  constexpr int PAD = F::PAD;
+  constexpr int TP = tr_pad<T>();
   constexpr int S = M * DV + M;
-  __shared__ __align__(16) T sOm[M * (D + PAD)];
+  __shared__ __align__(16) T sOm[M * (D + TP)];
   __shared__ float sSk[4][32];
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
   const int bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch;
   const int cb = blockIdx.x * 4 + wv;
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
-  copy_rows<T>(sOm, D + PAD, omq_h, D, M, D, 0, 0, M, tid, 256);
+  copy_rows<T>(sOm, D + TP, omq_h, D, M, D, 0, 0, M, tid, 256);
   __syncthreads();
   const bool active = cb < nch;
   const int s0 = (active ? cb : nch - 1) * 32;
@@ -1035,7 +1043,7 @@ __global__ __launch_bounds__(256) void k_bwd_keys(BwdArgs a, int nfb) {
     for (int pt = 0; pt < M / 32; ++pt)
 #pragma unroll
       for (int sp = 0; sp < F::CSTEPS; ++sp)
-        dk = F::mma(dlf[pt][sp], F::tld_crow(sOm, D + PAD, pt * 32, sp, Dt * 32), dk);
+        dk = F::mma(dlf[pt][sp], F::tld_crow(sOm, D + TP, pt * 32, sp, Dt * 32), dk);
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int jj = s0 + crow(v, h);

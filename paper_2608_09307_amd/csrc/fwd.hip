@@ -80,7 +80,7 @@ __global__ __launch_bounds__(256) void k_chunk_state(FwdArgs a) {
   if (active) {
     // V^T of the chunk, token index permuted (it pairs with a register operand)
     for (int idx = l; idx < 32 * (DV / 4); idx += 64) {
-      int jj = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
+      int jj = idx % 32, d0 = (idx / 32) * 4;
       bool ok = tok0 + jj < n;
 #pragma unroll
       for (int e = 0; e < 4; ++e)
@@ -191,7 +191,7 @@ struct RCfg {
   static constexpr int FB = M < 128 ? M : 128;          // feature block (<= 128 as in Alg. 1)
   static constexpr int NFB = M / FB;
   static constexpr int WIN = BC + 32 * NA - 1;           // anchor rows the chunk can touch
-  static constexpr int UST = WIN + 1;
+  static constexpr int UST = ((WIN + 2) / 4) * 4 + 2;   // odd dword stride: conflict-free 2-byte column reads
   static constexpr int RPW = BC / NW;
   static constexpr int ES = sizeof(T);
   static constexpr int a16(int x) { return (x + 15) & ~15; }
@@ -247,8 +247,10 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
   // ---- prologue: everything else (all waves) ----
   const int fbk = blockIdx.z;
   copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fbk * FB * D, D, FB, D, 0, 0, FB, tid, NT);
+  // transposed copies: consecutive lanes take consecutive p (or j), so the
+  // 2-byte LDS writes of one instruction fall in one row
   for (int idx = tid; idx < FB * (DV / 4); idx += NT) {
-    int p = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
+    int p = idx % FB, d0 = (idx / FB) * 4;
     f32x4 x = has_bnd ? *(const f32x4*)(bst + (size_t)(fbk * FB + p) * DV + d0)
                       : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -256,7 +258,7 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
   }
   for (int p = tid; p < M; p += NT) sA[p] = has_bnd ? bst[(size_t)M * DV + p] : 0.0f;
   for (int idx = tid; idx < 32 * (DV / 4); idx += NT) {
-    int jj = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
+    int jj = idx % 32, d0 = (idx / 32) * 4;
     bool ok = s0 + jj < n;
 #pragma unroll
     for (int e = 0; e < 4; ++e)
