@@ -929,162 +929,177 @@ __global__ __launch_bounds__(256) void k_bwd_revscan(BwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// key side: per chunk (one wave), tokens j:
+// key side, per chunk b and token j (frame of the boundary gradient: Rex_{b+1}):
 //   dchi_j = 2^(R_j - Rex_{b+1}) (Ghat_b v_j + ghat_b) + dchi_intra_j
 //   dv_j   = 2^(R_j - Rex_{b+1}) Ghat_b^T chi_j + dv_intra_j
 //   dlambda = dchi (*) chi;  dk_j = Omega^T dlambda_j - (sum_p dlambda_jp) k_j
+// Four waves per chunk, two chunks per workgroup.  Phase 1: wave w forms
+// X = Ghat V^T, dchi and dlambda for feature tiles w, w+4, ... (registers <->
+// feature, lanes <-> token) and leaves dlambda and eps chi in LDS; phase 2:
+// wave w contracts them over the features for the dk / dv column tiles w, w+4, ...
 // ---------------------------------------------------------------------------
 template <typename T, int D, int DV, int M>
-__global__ __launch_bounds__(256) void k_bwd_keys(BwdArgs a, int nfb) {
+struct KCfg {
+  static constexpr int PAD = MF<T>::PAD;
+  static constexpr int TP = tr_pad<T>();
+  static constexpr int CPB = 2;                       // chunks per workgroup
+  static constexpr int WPC = 4;                       // waves per chunk
+  static constexpr int ES = sizeof(T);
+  static constexpr int a16(int x) { return (x + 15) & ~15; }
+  static constexpr int oOm = 0;                                        // Omega*log2 e [p][D]
+  static constexpr int oDL = oOm + a16(M * (D + TP) * ES);             // dlambda [c][j][p]
+  static constexpr int oCE = oDL + a16(CPB * 32 * (M + PAD) * ES);     // eps chi  [c][j][p]
+  static constexpr int oSk = oCE + a16(CPB * 32 * (M + PAD) * ES);     // sum_p dlambda partials
+  static constexpr int BYTES = oSk + a16(CPB * WPC * 32 * 4);
+};
+
+// A-operand fragment of Ghat rows (float) at k0 in the operand type, hi + lo
+template <typename T>
+LS_DEV void ghat_frag(const float* row, int k0, typename MF<T>::frag& hi, typename MF<T>::frag& lo) {
+  if constexpr (sizeof(T) == 2) {
+    const f32x4 x0 = *(const f32x4*)(row + k0), x1 = *(const f32x4*)(row + k0 + 4);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float x = e < 4 ? x0[e] : x1[e - 4];
+      hi[e] = (bf16)x;
+      lo[e] = (bf16)(x - (float)hi[e]);
+    }
+  } else {
+    hi = row[k0];
+    lo = 0.0f;
+  }
+}
+
+template <typename T, int D, int DV, int M>
+__global__ __launch_bounds__(512) void k_bwd_keys(BwdArgs a, int nfb) {
   using F = MF<T>;
-  constexpr int TP = tr_pad<T>();
+  using C = KCfg<T, D, DV, M>;
+  constexpr int PAD = C::PAD, TP = C::TP, WPC = C::WPC;
   constexpr int S = M * DV + M;
-  __shared__ __align__(16) T sOm[M * (D + TP)];
-  __shared__ float sSk[4][32];
+  static_assert(C::BYTES <= 160 * 1024, "keys LDS budget");
+  __shared__ __align__(16) char smem[C::BYTES];
+  T* sOm = (T*)(smem + C::oOm);
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
+  const int cw = wv / WPC, w = wv % WPC;              // chunk slot, wave within the chunk
+  T* sDL = (T*)(smem + C::oDL) + cw * 32 * (M + PAD);
+  T* sCE = (T*)(smem + C::oCE) + cw * 32 * (M + PAD);
+  float* sSk = (float*)(smem + C::oSk) + cw * WPC * 32;
   const int bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch;
-  const int cb = blockIdx.x * 4 + wv;
+  const int cb = blockIdx.x * C::CPB + cw;
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
-  copy_rows<T>(sOm, D + TP, omq_h, D, M, D, 0, 0, M, tid, 256);
-  __syncthreads();
-  const bool active = cb < nch;
-  const int s0 = (active ? cb : nch - 1) * 32;
+  copy_rows<T>(sOm, D + TP, omq_h, D, M, D, 0, 0, M, tid, 64 * C::CPB * WPC);
+  const bool active = cb < nch;                       // wave-uniform
+  const int cbx = active ? cb : nch - 1;
+  const int s0 = cbx * 32;
   const size_t seq = (size_t)bh * n;
   const T* ks = (const T*)a.k + seq * D;
   const T* vs = (const T*)a.v + seq * DV;
-  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
   const float* rx = a.rex + (size_t)bh * (nch + 1);
-  const int cbx = active ? cb : nch - 1;
   const float* G = a.gst + ((size_t)bh * nch + cbx) * S;    // Ghat_b [p][d], ghat [p]
   const bool has_after = cbx < nch - 1;
-  // key features (lanes <-> token, regs <-> p)
-  f32x16 acc[M / 32];
-  float nk;
-  key_logits<T, D, M, true>(acc, nk, ks, s0, n, omk_h);
   const int j = s0 + col;
-  const bool vt = j < n;
-  float mx = kNegInf;
-#pragma unroll
-  for (int pt = 0; pt < M / 32; ++pt)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      float x = vt ? acc[pt][v] - 0.5f * kLog2e * nk : kNegInf;
-      acc[pt][v] = x;
-      mx = fmaxf(mx, x);
-    }
-  mx = half_swap_max(mx);
-  float R = mx;
-#pragma unroll
-  for (int o = 1; o < 32; o <<= 1) {
-    float tt = __shfl_up(R, o, 32);
-    if (col >= o) R = fmaxf(R, tt);
-  }
-  R = fmaxf(R, rx[cbx]);
-  const float eps_j = has_after ? fast_exp2(R - rx[cbx + 1]) : 0.0f;
-  const float rsm = rsqrtf((float)M);
-#pragma unroll
-  for (int pt = 0; pt < M / 32; ++pt)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) acc[pt][v] = vt ? fast_exp2(acc[pt][v] - R) * rsm : 0.0f;
-  // dchi (lanes <-> token, regs <-> p)
+  const bool vt = active && j < n;
+  const float eps_j = (vt && has_after) ? fast_exp2(a.rj[seq + j] - rx[cbx + 1]) : 0.0f;
+
+  // ---- phase 1: per feature tile ----
   float sk = 0.0f;
-  typename F::frag dlf[M / 32][F::CSTEPS];
-  typename F::frag chf[M / 32][F::CSTEPS];
-#pragma unroll
-  for (int pt = 0; pt < M / 32; ++pt) {
+  for (int pt = w; pt < M / 32; pt += WPC) {
     f32x16 X = zero16();
     if (has_after) {
-      // X[p, j] = Ghat[p, :] . v_j  (Ghat split hi + lo for accuracy)
+      const float* grow = G + (size_t)(pt * 32 + col) * DV;
 #pragma unroll 2
       for (int s = 0; s < DV / F::KS; ++s) {
         const int k0 = s * F::KS + h * F::KPL;
-        typename F::frag vf = vt ? F::ld(vs + (size_t)j * DV, k0) : F::zero();
-        const float* gr = G + (size_t)(pt * 32 + col) * DV + k0;
-        if constexpr (sizeof(T) == 2) {
-          bf16x8 hi, lo;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            float x = gr[e];
-            hi[e] = (bf16)x;
-            lo[e] = (bf16)(x - (float)hi[e]);
-          }
-          X = F::mma(hi, vf, X);
-          X = F::mma(lo, vf, X);
-        } else {
-          X = F::mma(gr[0], vf, X);
-        }
+        typename F::frag hi, lo;
+        ghat_frag<T>(grow, k0, hi, lo);
+        const typename F::frag vf = vt ? F::ld(vs + (size_t)j * DV, k0) : F::zero();
+        X = F::mma(hi, vf, X);
+        if constexpr (sizeof(T) == 2) X = F::mma(lo, vf, X);
       }
     }
+    // registers <-> p = pt*32 + crow(v, h) (four contiguous per group g), lanes <-> token j
+    const T* chirow = (const T*)a.chi + (seq + (vt ? j : s0)) * M;
+    const float* dcrow = a.dchi + (seq + (vt ? j : s0)) * M;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int p = pt * 32 + crow(v, h);
-      float dc = 0.0f;
-      if (vt) dc = eps_j * (X[v] + (has_after ? G[(size_t)M * DV + p] : 0.0f)) + a.dchi[(seq + j) * M + p];
-      const float dl = dc * acc[pt][v];
-      sk += dl;
-      X[v] = dl * kLn2;
-    }
+    for (int g = 0; g < 4; ++g) {
+      const int p0 = pt * 32 + 8 * g + 4 * h;
+      float ch[4];
+      ld4f<T>(chirow + F::sigma(p0), ch);
+      const f32x4 di = *(const f32x4*)(dcrow + p0);
+      const f32x4 gh = has_after ? *(const f32x4*)(G + (size_t)M * DV + p0) : f32x4{0.f, 0.f, 0.f, 0.f};
+      T dl4[4], ce4[4];
 #pragma unroll
-    for (int sp = 0; sp < F::CSTEPS; ++sp) {
-      dlf[pt][sp] = F::cfrag(X, sp);
-      f32x16 cs = acc[pt] * eps_j;
-      chf[pt][sp] = F::cfrag(cs, sp);
+      for (int e = 0; e < 4; ++e) {
+        const float c = vt ? ch[e] : 0.0f;
+        const float dc = vt ? eps_j * (X[4 * g + e] + gh[e]) + di[e] : 0.0f;
+        const float dl = dc * c;
+        sk += dl;
+        dl4[e] = (T)(dl * kLn2);                      // paired with Omega * log2(e)
+        ce4[e] = (T)(c * eps_j);
+      }
+      // natural feature order in LDS (the phase-2 operands read rows j, k = p)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        sDL[col * (M + PAD) + p0 + e] = dl4[e];
+        sCE[col * (M + PAD) + p0 + e] = ce4[e];
+      }
     }
   }
   sk = half_swap_add(sk);
-  if (h == 0) sSk[wv][col] = sk;
+  if (h == 0) sSk[w * 32 + col] = sk;
   __syncthreads();
-  // dk[j, D] = sum_p dlambda[j, p] Omega[p, D] - sk_j k_j   (lanes <-> D, regs <-> j)
-#pragma unroll 1
-  for (int Dt = 0; Dt < D / 32; ++Dt) {
-    no_hoist();
+
+  // ---- phase 2a: dk column tiles (regs <-> token, lanes <-> D) ----
+  for (int Dt = w; Dt < D / 32; Dt += WPC) {
     f32x16 dk = zero16();
+#pragma unroll 2
+    for (int s = 0; s < M / F::KS; ++s) {
+      const int k0 = s * F::KS + h * F::KPL;
+      dk = F::mma(F::ld(sDL + col * (M + PAD), k0), F::tld_nat(sOm, D + TP, s * F::KS, Dt * 32), dk);
+    }
+    if (active) {
 #pragma unroll
-    for (int pt = 0; pt < M / 32; ++pt)
+      for (int v = 0; v < 16; ++v) {
+        const int jr = crow(v, h), jj = s0 + jr;
+        if (jj >= n) continue;
+        float skj = 0.0f;
 #pragma unroll
-      for (int sp = 0; sp < F::CSTEPS; ++sp)
-        dk = F::mma(dlf[pt][sp], F::tld_crow(sOm, D + TP, pt * 32, sp, Dt * 32), dk);
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int jj = s0 + crow(v, h);
-      if (active && jj < n) {
+        for (int ww = 0; ww < WPC; ++ww) skj += sSk[ww * 32 + jr];
         const int d = Dt * 32 + col;
-        float x = dk[v] - sSk[wv][crow(v, h)] * tof(ks[(size_t)jj * D + d]);
-        ((T*)a.dk)[(seq + jj) * D + d] = (T)x;
+        ((T*)a.dk)[(seq + jj) * D + d] = (T)(dk[v] - skj * tof(ks[(size_t)jj * D + d]));
       }
     }
   }
-  // dv[j, d] = sum_p (eps_j chi[j, p]) Ghat[p, d] + dv_intra  (lanes <-> d, regs <-> j)
-#pragma unroll 1
-  for (int dt = 0; dt < DV / 32; ++dt) {
-    no_hoist();
+  // ---- phase 2b: dv column tiles (regs <-> token, lanes <-> d) ----
+  for (int dt = w; dt < DV / 32; dt += WPC) {
     f32x16 dv = zero16();
     if (has_after) {
+#pragma unroll 2
+      for (int s = 0; s < M / F::KS; ++s) {
+        const int k0 = s * F::KS + h * F::KPL;
+        // B operand: Ghat rows k0 .. k0 + KPL - 1 (natural k), column dt*32 + col
+        typename F::frag hi, lo;
+        if constexpr (sizeof(T) == 2) {
 #pragma unroll
-      for (int pt = 0; pt < M / 32; ++pt)
-#pragma unroll
-        for (int sp = 0; sp < F::CSTEPS; ++sp) {
-          if constexpr (sizeof(T) == 2) {
-            bf16x8 hi, lo;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const int p = pt * 32 + 16 * sp + 8 * (e >> 2) + 4 * h + (e & 3);
-              float x = G[(size_t)p * DV + dt * 32 + col];
-              hi[e] = (bf16)x;
-              lo[e] = (bf16)(x - (float)hi[e]);
-            }
-            dv = F::mma(chf[pt][sp], hi, dv);
-            dv = F::mma(chf[pt][sp], lo, dv);
-          } else {
-            const int p = pt * 32 + crow(sp, h);
-            dv = F::mma(chf[pt][sp], G[(size_t)p * DV + dt * 32 + col], dv);
+          for (int e = 0; e < 8; ++e) {
+            const float x = G[(size_t)(k0 + e) * DV + dt * 32 + col];
+            hi[e] = (bf16)x;
+            lo[e] = (bf16)(x - (float)hi[e]);
           }
+        } else {
+          hi = G[(size_t)k0 * DV + dt * 32 + col];
+          lo = 0.0f;
         }
+        const typename F::frag cf = F::ld(sCE + col * (M + PAD), k0);
+        dv = F::mma(cf, hi, dv);
+        if constexpr (sizeof(T) == 2) dv = F::mma(cf, lo, dv);
+      }
     }
+    if (active) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int jj = s0 + crow(v, h);
-      if (active && jj < n) {
+      for (int v = 0; v < 16; ++v) {
+        const int jj = s0 + crow(v, h);
+        if (jj >= n) continue;
         const int d = dt * 32 + col;
         float x = dv[v];
         for (int b = 0; b < nfb; ++b) x += a.dvin[(((size_t)b * a.BH + bh) * n + jj) * DV + d];
@@ -1148,7 +1163,7 @@ static int run_bwd(const Shape& s, BwdArgs a, hipStream_t st) {
   k_bwd_revscan<S><<<dim3((S / 4 + 255) / 256, BH), 256, 0, st>>>(a);
   }
   { ProfScope ps("bwd_keys", st);
-  k_bwd_keys<T, D, DV, M><<<dim3((nch + 3) / 4, BH), 256, 0, st>>>(a, NFB);
+  k_bwd_keys<T, D, DV, M><<<dim3((nch + KCfg<T, D, DV, M>::CPB - 1) / KCfg<T, D, DV, M>::CPB, BH), 64 * KCfg<T, D, DV, M>::CPB * KCfg<T, D, DV, M>::WPC, 0, st>>>(a, NFB);
   }
   if (int rc = launch_err("keys")) return rc;
   ProfScope psf("bwd_final", st);

@@ -25,6 +25,10 @@ typedef bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16;
+typedef f16 f16x8 __attribute__((ext_vector_type(8)));
+typedef f16 f16x4 __attribute__((ext_vector_type(4)));
+typedef f16 f16x2 __attribute__((ext_vector_type(2)));
 
 #define LS_DEV __device__ __forceinline__
 
@@ -267,5 +271,61 @@ LS_DEV void copy_rows(T* lds, int lstride, const T* g, int gstride, int rows, in
 #pragma unroll
       for (int e = 0; e < vec; ++e) dst[e] = (T)0.0f;
     }
+  }
+}
+
+// ---- composite-query logits from f16 operands (bf16 inputs) ----
+// q, r and Omega*log2(e) are kept in LDS as f16 (converted once per row,
+// anchor window or workgroup), so z = q (*) r takes four packed f16
+// multiplies per 16-wide k-step and |z|^2 four f16 dot products with float32
+// accumulation; the logits use the f16 matrix-core instruction (same rate as
+// bf16, with 11 mantissa bits for z).  Lanes <-> anchor (z rows from rrow),
+// registers <-> feature (Omega rows pt*32 + col at row stride LD).
+// Returns |z|^2 of the lane's anchor (both wave halves).
+template <int D, int FB, int LD>
+LS_DEV float logits_f16(f32x16 (&acc)[FB / 32], const f16* qrow, const f16* rrow, const f16* om) {
+  const int l = lane_id(), col = l & 31, h = l >> 5;
+  float nz = 0.0f;
+  {
+    const int k0 = h * 8;
+    const f16x8 z = *(const f16x8*)(qrow + k0) * *(const f16x8*)(rrow + k0);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) nz = __builtin_amdgcn_fdot2(f16x2{z[2 * e], z[2 * e + 1]}, f16x2{z[2 * e], z[2 * e + 1]}, nz, false);
+#pragma unroll
+    for (int pt = 0; pt < FB / 32; ++pt)
+      acc[pt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(*(const f16x8*)(om + (pt * 32 + col) * LD + k0), z, zero16(), 0, 0, 0);
+  }
+#pragma unroll 1
+  for (int s = 1; s < D / 16; ++s) {
+    const int k0 = s * 16 + h * 8;
+    const f16x8 z = *(const f16x8*)(qrow + k0) * *(const f16x8*)(rrow + k0);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) nz = __builtin_amdgcn_fdot2(f16x2{z[2 * e], z[2 * e + 1]}, f16x2{z[2 * e], z[2 * e + 1]}, nz, false);
+#pragma unroll
+    for (int pt = 0; pt < FB / 32; ++pt)
+      acc[pt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(*(const f16x8*)(om + (pt * 32 + col) * LD + k0), z, acc[pt], 0, 0, 0);
+  }
+  return half_swap_add(nz);
+}
+
+// rows [row0, row0 + rows) of a [*, gstride] matrix (bf16 or float) into LDS
+// as f16, times `scale`; rows outside [valid_lo, valid_hi) become zero.
+template <typename Tin>
+LS_DEV void copy_rows_f16(f16* lds, int lstride, const Tin* g, int gstride, int rows, int cols, int row0,
+                          int valid_lo, int valid_hi, int tid, int nthreads, float scale = 1.0f) {
+  const int cpr = cols / 4;
+  for (int idx = tid; idx < rows * cpr; idx += nthreads) {
+    const int rr = idx / cpr, cc = (idx % cpr) * 4;
+    const int grow = row0 + rr;
+    f16x4 x;
+    if (grow >= valid_lo && grow < valid_hi) {
+      const Tin* src = g + (size_t)grow * gstride + cc;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[e] = (f16)((float)src[e] * scale);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[e] = (f16)0.0f;
+    }
+    *(f16x4*)(lds + rr * lstride + cc) = x;
   }
 }

@@ -246,7 +246,11 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
   if (wv == 0) chunk_key_features<T, D, M>(ks, s0, n, omk_h, Rexb, sChi, M + PAD, sRj);
   // ---- prologue: everything else (all waves) ----
   const int fbk = blockIdx.z;
-  copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fbk * FB * D, D, FB, D, 0, 0, FB, tid, NT);
+  if constexpr (sizeof(T) == 2)
+    copy_rows_f16<float>((f16*)sOm, D + PAD, a.omega + ((size_t)hh * M + (size_t)fbk * FB) * D, D, FB, D, 0, 0, FB,
+                         tid, NT, kLog2e);
+  else
+    copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fbk * FB * D, D, FB, D, 0, 0, FB, tid, NT);
   // transposed copies: consecutive lanes take consecutive p (or j), so the
   // 2-byte LDS writes of one instruction fall in one row
   for (int idx = tid; idx < FB * (DV / 4); idx += NT) {
@@ -264,7 +268,8 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     for (int e = 0; e < 4; ++e)
       sVt[(d0 + e) * (32 + PAD) + F::sigma(jj)] = ok ? vs[(size_t)(s0 + jj) * DV + d0 + e] : (T)0.0f;
   }
-  copy_rows<T>(sR, D + PAD, rs_, D, WIN, D, wb, 0, n, tid, NT);
+  if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sR, D + PAD, rs_, D, WIN, D, wb, 0, n, tid, NT);
+  else copy_rows<T>(sR, D + PAD, rs_, D, WIN, D, wb, 0, n, tid, NT);
   for (int idx = tid; idx < WIN * (DV / 4); idx += NT) {
     int wi = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
     int c = wb + wi;
@@ -272,7 +277,8 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) sUt[(d0 + e) * UST + wi] = ok ? us[(size_t)c * DV + d0 + e] : (T)0.0f;
   }
-  copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
+  if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
+  else copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
   __syncthreads();
 
   const int fb = blockIdx.z;       // feature block handled by this workgroup
@@ -306,30 +312,25 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
       const T* rrow = sR + wi * (D + PAD);
       // G1: log2 features of the composite queries, lanes <-> anchor, regs <-> p
       f32x16 accL[FB / 32];
+      float nz;
+      if constexpr (sizeof(T) == 2) {
+        nz = logits_f16<D, FB, D + PAD>(accL, (const f16*)qrow, (const f16*)rrow, (const f16*)sOm);
+      } else {
 #pragma unroll
-      for (int pt = 0; pt < FB / 32; ++pt) accL[pt] = zero16();
-      float nz = 0.0f;
+        for (int pt = 0; pt < FB / 32; ++pt) accL[pt] = zero16();
+        nz = 0.0f;
 #pragma unroll 2
-      for (int s = 0; s < D / F::KS; ++s) {
-        const int k0 = s * F::KS + h * F::KPL;
-        typename F::frag qf = F::ld(qrow, k0), rf = F::ld(rrow, k0), zf;
-        if constexpr (sizeof(T) == 2) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            float p = valid ? fel(qf, e) * fel(rf, e) : 0.0f;
-            nz += p * p;
-            zf[e] = (bf16)p;
-          }
-        } else {
-          float p = valid ? qf * rf : 0.0f;
+        for (int s = 0; s < D / F::KS; ++s) {
+          const int k0 = s * F::KS + h * F::KPL;
+          const float p = F::ld(qrow, k0) * F::ld(rrow, k0);
           nz += p * p;
-          zf = p;
-        }
 #pragma unroll
-        for (int pt = 0; pt < FB / 32; ++pt)
-          accL[pt] = F::mma(F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), zf, accL[pt]);
+          for (int pt = 0; pt < FB / 32; ++pt)
+            accL[pt] = F::mma(F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), p, accL[pt]);
+        }
+        nz = half_swap_add(nz);
       }
-      nz = half_swap_add(nz);
+      // invalid anchors: z is finite (zero-filled rows) and the bias removes them
       const float bias = valid ? -0.5f * kLog2e * nz : kNegInf;
       float tm = kNegInf;
 #pragma unroll
