@@ -29,6 +29,8 @@
 // The anchor sweeps are anchor-stationary: a workgroup owns 32 anchors and
 // walks the rows that see them, so du and dr are summed in registers (no
 // atomics anywhere); dq of a row is the sum of its anchor tiles' partials.
+#include <type_traits>
+
 #include "common.h"
 #include "keyfeat.h"
 #include "linsimp_internal.h"
@@ -174,7 +176,8 @@ struct AsCfg {
   static constexpr int oRj = oU + a16(32 * (DV + PAD) * ES);                // R_j of the chunk
   static constexpr int oA = oRj + a16(32 * 4);                              // boundary a
   static constexpr int oW = oA + a16(FB * 4);                               // per wave: dN (DV), s_c (32)
-  static constexpr int BYTES0 = oW + a16(NW * (DV + 32) * 4);
+  static constexpr int oOb = oW + a16(NW * (DV + 32) * 4);                 // Omega*log2 e, operand type (dz)
+  static constexpr int BYTES0 = oOb + a16(FB * (D + TP) * ES);
   static constexpr int RED = (NW / 2) * 32 * mx(DV, D) * 4;                 // end-of-sweep reduction
   static constexpr int BYTES = mx(BYTES0, RED);
 };
@@ -214,30 +217,26 @@ LS_DEV void query_features(typename MF<T>::frag (&pf)[FB / 32][MF<T>::CSTEPS], c
   constexpr int PAD = F::PAD;
   const int l = lane_id(), col = l & 31, h = l >> 5;
   f32x16 accL[FB / 32];
+  float nz;
+  if constexpr (sizeof(T) == 2) {
+    // bf16 inputs: q, r and Omega*log2(e) sit in LDS as f16 (see logits_f16)
+    nz = logits_f16<D, FB, D + PAD>(accL, (const f16*)qrow, (const f16*)rrow, (const f16*)sOm);
+  } else {
 #pragma unroll
-  for (int pt = 0; pt < FB / 32; ++pt) accL[pt] = zero16();
-  float nz = 0.0f;
+    for (int pt = 0; pt < FB / 32; ++pt) accL[pt] = zero16();
+    nz = 0.0f;
 #pragma unroll 2
-  for (int s = 0; s < D / F::KS; ++s) {
-    const int k0 = s * F::KS + h * F::KPL;
-    typename F::frag qf = F::ld(qrow, k0), rf = F::ld(rrow, k0), zf;
-    if constexpr (sizeof(T) == 2) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float p = valid ? fel(qf, e) * fel(rf, e) : 0.0f;
-        nz += p * p;
-        zf[e] = (bf16)p;
-      }
-    } else {
-      float p = valid ? qf * rf : 0.0f;
+    for (int s = 0; s < D / F::KS; ++s) {
+      const int k0 = s * F::KS + h * F::KPL;
+      const float p = F::ld(qrow, k0) * F::ld(rrow, k0);
       nz += p * p;
-      zf = p;
-    }
 #pragma unroll
-    for (int pt = 0; pt < FB / 32; ++pt)
-      accL[pt] = F::mma(F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), zf, accL[pt]);
+      for (int pt = 0; pt < FB / 32; ++pt)
+        accL[pt] = F::mma(F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), p, accL[pt]);
+    }
+    nz = half_swap_add(nz);
   }
-  nz = half_swap_add(nz);
+  // masked anchors: z is finite (zero-filled rows) and the offset removes them
   const float off = valid ? -0.5f * kLog2e * nz - Li : kNegInf;
 #pragma unroll
   for (int pt = 0; pt < FB / 32; ++pt) {
@@ -291,8 +290,14 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
   const T* chis = (const T*)a.chi + seq * M + fb * FB;
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
 
-  copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
-  copy_rows<T>(sR, D + PAD, rs_, D, 32, D, c0, 0, n, tid, NT);
+  if constexpr (sizeof(T) == 2) {
+    copy_rows_f16<float>((f16*)sOm, D + PAD, a.omega + ((size_t)hh * M + (size_t)fb * FB) * D, D, FB, D, 0, 0, FB,
+                         tid, NT, kLog2e);
+    copy_rows_f16<T>((f16*)sR, D + PAD, rs_, D, 32, D, c0, 0, n, tid, NT);
+  } else {
+    copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
+    copy_rows<T>(sR, D + PAD, rs_, D, 32, D, c0, 0, n, tid, NT);
+  }
   f32x16 du[DV / 32];
 #pragma unroll
   for (int dt = 0; dt < DV / 32; ++dt) du[dt] = zero16();
@@ -315,7 +320,8 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
     }
     copy_rows<T>(sChi, FB + PAD, chis, M, 32, FB, s0, 0, n, tid, NT);
     copy_rows<T>(sV, DV + C::TP, vs, DV, 32, DV, s0, 0, n, tid, NT);
-    copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
+    if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
+    else copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
     for (int j = tid; j < 32; j += NT) sRj[j] = (s0 + j < n) ? a.rj[seq + s0 + j] : 0.0f;
     __syncthreads();
 
@@ -426,8 +432,16 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
   const T* chis = (const T*)a.chi + seq * M + fb * FB;
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
 
-  copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
-  copy_rows<T>(sR, D + PAD, rs_, D, 32, D, c0, 0, n, tid, NT);
+  T* sOb = (T*)(smem + C::oOb);
+  copy_rows<T>(sOb, D + C::TP, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
+  if constexpr (sizeof(T) == 2) {
+    copy_rows_f16<float>((f16*)sOm, D + PAD, a.omega + ((size_t)hh * M + (size_t)fb * FB) * D, D, FB, D, 0, 0, FB,
+                         tid, NT, kLog2e);
+    copy_rows_f16<T>((f16*)sR, D + PAD, rs_, D, 32, D, c0, 0, n, tid, NT);
+  } else {
+    copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
+    copy_rows<T>(sR, D + PAD, rs_, D, 32, D, c0, 0, n, tid, NT);
+  }
   copy_rows<T>(sU, DV + PAD, us, DV, 32, DV, c0, 0, n, tid, NT);
   f32x16 dr[D / 32];
 #pragma unroll
@@ -452,7 +466,8 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
     }
     copy_rows<T>(sChi, FB + C::TP, chis, M, 32, FB, s0, 0, n, tid, NT);
     copy_rows<T>(sV, DV + PAD, vs, DV, 32, DV, s0, 0, n, tid, NT);
-    copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
+    if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
+    else copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
     for (int j = tid; j < 32; j += NT) sRj[j] = (s0 + j < n) ? a.rj[seq + s0 + j] : 0.0f;
     __syncthreads();
 
@@ -469,7 +484,8 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       const T* qrow = sQ + t * (D + PAD);
       float qD[D / 32];
 #pragma unroll
-      for (int Dt = 0; Dt < D / 32; ++Dt) qD[Dt] = tof(qrow[Dt * 32 + col]);
+      for (int Dt = 0; Dt < D / 32; ++Dt)
+        qD[Dt] = sizeof(T) == 2 ? (float)((const f16*)qrow)[Dt * 32 + col] : tof(qrow[Dt * 32 + col]);
       wave_lds_sync();
       const int c = c0 + col;
       const bool valid = (i - c >= 0) && (i - c < w);
@@ -561,13 +577,17 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
         for (int pt = 0; pt < FB / 32; ++pt)
 #pragma unroll
           for (int sp = 0; sp < F::CSTEPS; ++sp)
-            dz = F::mma(dlf[pt][sp], F::tld_crow(sOm, D + PAD, pt * 32, sp, Dt * 32), dz);
+            dz = F::mma(dlf[pt][sp], F::tld_crow(sOb, D + C::TP, pt * 32, sp, Dt * 32), dz);
         float rv[16];
 #pragma unroll
         for (int sp = 0; sp < F::CSTEPS; ++sp) {
-          typename F::frag rf = F::tld_crow(sR, D + PAD, 0, sp, Dt * 32);
+          if constexpr (sizeof(T) == 2) {
+            const f16x8 rf = tld_crow_f16((const f16*)sR, D + PAD, 0, sp, Dt * 32);
 #pragma unroll
-          for (int e = 0; e < F::KPL; ++e) rv[F::KPL * sp + e] = fel(rf, e);
+            for (int e = 0; e < 8; ++e) rv[8 * sp + e] = (float)rf[e];
+          } else {
+            rv[sp] = F::tld_crow(sR, D + PAD, 0, sp, Dt * 32);
+          }
         }
         const float qd = qD[Dt];
         const float* sch = sSc + 4 * h;
@@ -722,7 +742,8 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
   const int w = a.w;
   const int pw = fb * FB + wv * 32;            // first feature of this wave's tile
 
-  copy_rows<T>(sR, D + PAD, rs_, D, 32 * C::NT32, D, wb, 0, n, tid, NT);
+  if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sR, D + PAD, rs_, D, 32 * C::NT32, D, wb, 0, n, tid, NT);
+  else copy_rows<T>(sR, D + PAD, rs_, D, 32 * C::NT32, D, wb, 0, n, tid, NT);
   copy_rows<T>(sU, DV + C::TP, us, DV, WIN, DV, wb, 0, n, tid, NT);
   if (tid < 32) sL[tid] = (s0 + tid < n) ? a.stats[(seq + s0 + tid) * 2] : 0.0f;
   __syncthreads();
@@ -739,10 +760,21 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
 #pragma unroll 2
       for (int s = 0; s < D / F::KS; ++s) {
         const int k0 = s * F::KS + h * F::KPL;
-        typename F::frag qf = vi ? F::ld(qrow, k0) : F::zero(), rf = F::ld(rrow, k0);
+        typename F::frag qf = vi ? F::ld(qrow, k0) : F::zero();
         typename F::frag qh, ql, rh, rl;
         sq_split<T>(qf, qh, ql);
-        sq_split<T>(rf, rh, rl);
+        if constexpr (sizeof(T) == 2) {
+          // bf16 inputs: r is held as f16 (exact for bf16 values in the normal range)
+          const f16x8 r16 = *(const f16x8*)((const f16*)rrow + k0);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float x = (float)r16[e], sq = x * x;
+            rh[e] = (bf16)sq;
+            rl[e] = (bf16)(sq - (float)rh[e]);
+          }
+        } else {
+          sq_split<T>(F::ld(rrow, k0), rh, rl);
+        }
         acc = F::mma(qh, rh, acc);
         if constexpr (sizeof(T) == 2) {
           acc = F::mma(qh, rl, acc);
@@ -762,9 +794,24 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
     }
   }
   // this wave's Omega tile (log2e-scaled) as B operands, resident in registers
-  typename F::frag omf[D / F::KS];
+  // (bf16 inputs: f16 copies of Omega*log2 e, q and r; the logits use the f16 matrix cores)
+  using OF = typename std::conditional<sizeof(T) == 2, f16x8, float>::type;
+  OF omf[D / F::KS];
 #pragma unroll
-  for (int s = 0; s < D / F::KS; ++s) omf[s] = F::ld(omq_h + (size_t)(pw + col) * D, s * F::KS + h * F::KPL);
+  for (int s = 0; s < D / F::KS; ++s) {
+    const int k0 = s * F::KS + h * F::KPL;
+    if constexpr (sizeof(T) == 2) {
+      const float* orow = a.omega + ((size_t)hh * M + pw + col) * D + k0;
+      const f32x4 o0 = *(const f32x4*)orow, o1 = *(const f32x4*)(orow + 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        omf[s][e] = (f16)(o0[e] * kLog2e);
+        omf[s][4 + e] = (f16)(o1[e] * kLog2e);
+      }
+    } else {
+      omf[s] = F::ld(omq_h + (size_t)(pw + col) * D, k0);
+    }
+  }
   __syncthreads();
 
   f32x16 Fm[DV / 32];
@@ -778,7 +825,10 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
     const float inv = uniform(a.rowstat[(seq + i) * 2]);
     const float dZ = uniform(a.rowstat[(seq + i) * 2 + 1]);
     const float fr = uniform(t < tlast ? fast_exp2(sRj[t] - sRj[t + 1]) : 1.0f);
-    for (int e = l; e < D; e += 64) sQ[e] = qs[(size_t)i * D + e];
+    for (int e = l; e < D; e += 64) {
+      if constexpr (sizeof(T) == 2) ((f16*)sQ)[e] = (f16)(float)qs[(size_t)i * D + e];
+      else sQ[e] = qs[(size_t)i * D + e];
+    }
     float dN[DV / 32], vv[DV / 32];
 #pragma unroll
     for (int dt = 0; dt < DV / 32; ++dt) {
@@ -793,16 +843,18 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
 #pragma unroll
     for (int s = 0; s < D / F::KS; ++s) {
       const int k0 = s * F::KS + h * F::KPL;
-      typename F::frag qf = F::ld(sQ, k0), bq;
       if constexpr (sizeof(T) == 2) {
+        const f16x8 bq = omf[s] * *(const f16x8*)((const f16*)sQ + k0);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) bq[e] = (bf16)(fel(omf[s], e) * fel(qf, e));
+        for (int an = 0; an < NA; ++an)
+          acc[an] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+              *(const f16x8*)((const f16*)sR + (t + AW - 1 - 32 * an - col) * (D + PAD) + k0), bq, acc[an], 0, 0, 0);
       } else {
-        bq = omf[s] * qf;
-      }
+        const float bq = omf[s] * F::ld(sQ, k0);
 #pragma unroll
-      for (int an = 0; an < NA; ++an)
-        acc[an] = F::mma(F::ld(sR + (t + AW - 1 - 32 * an - col) * (D + PAD), k0), bq, acc[an]);
+        for (int an = 0; an < NA; ++an)
+          acc[an] = F::mma(F::ld(sR + (t + AW - 1 - 32 * an - col) * (D + PAD), k0), bq, acc[an]);
+      }
     }
     // psi = 2^(L + bias); bias -inf outside the window
     typename F::frag pf[NA][F::CSTEPS];
@@ -823,7 +875,12 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
 #pragma unroll
       for (int sp = 0; sp < F::CSTEPS; ++sp) pf[an][sp] = F::cfrag(acc[an], sp);
     }
-    fpart = fpart * fr + dZ * ps;
+    if (fr != 1.0f) {
+      fpart *= fr;
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt) Fm[dt] *= fr;
+    }
+    fpart += dZ * ps;
     // F <- 2^(R_t - R_{t+1}) F + (sum_c psi_c u_c^T) diag(dN)
 #pragma unroll
     for (int dt = 0; dt < DV / 32; ++dt) {
@@ -836,7 +893,7 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
           y = F::mma(pf[an][sp], F::tld_crow_map(sU, DV + C::TP, sp, dt * 32, rmap), y);
       }
 #pragma unroll
-      for (int v = 0; v < 16; ++v) Fm[dt][v] = Fm[dt][v] * fr + y[v] * dN[dt];
+      for (int v = 0; v < 16; ++v) Fm[dt][v] += y[v] * dN[dt];
     }
     // intra dchi_t[p] = F_t[p, :] . v_t + f_t[p]  (p of register col >> 1)
     float X[16];

@@ -329,3 +329,12 @@ LS_DEV void copy_rows_f16(f16* lds, int lstride, const Tin* g, int gstride, int 
     *(f16x4*)(lds + rr * lstride + cc) = x;
   }
 }
+
+// crow-order operand fragment (see MF<bf16>::tld_crow) of a 16-bit matrix
+// stored as f16; the transposing read moves raw 16-bit values
+LS_DEV f16x8 tld_crow_f16(const f16* mat, int ld, int kbase, int sp, int n0) {
+  const int h = (threadIdx.x & 63) >> 5;
+  const bf16* m = (const bf16*)mat;
+  return __builtin_bit_cast(f16x8, cat44(lds_tr4(tr_addr(m, ld, kbase + 16 * sp + 4 * h, n0)),
+                                         lds_tr4(tr_addr(m, ld, kbase + 16 * sp + 8 + 4 * h, n0))));
+}
