@@ -248,13 +248,18 @@ LS_DEV void query_features(typename MF<T>::frag (&pf)[FB / 32][MF<T>::CSTEPS], c
 }
 
 // frame ratios 2^(R_j - R_i) of the chunk tokens j <= t for the registers' rows j
+// (all sixteen computed, later tokens then zeroed: no branches around the reads)
 LS_DEV void frame_ratios(float (&sj)[16], const float* sRj, int t, float Ri) {
   const int h = lane_id() >> 5;
   const float* sRjh = sRj + 4 * h;
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int j = crow(v, h);
-    sj[v] = (j <= t) ? fast_exp2(sRjh[8 * (v >> 2) + (v & 3)] - Ri) : 0.0f;
+  for (int g = 0; g < 4; ++g) {
+    const f32x4 r4 = *(const f32x4*)(sRjh + 8 * g);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float x = fast_exp2(r4[e] - Ri);
+      sj[4 * g + e] = (8 * g + 4 * h + e <= t) ? x : 0.0f;
+    }
   }
 }
 
@@ -433,7 +438,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
 
   T* sOb = (T*)(smem + C::oOb);
-  copy_rows<T>(sOb, D + C::TP, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
+  copy_rows_as<T>(sOb, D + C::TP, a.omega + ((size_t)hh * M + (size_t)fb * FB) * D, D, FB, D, 0, 0, FB, tid, NT);
   if constexpr (sizeof(T) == 2) {
     copy_rows_f16<float>((f16*)sOm, D + PAD, a.omega + ((size_t)hh * M + (size_t)fb * FB) * D, D, FB, D, 0, 0, FB,
                          tid, NT, kLog2e);
@@ -521,7 +526,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       typename F::frag qqf[F::CSTEPS];
 #pragma unroll
       for (int sp = 0; sp < F::CSTEPS; ++sp) qqf[sp] = F::cfrag(accQ, sp);
-      // dell (natural-log derivative, times ln 2 to pair with Omega log2 e)
+      // dell = dpsi (*) psi (derivative with respect to the natural-log feature)
       typename F::frag dlf[FB / 32][F::CSTEPS];
       float sc = 0.0f;
 #pragma unroll
@@ -559,7 +564,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
         for (int v = 0; v < 16; ++v) {
           const float dl = dps[v] * fel(pf[pt][v / F::KPL], v % F::KPL);
           sc += dl;
-          dps[v] = dl * kLn2;
+          dps[v] = dl;
         }
 #pragma unroll
         for (int sp = 0; sp < F::CSTEPS; ++sp) dlf[pt][sp] = F::cfrag(dps, sp);

@@ -309,25 +309,34 @@ LS_DEV float logits_f16(f32x16 (&acc)[FB / 32], const f16* qrow, const f16* rrow
 }
 
 // rows [row0, row0 + rows) of a [*, gstride] matrix (bf16 or float) into LDS
-// as f16, times `scale`; rows outside [valid_lo, valid_hi) become zero.
-template <typename Tin>
-LS_DEV void copy_rows_f16(f16* lds, int lstride, const Tin* g, int gstride, int rows, int cols, int row0,
-                          int valid_lo, int valid_hi, int tid, int nthreads, float scale = 1.0f) {
+// as Tout (row stride lstride), times `scale`; rows outside [valid_lo,
+// valid_hi) become zero.
+template <typename Tout, typename Tin>
+LS_DEV void copy_rows_as(Tout* lds, int lstride, const Tin* g, int gstride, int rows, int cols, int row0,
+                         int valid_lo, int valid_hi, int tid, int nthreads, float scale = 1.0f) {
   const int cpr = cols / 4;
   for (int idx = tid; idx < rows * cpr; idx += nthreads) {
     const int rr = idx / cpr, cc = (idx % cpr) * 4;
     const int grow = row0 + rr;
-    f16x4 x;
+    typedef Tout V4 __attribute__((ext_vector_type(4)));
+    V4 x;
     if (grow >= valid_lo && grow < valid_hi) {
       const Tin* src = g + (size_t)grow * gstride + cc;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) x[e] = (f16)((float)src[e] * scale);
+      for (int e = 0; e < 4; ++e) x[e] = (Tout)((float)src[e] * scale);
     } else {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) x[e] = (f16)0.0f;
+      for (int e = 0; e < 4; ++e) x[e] = (Tout)0.0f;
     }
-    *(f16x4*)(lds + rr * lstride + cc) = x;
+    *(V4*)(lds + rr * lstride + cc) = x;
   }
+}
+
+// the same into f16 (q, r and Omega*log2(e) of the f16 logits)
+template <typename Tin>
+LS_DEV void copy_rows_f16(f16* lds, int lstride, const Tin* g, int gstride, int rows, int cols, int row0,
+                          int valid_lo, int valid_hi, int tid, int nthreads, float scale = 1.0f) {
+  copy_rows_as<f16, Tin>(lds, lstride, g, gstride, rows, cols, row0, valid_lo, valid_hi, tid, nthreads, scale);
 }
 
 // crow-order operand fragment (see MF<bf16>::tld_crow) of a 16-bit matrix
