@@ -210,8 +210,21 @@ LS_DEV void reduce_waves(f32x16 (&acc)[NT], float* red, int wv, int NW) {
 
 // psi[p, c] of one (row, anchor tile) pair: log2 features of z = q_i (*) r_c
 // against the block's Omega rows, shifted by L_i, masked anchors give 0.
-template <typename T, int D, int FB>
-LS_DEV void query_features(typename MF<T>::frag (&pf)[FB / 32][MF<T>::CSTEPS], const T* qrow,
+// Psi fragments are operand fragments (MF<T>::frag) where psi feeds the
+// matrix cores, or f16x8 where it only scales (psi <= 1 after the shift).
+LS_DEV void to_frag(bf16x8& f, const f32x16& acc, int sp) { f = MF<bf16>::cfrag(acc, sp); }
+LS_DEV void to_frag(float& f, const f32x16& acc, int sp) { f = MF<float>::cfrag(acc, sp); }
+LS_DEV void to_frag(f16x8& f, const f32x16& acc, int sp) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const f16x2 x = __builtin_bit_cast(f16x2, __builtin_amdgcn_cvt_pkrtz(acc[8 * sp + 2 * e], acc[8 * sp + 2 * e + 1]));
+    f[2 * e] = x[0];
+    f[2 * e + 1] = x[1];
+  }
+}
+
+template <typename T, int D, int FB, typename PF = typename MF<T>::frag>
+LS_DEV void query_features(PF (&pf)[FB / 32][MF<T>::CSTEPS], const T* qrow,
                            const T* rrow, const T* sOm, bool valid, float Li) {
   using F = MF<T>;
   constexpr int PAD = F::PAD;
@@ -243,7 +256,7 @@ LS_DEV void query_features(typename MF<T>::frag (&pf)[FB / 32][MF<T>::CSTEPS], c
 #pragma unroll
     for (int v = 0; v < 16; ++v) accL[pt][v] = fast_exp2(accL[pt][v] + off);
 #pragma unroll
-    for (int sp = 0; sp < F::CSTEPS; ++sp) pf[pt][sp] = F::cfrag(accL[pt], sp);
+    for (int sp = 0; sp < F::CSTEPS; ++sp) to_frag(pf[pt][sp], accL[pt], sp);
   }
 }
 
@@ -447,7 +460,8 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
     copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
     copy_rows<T>(sR, D + PAD, rs_, D, 32, D, c0, 0, n, tid, NT);
   }
-  copy_rows<T>(sU, DV + PAD, us, DV, 32, DV, c0, 0, n, tid, NT);
+  if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sU, DV + PAD, us, DV, 32, DV, c0, 0, n, tid, NT);
+  else copy_rows<T>(sU, DV + PAD, us, DV, 32, DV, c0, 0, n, tid, NT);
   f32x16 dr[D / 32];
 #pragma unroll
   for (int Dt = 0; Dt < D / 32; ++Dt) dr[Dt] = zero16();
@@ -494,24 +508,26 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       wave_lds_sync();
       const int c = c0 + col;
       const bool valid = (i - c >= 0) && (i - c < w);
-      typename F::frag pf[FB / 32][F::CSTEPS];
-      query_features<T, D, FB>(pf, qrow, sR + col * (D + PAD), sOm, valid, Li);
+      // psi only scales dpsi here: f16 fragments (bf16 inputs)
+      using PF = typename std::conditional<sizeof(T) == 2, f16x8, typename F::frag>::type;
+      PF pf[FB / 32][F::CSTEPS];
+      query_features<T, D, FB, PF>(pf, qrow, sR + col * (D + PAD), sOm, valid, Li);
       // dA^T fragments: lanes <-> anchor, natural d order
       const T* urow = sU + col * (DV + PAD);
       typename F::frag daf[DV / F::KS];
 #pragma unroll
       for (int s = 0; s < DV / F::KS; ++s) {
         const int k0 = s * F::KS + h * F::KPL;
-        typename F::frag uf = F::ld(urow, k0);
         if constexpr (sizeof(T) == 2) {
+          const f16x8 uf = *(const f16x8*)((const f16*)urow + k0);
           const f32x4 d0 = *(const f32x4*)(sDN + k0), d1 = *(const f32x4*)(sDN + k0 + 4);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            daf[s][e] = (bf16)(fel(uf, e) * d0[e]);
-            daf[s][4 + e] = (bf16)(fel(uf, 4 + e) * d1[e]);
+            daf[s][e] = (bf16)__builtin_fmaf((float)uf[e], d0[e], 0.0f);   // one mixed-precision FMA
+            daf[s][4 + e] = (bf16)__builtin_fmaf((float)uf[4 + e], d1[e], 0.0f);
           }
         } else {
-          daf[s] = uf * sDN[k0];
+          daf[s] = F::ld(urow, k0) * sDN[k0];
         }
       }
       // Q^T[j, c] = (v_j . dA_c + dZ_i) 2^(R_j - R_i), j <= i  (regs <-> j, lanes <-> anchor)
@@ -562,7 +578,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
         }
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const float dl = dps[v] * fel(pf[pt][v / F::KPL], v % F::KPL);
+          const float dl = __builtin_fmaf(fel(pf[pt][v / F::KPL], v % F::KPL), dps[v], 0.0f);
           sc += dl;
           dps[v] = dl;
         }

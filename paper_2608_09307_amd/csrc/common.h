@@ -166,6 +166,7 @@ template <typename T> LS_DEV T fromf(float x) { return (T)x; }
 // fragment element access as float
 LS_DEV float fel(const bf16x8& f, int e) { return (float)f[e]; }
 LS_DEV float fel(const float& f, int) { return f; }
+LS_DEV float fel(const f16x8& f, int e) { return (float)f[e]; }
 
 LS_DEV float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
