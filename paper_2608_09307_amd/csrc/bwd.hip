@@ -64,11 +64,20 @@ struct BwdArgs {
 
 static constexpr float kLn2 = 0.6931471805599453f;
 
-// Row padding (elements) of LDS buffers read only with ds_read_b64_tr_b16:
-// a 288-byte bf16 row (72 dwords) puts the four rows of one transposed read
-// 8 banks apart, so each 16-lane group is conflict-free.  Buffers read with
-// 16-byte row reads keep MF<T>::PAD (272-byte rows).
-template <typename T> constexpr int tr_pad() { return sizeof(T) == 2 ? 16 : 1; }
+// Row padding (elements) of LDS buffers read with ds_read_b64_tr_b16.  One
+// transposing read touches 8 rows x 64 bytes; it runs at full rate when the
+// row pitch is 64 or 192 bytes modulo 256 (the four rows of each 16-lane group
+// 16 dwords apart), e.g. 320-byte rows for 128 bf16 columns, against a half
+// rate at 288 bytes and a third at 272 (measured on gfx950).  16-byte row
+// reads run at the same rate for any of these pitches.
+template <typename T, int N> constexpr int tr_pad() {
+  if (sizeof(T) != 2) return 1;
+  for (int p = 0; p < 128; p += 8) {
+    const int b = (2 * (N + p)) % 256;
+    if (b == 64 || b == 192) return p;
+  }
+  return 8;
+}
 
 // ---------------------------------------------------------------------------
 // prep: row scalars and zeroed float32 accumulators
@@ -156,7 +165,7 @@ __global__ __launch_bounds__(256) void k_bwd_keyfeat(BwdArgs a) {
 // and the anchor-side sums stay in registers; the waves' sums are added once
 // at the end.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int DV, int M, int NA>
+template <typename T, int D, int DV, int M, int NA, bool DQ>
 struct AsCfg {
   static constexpr int PAD = MF<T>::PAD;
   static constexpr int FB = M < 128 ? M : 128;
@@ -167,17 +176,21 @@ struct AsCfg {
   static constexpr int mx(int x, int y) { return x > y ? x : y; }
   static constexpr int oOm = 0;                                             // Omega block [p][D]
   static constexpr int oM = oOm + a16(FB * (D + PAD) * ES);                 // boundary M ([d][sigma(p)] or [p][d])
-  static constexpr int TP = tr_pad<T>();
+  static constexpr int TPF = tr_pad<T, FB>(), TPV = tr_pad<T, DV>(), TPD = tr_pad<T, D>();
+  // row pitches: chi and r are read transposed by the dq/dr sweep, V by the du sweep
+  static constexpr int CST = DQ ? FB + TPF : FB + PAD;
+  static constexpr int VST = DQ ? DV + PAD : DV + TPV;
+  static constexpr int RST = DQ ? D + TPD : D + PAD;
   static constexpr int oChi = oM + a16(mx(DV * (FB + PAD), FB * (DV + PAD)) * ES);   // chi [j][sigma(p)]
-  static constexpr int oV = oChi + a16(32 * (FB + TP) * ES);                // V [j][d]
-  static constexpr int oQ = oV + a16(32 * (DV + TP) * ES);                  // q rows of the chunk
+  static constexpr int oV = oChi + a16(32 * CST * ES);                      // V [j][d]
+  static constexpr int oQ = oV + a16(32 * VST * ES);                        // q rows of the chunk
   static constexpr int oR = oQ + a16(32 * (D + PAD) * ES);                  // r of the anchor tile
-  static constexpr int oU = oR + a16(32 * (D + PAD) * ES);                  // u of the anchor tile
+  static constexpr int oU = oR + a16(32 * RST * ES);                        // u of the anchor tile
   static constexpr int oRj = oU + a16(32 * (DV + PAD) * ES);                // R_j of the chunk
   static constexpr int oA = oRj + a16(32 * 4);                              // boundary a
   static constexpr int oW = oA + a16(FB * 4);                               // per wave: dN (DV), s_c (32)
   static constexpr int oOb = oW + a16(NW * (DV + 32) * 4);                 // Omega*log2 e, operand type (dz)
-  static constexpr int BYTES0 = oOb + a16(FB * (D + TP) * ES);
+  static constexpr int BYTES0 = DQ ? oOb + a16(FB * (D + TPD) * ES) : oOb;
   static constexpr int RED = (NW / 2) * 32 * mx(DV, D) * 4;                 // end-of-sweep reduction
   static constexpr int BYTES = mx(BYTES0, RED);
 };
@@ -283,7 +296,7 @@ LS_DEV void frame_ratios(float (&sj)[16], const float* sRj, int t, float Ri) {
 template <typename T, int D, int DV, int M, int NA>
 __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
   using F = MF<T>;
-  using C = AsCfg<T, D, DV, M, NA>;
+  using C = AsCfg<T, D, DV, M, NA, false>;
   constexpr int PAD = C::PAD, FB = C::FB, NW = C::NW;
   constexpr int NT = 64 * NW;
   constexpr int S = M * DV + M;
@@ -336,8 +349,8 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
         for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = (T)x[e];
       }
     }
-    copy_rows<T>(sChi, FB + PAD, chis, M, 32, FB, s0, 0, n, tid, NT);
-    copy_rows<T>(sV, DV + C::TP, vs, DV, 32, DV, s0, 0, n, tid, NT);
+    copy_rows<T>(sChi, C::CST, chis, M, 32, FB, s0, 0, n, tid, NT);
+    copy_rows<T>(sV, C::VST, vs, DV, 32, DV, s0, 0, n, tid, NT);
     if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
     else copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
     for (int j = tid; j < 32; j += NT) sRj[j] = (s0 + j < n) ? a.rj[seq + s0 + j] : 0.0f;
@@ -362,7 +375,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
       float sj[16];
       frame_ratios(sj, sRj, t, Ri);
       f32x16 accP = zero16();
-      const T* chirow = sChi + col * (FB + PAD);
+      const T* chirow = sChi + col * C::CST;
 #pragma unroll
       for (int pt = 0; pt < FB / 32; ++pt)
 #pragma unroll
@@ -388,7 +401,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
         }
 #pragma unroll
         for (int sp = 0; sp < F::CSTEPS; ++sp)
-          accA = F::mma(ppf[sp], F::tld_crow(sV, DV + C::TP, 0, sp, dt * 32), accA);
+          accA = F::mma(ppf[sp], F::tld_crow(sV, C::VST, 0, sp, dt * 32), accA);
 #pragma unroll
         for (int v = 0; v < 16; ++v) du[dt][v] += accA[v] * dN[dt];
       }
@@ -419,7 +432,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
 template <typename T, int D, int DV, int M, int NA>
 __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
   using F = MF<T>;
-  using C = AsCfg<T, D, DV, M, NA>;
+  using C = AsCfg<T, D, DV, M, NA, true>;
   constexpr int PAD = C::PAD, FB = C::FB, NW = C::NW;
   constexpr int NT = 64 * NW;
   constexpr int S = M * DV + M;
@@ -451,14 +464,14 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
 
   T* sOb = (T*)(smem + C::oOb);
-  copy_rows_as<T>(sOb, D + C::TP, a.omega + ((size_t)hh * M + (size_t)fb * FB) * D, D, FB, D, 0, 0, FB, tid, NT);
+  copy_rows_as<T>(sOb, D + C::TPD, a.omega + ((size_t)hh * M + (size_t)fb * FB) * D, D, FB, D, 0, 0, FB, tid, NT);
   if constexpr (sizeof(T) == 2) {
     copy_rows_f16<float>((f16*)sOm, D + PAD, a.omega + ((size_t)hh * M + (size_t)fb * FB) * D, D, FB, D, 0, 0, FB,
                          tid, NT, kLog2e);
-    copy_rows_f16<T>((f16*)sR, D + PAD, rs_, D, 32, D, c0, 0, n, tid, NT);
+    copy_rows_f16<T>((f16*)sR, C::RST, rs_, D, 32, D, c0, 0, n, tid, NT);
   } else {
     copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
-    copy_rows<T>(sR, D + PAD, rs_, D, 32, D, c0, 0, n, tid, NT);
+    copy_rows<T>(sR, C::RST, rs_, D, 32, D, c0, 0, n, tid, NT);
   }
   if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sU, DV + PAD, us, DV, 32, DV, c0, 0, n, tid, NT);
   else copy_rows<T>(sU, DV + PAD, us, DV, 32, DV, c0, 0, n, tid, NT);
@@ -483,15 +496,28 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       }
       for (int p = tid; p < FB; p += NT) sA[p] = bst[(size_t)M * DV + fb * FB + p];
     }
-    copy_rows<T>(sChi, FB + C::TP, chis, M, 32, FB, s0, 0, n, tid, NT);
-    copy_rows<T>(sV, DV + PAD, vs, DV, 32, DV, s0, 0, n, tid, NT);
+    copy_rows<T>(sChi, C::CST, chis, M, 32, FB, s0, 0, n, tid, NT);
+    copy_rows<T>(sV, C::VST, vs, DV, 32, DV, s0, 0, n, tid, NT);
     if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
     else copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
     for (int j = tid; j < 32; j += NT) sRj[j] = (s0 + j < n) ? a.rj[seq + s0 + j] : 0.0f;
     __syncthreads();
 
+    // upstream-gradient rows are fetched one row ahead
+    constexpr int NG = (DV + 63) / 64;
+    float gpre[NG];
+    auto load_g = [&](int t) {
+      const size_t i = (size_t)min(s0 + t, n - 1);
+#pragma unroll
+      for (int e = 0; e < NG; ++e) gpre[e] = (e * 64 + l < DV) ? tof(gs[i * DV + e * 64 + l]) : 0.0f;
+    };
+    load_g(wv);
 #pragma unroll 1
     for (int t = wv; t < 32; t += NW) {
+      float gv[NG];
+#pragma unroll
+      for (int e = 0; e < NG; ++e) gv[e] = gpre[e];
+      if (t + NW < 32) load_g(t + NW);
       const int i = s0 + t;
       if (i >= n || i < c0 || i - c0 > w + 30) continue;
       const float Li = uniform(a.stats[(seq + i) * 2]);
@@ -499,7 +525,9 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       const float dZ = uniform(a.rowstat[(seq + i) * 2 + 1]);
       const float Ri = uniform(sRj[t]);
       const float sb = uniform(has_bnd ? fast_exp2(Rexb - Ri) : 0.0f);
-      for (int d = l; d < DV; d += 64) sDN[d] = tof(gs[(size_t)i * DV + d]) * inv;
+#pragma unroll
+      for (int e = 0; e < NG; ++e)
+        if (e * 64 + l < DV) sDN[e * 64 + l] = gv[e] * inv;
       const T* qrow = sQ + t * (D + PAD);
       float qD[D / 32];
 #pragma unroll
@@ -511,7 +539,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       // psi only scales dpsi here: f16 fragments (bf16 inputs)
       using PF = typename std::conditional<sizeof(T) == 2, f16x8, typename F::frag>::type;
       PF pf[FB / 32][F::CSTEPS];
-      query_features<T, D, FB, PF>(pf, qrow, sR + col * (D + PAD), sOm, valid, Li);
+      query_features<T, D, FB, PF>(pf, qrow, sR + col * (C::RST), sOm, valid, Li);
       // dA^T fragments: lanes <-> anchor, natural d order
       const T* urow = sU + col * (DV + PAD);
       typename F::frag daf[DV / F::KS];
@@ -534,7 +562,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       f32x16 accQ = zero16();
 #pragma unroll
       for (int s = 0; s < DV / F::KS; ++s)
-        accQ = F::mma(F::ld(sV + col * (DV + PAD), s * F::KS + h * F::KPL), daf[s], accQ);
+        accQ = F::mma(F::ld(sV + col * C::VST, s * F::KS + h * F::KPL), daf[s], accQ);
       float sj[16];
       frame_ratios(sj, sRj, t, Ri);
 #pragma unroll
@@ -568,11 +596,11 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
           if constexpr (sizeof(T) == 2) {
             const int g = l >> 4, s4 = l & 15;
             const int pcol = F::sigma(pt * 32 + 16 * (g & 1) + 4 * (s4 & 3));
-            bf16x4 x0 = lds_tr4(sChi + (16 * sp + 4 * h + (s4 >> 2)) * (FB + C::TP) + pcol);
-            bf16x4 x1 = lds_tr4(sChi + (16 * sp + 8 + 4 * h + (s4 >> 2)) * (FB + C::TP) + pcol);
+            bf16x4 x0 = lds_tr4(sChi + (16 * sp + 4 * h + (s4 >> 2)) * (C::CST) + pcol);
+            bf16x4 x1 = lds_tr4(sChi + (16 * sp + 8 + 4 * h + (s4 >> 2)) * (C::CST) + pcol);
             cf = cat44(x0, x1);
           } else {
-            cf = sChi[crow(sp, h) * (FB + C::TP) + pt * 32 + col];
+            cf = sChi[crow(sp, h) * (C::CST) + pt * 32 + col];
           }
           dps = F::mma(cf, qqf[sp], dps);
         }
@@ -598,16 +626,16 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
         for (int pt = 0; pt < FB / 32; ++pt)
 #pragma unroll
           for (int sp = 0; sp < F::CSTEPS; ++sp)
-            dz = F::mma(dlf[pt][sp], F::tld_crow(sOb, D + C::TP, pt * 32, sp, Dt * 32), dz);
+            dz = F::mma(dlf[pt][sp], F::tld_crow(sOb, D + C::TPD, pt * 32, sp, Dt * 32), dz);
         float rv[16];
 #pragma unroll
         for (int sp = 0; sp < F::CSTEPS; ++sp) {
           if constexpr (sizeof(T) == 2) {
-            const f16x8 rf = tld_crow_f16((const f16*)sR, D + PAD, 0, sp, Dt * 32);
+            const f16x8 rf = tld_crow_f16((const f16*)sR, C::RST, 0, sp, Dt * 32);
 #pragma unroll
             for (int e = 0; e < 8; ++e) rv[8 * sp + e] = (float)rf[e];
           } else {
-            rv[sp] = F::tld_crow(sR, D + PAD, 0, sp, Dt * 32);
+            rv[sp] = F::tld_crow(sR, C::RST, 0, sp, Dt * 32);
           }
         }
         const float qd = qD[Dt];
@@ -691,7 +719,13 @@ struct StCfg {
   static constexpr int a16(int x) { return (x + 15) & ~15; }
   static constexpr int oR = 0;
   static constexpr int oU = oR + a16(32 * NT32 * (D + PAD) * ES);
-  static constexpr int TP = tr_pad<T>();
+  // bytes after the u window (rows of pitch DV + tp)
+  static constexpr int tail(int tp) {
+    return a16(WIN * (DV + tp) * ES) + a16(32 * (FB + PAD) * ES) + a16(32 * AW * 4) + 2 * a16(32 * 4) +
+           a16(NW * D * ES) + a16(NW * RB * DV * 4);
+  }
+  // full-rate transposing reads of u when two workgroups still fit a CU
+  static constexpr int TP = (oU + tail(tr_pad<T, DV>()) <= 80 * 1024 || sizeof(T) != 2) ? tr_pad<T, DV>() : 16;
   static constexpr int oChi = oU + a16(WIN * (DV + TP) * ES);
   static constexpr int oNz = oChi + a16(32 * (FB + PAD) * ES);
   static constexpr int oRj = oNz + a16(32 * AW * 4);
@@ -1019,7 +1053,7 @@ __global__ __launch_bounds__(256) void k_bwd_revscan(BwdArgs a) {
 template <typename T, int D, int DV, int M>
 struct KCfg {
   static constexpr int PAD = MF<T>::PAD;
-  static constexpr int TP = tr_pad<T>();
+  static constexpr int TP = tr_pad<T, D>();
   static constexpr int CPB = 2;                       // chunks per workgroup
   static constexpr int WPC = 4;                       // waves per chunk
   static constexpr int ES = sizeof(T);
@@ -1212,7 +1246,7 @@ static int launch_err(const char* what) {
 
 template <typename T, int D, int DV, int M, int NA>
 static int run_bwd(const Shape& s, BwdArgs a, hipStream_t st) {
-  using A = AsCfg<T, D, DV, M, NA>;
+  using A = AsCfg<T, D, DV, M, NA, true>;
   constexpr int NFB = A::NFB;
   constexpr int NS = NA + 1;
   const int BH = (int)s.BH();
