@@ -16,9 +16,12 @@ Each function cites the passage of the paper it writes out:
 * ``montecarlo`` -- Lemma 1 (unbiasedness) and the closed-form variance of the
                     random-feature kernel estimate.
 * ``features``   -- the orthogonal random-feature bank of App. B.1.
+* ``layer``      -- the full head around the core: L2 normalisation and the
+                    query temperature (Sec. 3.1), the gated RMSNorm output
+                    (eq:gated-output) and the channel-wise gate variant.
 
 Reading conventions (where the paper is silent or ambiguous) are listed in
 the module docstring of ``linsimp``.
 """
 
-from . import linsimp, brute, montecarlo, features  # noqa: F401
+from . import linsimp, brute, montecarlo, features, layer  # noqa: F401
