@@ -102,11 +102,15 @@ def _l2_backward(x, dxh, norm_eps):
 
 
 def head_backward(q, k, v, r, u, Omega, w, tau, gate, dy, norm_eps=NORM_EPS, rms_eps=RMS_EPS,
-                  eps=linsimp.EPS):
+                  eps=linsimp.EPS, parts=None):
     """Exact gradient of sum(dy * y) for one head.
 
     Returns (dq, dk, dv, dr, du, dtau, dgate): dgate is a float (d gamma) for
     the per-head gate and an [n, Dv] array (d logits) for the channel-wise one.
+    If ``parts`` is a dict it receives the two inner products behind dtau and
+    dgamma as their factors: q_hat and the core gradient of the scaled query
+    (dtau = sum q_hat * dq_core), and dy and o_hat g (1 - g) (dgamma = their sum
+    of products).
     """
     q, k, v, r, u, Omega, dy = _f64(q, k, v, r, u, Omega, dy)
     qh, _ = l2_normalize(q, norm_eps)
@@ -126,6 +130,8 @@ def head_backward(q, k, v, r, u, Omega, w, tau, gate, dy, norm_eps=NORM_EPS, rms
     dqc, dkh, dv, drh, du = linsimp.backward(tau * qh, kh, v, rh, u, Omega, w, dot, eps)
     # temperature and L2 normalisation
     dtau = float(np.sum(qh * dqc))
+    if parts is not None:
+        parts.update(q_hat=qh, dq_core=dqc, dy=dy, gate_factor=oh * g * (1.0 - g))
     dq = _l2_backward(q, tau * dqc, norm_eps)
     dk = _l2_backward(k, dkh, norm_eps)
     dr = _l2_backward(r, drh, norm_eps)

@@ -1,6 +1,8 @@
 // C ABI of the LinSimp library: argument validation, workspace carving and
-// dispatch to the HIP kernels.  Declarations and contracts: include/linsimp.h.
+// dispatch to the HIP kernels.  Declarations and contracts: include/linsimp.h
+// (the core) and include/linsimp_head.h (the full head around it).
 #include "../../include/linsimp.h"
+#include "../../include/linsimp_head.h"
 
 #include <stdarg.h>
 #include <stdio.h>
@@ -301,8 +303,162 @@ int linsimp_timing_read(char* names, int names_len, float* total_ms, int* counts
   return rc < 0 ? rc : nk;
 }
 
+// ---- full head (include/linsimp_head.h) ----
+}  // extern "C"
+
+namespace {
+
+// `saved` of the head: q', k', r' [BH n D], o~ [BH n Dv] (dtype), stats [BH n 2]
+// and rho [BH n] (float32), each region 256-byte aligned.
+struct HeadSaved {
+  void *qn, *kn, *rn, *ot;
+  float *stats, *rho;
+};
+
+size_t head_saved_bytes(const Shape& s, HeadSaved* hs, void* base) {
+  const size_t rows = (size_t)s.BH() * s.n;
+  const size_t es = s.esize();
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    void* p = base ? (char*)base + off : nullptr;
+    off += al(bytes);
+    return p;
+  };
+  void* qn = take(rows * s.D * es);
+  void* kn = take(rows * s.D * es);
+  void* rn = take(rows * s.D * es);
+  void* ot = take(rows * s.Dv * es);
+  float* stats = (float*)take(rows * 2 * sizeof(float));
+  float* rho = (float*)take(rows * sizeof(float));
+  if (hs) *hs = HeadSaved{qn, kn, rn, ot, stats, rho};
+  return off;
+}
+
+// backward workspace: the core's, then d o~ [BH n Dv] dtype and the per-row
+// partials [BH n] float32 of dgamma and dtau
+size_t head_ws_bytes(const Shape& s, bool backward) {
+  size_t b = al(workspace_bytes(s, backward));
+  if (backward) {
+    const size_t rows = (size_t)s.BH() * s.n;
+    b += al(rows * s.Dv * s.esize()) + 2 * al(rows * sizeof(float));
+  }
+  return b;
+}
+
+int check_head(const linsimp_dims* dims, const linsimp_head_opts* opts, Shape* s, bool backward) {
+  int rc = check_dims(dims, s, backward);
+  if (rc) return rc;
+  if (opts == nullptr) { set_error("opts is NULL"); return LINSIMP_E_INVALID_ARG; }
+  if (opts->gate != LINSIMP_GATE_HEAD && opts->gate != LINSIMP_GATE_CHANNEL) {
+    set_error("opts->gate %d is not a linsimp_gate_kind", opts->gate);
+    return LINSIMP_E_INVALID_ARG;
+  }
+  if (!(opts->norm_eps > 0.0f) || !(opts->rms_eps >= 0.0f)) {
+    set_error("opts: norm_eps must be > 0 and rms_eps >= 0");
+    return LINSIMP_E_INVALID_ARG;
+  }
+  const bool okw = (s->D == 32 || s->D == 64 || s->D == 128) && (s->Dv == 32 || s->Dv == 64 || s->Dv == 128);
+  if (!okw) {
+    set_error("head: D=%d Dv=%d not in {32, 64, 128}", s->D, s->Dv);
+    return LINSIMP_E_UNSUPPORTED;
+  }
+  return LINSIMP_OK;
+}
+
+int check_buf(const char* what, const void* p, size_t bytes, size_t need) {
+  if (p == nullptr || ((uintptr_t)p & 255) != 0) {
+    set_error("%s must be a non-NULL 256-byte aligned device pointer", what);
+    return LINSIMP_E_WORKSPACE;
+  }
+  if (bytes < need) {
+    set_error("%s too small: %zu bytes given, %zu needed", what, bytes, need);
+    return LINSIMP_E_WORKSPACE;
+  }
+  return LINSIMP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t linsimp_head_saved_size(const linsimp_dims* dims) {
+  Shape s;
+  linsimp_head_opts o{1e-12f, 1e-6f, LINSIMP_GATE_HEAD};
+  if (check_head(dims, &o, &s, false) != LINSIMP_OK) return 0;
+  return head_saved_bytes(s, nullptr, nullptr);
+}
+
+size_t linsimp_head_workspace_size(const linsimp_dims* dims, int for_backward) {
+  Shape s;
+  linsimp_head_opts o{1e-12f, 1e-6f, LINSIMP_GATE_HEAD};
+  if (check_head(dims, &o, &s, for_backward != 0) != LINSIMP_OK) return 0;
+  return head_ws_bytes(s, for_backward != 0);
+}
+
+int linsimp_head_fwd(const linsimp_dims* dims, const linsimp_head_opts* opts, const void* q,
+                     const void* k, const void* v, const void* r, const void* u,
+                     const float* omega, const float* tau, const void* gate, void* y, void* saved,
+                     size_t saved_bytes, void* workspace, size_t workspace_bytes_, void* stream) {
+  Shape s;
+  int rc = check_head(dims, opts, &s, false);
+  if (rc) return rc;
+  const void* ps[] = {q, k, v, r, u, omega, tau, gate, y};
+  if ((rc = check_ptrs("q,k,v,r,u,omega,tau,gate,y", ps, 9))) return rc;
+  if ((rc = check_buf("saved", saved, saved_bytes, head_saved_bytes(s, nullptr, nullptr)))) return rc;
+  if ((rc = check_buf("workspace", workspace, workspace_bytes_, head_ws_bytes(s, false)))) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  HeadSaved hs;
+  head_saved_bytes(s, &hs, saved);
+  Workspace ws;
+  carve(s, workspace, false, &ws);
+  if ((rc = launch_head_prenorm(s, q, k, r, tau, hs.qn, hs.kn, hs.rn, opts->norm_eps, st))) return rc;
+  if ((rc = launch_forward(s, hs.qn, hs.kn, v, hs.rn, u, omega, hs.ot, hs.stats, nullptr, nullptr,
+                           nullptr, ws, st)))
+    return rc;
+  return launch_head_gate(s, hs.ot, gate, opts->gate == LINSIMP_GATE_CHANNEL, y, hs.rho,
+                          opts->rms_eps, st);
+}
+
+int linsimp_head_bwd(const linsimp_dims* dims, const linsimp_head_opts* opts, const void* q,
+                     const void* k, const void* v, const void* r, const void* u,
+                     const float* omega, const float* tau, const void* gate, const void* saved,
+                     const void* dy, void* dq, void* dk, void* dv, void* dr, void* du, float* dtau,
+                     void* dgate, void* workspace, size_t workspace_bytes_, void* stream) {
+  Shape s;
+  int rc = check_head(dims, opts, &s, true);
+  if (rc) return rc;
+  const void* ps[] = {q, k, v, r, u, omega, tau, gate, dy, dq, dk, dv, dr, du, dtau, dgate};
+  if ((rc = check_ptrs("q,k,v,r,u,omega,tau,gate,dy,dq,dk,dv,dr,du,dtau,dgate", ps, 16))) return rc;
+  if (saved == nullptr || ((uintptr_t)saved & 255) != 0) {
+    set_error("saved must be the 256-byte aligned buffer linsimp_head_fwd filled");
+    return LINSIMP_E_INVALID_ARG;
+  }
+  if ((rc = check_buf("workspace", workspace, workspace_bytes_, head_ws_bytes(s, true)))) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  const bool channel = opts->gate == LINSIMP_GATE_CHANNEL;
+  HeadSaved hs;
+  head_saved_bytes(s, &hs, (void*)saved);
+  Workspace ws;
+  carve(s, workspace, true, &ws);
+  const size_t rows = (size_t)s.BH() * s.n;
+  char* tail = (char*)workspace + al(workspace_bytes(s, true));
+  void* dot = tail;
+  float* part_g = (float*)(tail + al(rows * s.Dv * s.esize()));
+  float* part_t = (float*)((char*)part_g + al(rows * sizeof(float)));
+  if ((rc = launch_head_gate_bwd(s, hs.ot, hs.rho, gate, channel, dy, dot, dgate, part_g, st))) return rc;
+  // core gradients with respect to q', k', r' land in dq, dk, dr and are
+  // turned into gradients with respect to q, k, r in place
+  if ((rc = launch_backward(s, hs.qn, hs.kn, v, hs.rn, u, omega, hs.ot, hs.stats, dot, dq, dk, dv, dr,
+                            du, ws, st)))
+    return rc;
+  if ((rc = launch_head_prenorm_bwd(s, q, k, r, tau, dq, dk, dr, part_t, opts->norm_eps, st))) return rc;
+  if ((rc = launch_head_reduce(s, part_t, dtau, st))) return rc;
+  if (!channel && (rc = launch_head_reduce(s, part_g, (float*)dgate, st))) return rc;
+  return LINSIMP_OK;
+}
+
 const char* linsimp_last_error(void) { return g_err; }
 
-int linsimp_version(void) { return 100; }
+int linsimp_version(void) { return 101; }
 
 }  // extern "C"

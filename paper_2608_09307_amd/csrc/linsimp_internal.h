@@ -70,6 +70,19 @@ int launch_decode(int64_t S, int H, int D, int Dv, int m, int w, int dtype, floa
                   const float* omega, float* M, float* a, float* rho, void* ring_r, void* ring_u,
                   int64_t* pos, void* out, hipStream_t st);
 
+// steps of the full head around the core (head.hip)
+int launch_head_prenorm(const Shape& s, const void* q, const void* k, const void* r, const float* tau,
+                        void* qn, void* kn, void* rn, float norm_eps, hipStream_t st);
+int launch_head_gate(const Shape& s, const void* ot, const void* gate, bool channel, void* y,
+                     float* rho, float rms_eps, hipStream_t st);
+int launch_head_gate_bwd(const Shape& s, const void* ot, const float* rho, const void* gate,
+                         bool channel, const void* dy, void* dot, void* dgate, float* part,
+                         hipStream_t st);
+int launch_head_prenorm_bwd(const Shape& s, const void* q, const void* k, const void* r,
+                            const float* tau, void* dq, void* dk, void* dr, float* part,
+                            float norm_eps, hipStream_t st);
+int launch_head_reduce(const Shape& s, const float* part, float* out, hipStream_t st);
+
 void set_error(const char* fmt, ...);
 bool shape_supported(const Shape& s, bool backward);
 

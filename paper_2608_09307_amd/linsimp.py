@@ -1,4 +1,5 @@
-"""Thin ctypes binding of liblinsimp.so (the C ABI in include/linsimp.h).
+"""Thin ctypes binding of liblinsimp.so (the C ABI in include/linsimp.h and
+include/linsimp_head.h).
 
 Argument marshalling only: torch tensors are turned into device pointers and
 the current HIP stream is passed through.  Every step of the computation runs
@@ -33,9 +34,18 @@ class Dims(ctypes.Structure):
                 ("w", ctypes.c_int32), ("dtype", ctypes.c_int32), ("eps", ctypes.c_float)]
 
 
+class HeadOpts(ctypes.Structure):
+    _fields_ = [("norm_eps", ctypes.c_float), ("rms_eps", ctypes.c_float), ("gate", ctypes.c_int32)]
+
+
+GATE_HEAD, GATE_CHANNEL = 0, 1
+NORM_EPS, RMS_EPS = 1e-12, 1e-6
+
 EXPORTS = ("linsimp_workspace_size", "linsimp_fwd", "linsimp_bwd", "linsimp_prefill",
            "linsimp_decode_step", "linsimp_timing_enable", "linsimp_timing_read",
            "linsimp_last_error", "linsimp_version")
+HEAD_EXPORTS = ("linsimp_head_saved_size", "linsimp_head_workspace_size", "linsimp_head_fwd",
+                "linsimp_head_bwd")
 
 
 def lib_path() -> str:
@@ -71,6 +81,15 @@ def lib():
     L.linsimp_last_error.restype = ctypes.c_char_p
     L.linsimp_version.argtypes = []
     L.linsimp_version.restype = ctypes.c_int
+    po = ctypes.POINTER(HeadOpts)
+    L.linsimp_head_saved_size.argtypes = [pd]
+    L.linsimp_head_saved_size.restype = sz
+    L.linsimp_head_workspace_size.argtypes = [pd, ctypes.c_int]
+    L.linsimp_head_workspace_size.restype = sz
+    L.linsimp_head_fwd.argtypes = [pd, po] + [vp] * 10 + [sz, vp, sz, vp]
+    L.linsimp_head_fwd.restype = ctypes.c_int
+    L.linsimp_head_bwd.argtypes = [pd, po] + [vp] * 17 + [vp, sz, vp]
+    L.linsimp_head_bwd.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -215,3 +234,73 @@ def decode_step(state, q, k, v, r, u, omega, w, eps=EPS, out=None):
                                      _ptr(state["ring_u"], "ring_u"), _ptr(state["pos"], "pos"),
                                      _ptr(out, "out"), _stream()))
     return out
+
+
+# ---------------------------------------------------------------------------
+# Full head (include/linsimp_head.h)
+# ---------------------------------------------------------------------------
+
+def _aligned_bytes(nbytes: int, device) -> torch.Tensor:
+    buf = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+    off = (-buf.data_ptr()) % 256
+    return buf[off: off + nbytes]
+
+
+def head_opts(gate_kind=GATE_HEAD, norm_eps=NORM_EPS, rms_eps=RMS_EPS) -> HeadOpts:
+    return HeadOpts(norm_eps, rms_eps, gate_kind)
+
+
+def _gate_kind(gate: torch.Tensor, v: torch.Tensor) -> int:
+    return GATE_CHANNEL if gate.dim() == 4 else GATE_HEAD
+
+
+def head_fwd(q, k, v, r, u, omega, w, tau, gate, eps=EPS, norm_eps=NORM_EPS, rms_eps=RMS_EPS,
+             y=None, saved=None, workspace=None):
+    """Forward of one full head; returns (y, saved).  ``gate`` is gamma [H]
+    float32 (per-head gate) or logits [B, H, n, Dv] (channel-wise gate).
+    See linsimp_head_fwd."""
+    d = dims_of(q, v, omega, w, eps)
+    o = head_opts(_gate_kind(gate, v), norm_eps, rms_eps)
+    L = lib()
+    if y is None:
+        y = torch.empty(q.shape[:3] + (v.shape[-1],), dtype=q.dtype, device=q.device)
+    if saved is None:
+        nb = int(L.linsimp_head_saved_size(ctypes.byref(d)))
+        if nb == 0:
+            _check(-2)
+        saved = _aligned_bytes(nb, q.device)
+    if workspace is None:
+        nb = int(L.linsimp_head_workspace_size(ctypes.byref(d), 0))
+        if nb == 0:
+            _check(-2)
+        workspace = _aligned_bytes(nb, q.device)
+    _check(L.linsimp_head_fwd(ctypes.byref(d), ctypes.byref(o), _ptr(q, "q"), _ptr(k, "k"),
+                              _ptr(v, "v"), _ptr(r, "r"), _ptr(u, "u"), _ptr(omega, "omega"),
+                              _ptr(tau, "tau"), _ptr(gate, "gate"), _ptr(y, "y"),
+                              _ptr(saved, "saved"), saved.numel(), _ptr(workspace, "workspace"),
+                              workspace.numel(), _stream()))
+    return y, saved
+
+
+def head_bwd(q, k, v, r, u, omega, w, tau, gate, saved, dy, eps=EPS, norm_eps=NORM_EPS,
+             rms_eps=RMS_EPS, workspace=None):
+    """Backward of one full head; returns (dq, dk, dv, dr, du, dtau, dgate).
+    See linsimp_head_bwd."""
+    d = dims_of(q, v, omega, w, eps)
+    o = head_opts(_gate_kind(gate, v), norm_eps, rms_eps)
+    L = lib()
+    grads = [torch.empty_like(x) for x in (q, k, v, r, u)]
+    dtau = torch.empty_like(tau)
+    dgate = torch.empty_like(gate)
+    if workspace is None:
+        nb = int(L.linsimp_head_workspace_size(ctypes.byref(d), 1))
+        if nb == 0:
+            _check(-2)
+        workspace = _aligned_bytes(nb, q.device)
+    _check(L.linsimp_head_bwd(ctypes.byref(d), ctypes.byref(o), _ptr(q, "q"), _ptr(k, "k"),
+                              _ptr(v, "v"), _ptr(r, "r"), _ptr(u, "u"), _ptr(omega, "omega"),
+                              _ptr(tau, "tau"), _ptr(gate, "gate"), _ptr(saved, "saved"),
+                              _ptr(dy, "dy"), *[_ptr(g, "grad") for g in grads],
+                              _ptr(dtau, "dtau"), _ptr(dgate, "dgate"),
+                              _ptr(workspace, "workspace"), workspace.numel(), _stream()))
+    return (*grads, dtau, dgate)

@@ -102,6 +102,21 @@ def make_inputs(wl: Workload, device="cpu", with_grad: Optional[bool] = None):
     return out
 
 
+def make_head_params(wl: Workload, device="cpu", channel_gate: bool = False):
+    """Per-head parameters of the full head, from their own generator (seed
+    + 7919, so the streams of ``make_inputs`` are unchanged): tau [H] float32
+    around the paper's initial sqrt(D) (times exp(0.1 N(0,1))), and either
+    gamma [H] float32 around the initial -2 (plus 0.5 N(0,1)) or channel-gate
+    logits [B, H, n, Dv] (N(0,1), workload dtype)."""
+    g = _gen(device, wl.seed + 7919)
+    tau = torch.exp(0.1 * _normal((wl.H,), g, device)) * wl.D ** 0.5
+    if channel_gate:
+        gate = _normal((wl.B, wl.H, wl.n, wl.Dv), g, device).to(wl.torch_dtype)
+    else:
+        gate = -2.0 + 0.5 * _normal((wl.H,), g, device)
+    return {"tau": tau, "gate": gate}
+
+
 def make_decode_inputs(wl: Workload, device="cpu"):
     """Draw a decode workload: a prefix of ``n_prefix`` tokens per sequence
     (k, v, r, u [S, H, n_prefix, *]) and one new token per sequence

@@ -9,22 +9,47 @@ import pytest
 
 from paper_2608_09307_amd import linsimp as L
 
-HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
-                      "include", "linsimp.h")
+INCLUDE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
 
 
-def _declared():
-    text = open(HEADER).read()
-    return sorted(set(re.findall(r"\b(linsimp_[a-z_]+)\s*\(", text)))
+def _declared(header):
+    text = open(os.path.join(INCLUDE, header)).read()
+    decl = r"^(?:int|size_t|const char\*)\s+(linsimp_[a-z_]+)\s*\("
+    return sorted(set(re.findall(decl, text, flags=re.MULTILINE)))
 
 
 def test_library_exports_every_declared_symbol():
     lib = L.lib()
-    names = _declared()
-    assert set(names) == set(L.EXPORTS)
-    for name in names:
-        assert hasattr(lib, name), name
-    assert lib.linsimp_version() == 100
+    assert sorted(os.listdir(INCLUDE)) == ["linsimp.h", "linsimp_head.h"]
+    for header, exports in (("linsimp.h", L.EXPORTS), ("linsimp_head.h", L.HEAD_EXPORTS)):
+        names = _declared(header)
+        assert set(names) == set(exports), header
+        for name in names:
+            assert hasattr(lib, name), name
+    assert lib.linsimp_version() == 101
+
+
+def test_head_sizes_and_argument_errors():
+    lib = L.lib()
+    d = L.make_dims(2, 16, 16384, 128, 128, 128, 64, L.BF16)
+    saved = lib.linsimp_head_saved_size(ctypes.byref(d))
+    # q', k', r' and o~ in bf16, 2 + 1 floats per row
+    rows = 2 * 16 * 16384
+    assert saved == rows * (3 * 128 + 128) * 2 + rows * 12
+    assert lib.linsimp_head_workspace_size(ctypes.byref(d), 1) > L.workspace_size(d, True)
+    bad = L.make_dims(1, 1, 64, 48, 48, 32, 8, L.BF16)
+    assert lib.linsimp_head_saved_size(ctypes.byref(bad)) == 0
+    vp = ctypes.c_void_p
+    good = [4096 * (i + 1) for i in range(10)]
+    dd = L.make_dims(1, 1, 64, 32, 32, 32, 8, L.F32)
+    o = L.head_opts(7)
+    rc = lib.linsimp_head_fwd(ctypes.byref(dd), ctypes.byref(o), *[vp(p) for p in good],
+                              1 << 20, vp(1 << 20), 1 << 20, vp(0))
+    assert rc == -1 and b"gate" in lib.linsimp_last_error()
+    o = L.head_opts(L.GATE_HEAD)
+    rc = lib.linsimp_head_fwd(ctypes.byref(dd), ctypes.byref(o), *[vp(p) for p in good],
+                              16, vp(1 << 20), 1 << 20, vp(0))
+    assert rc == -3 and b"saved" in lib.linsimp_last_error()
 
 
 def test_workspace_size_and_unsupported_shapes():

@@ -1,0 +1,118 @@
+"""GPU parity of the full head (L2 normalisation + temperature, core, gated
+RMSNorm; per-head and channel-wise gates) against the float64 oracle of
+oracle.layer, through the C ABI (include/linsimp_head.h).
+
+Outputs and the gradients of q, k, v, r, u and of the channel-gate logits are
+held to relative L2 <= 1e-4 (float32) and <= 2e-2 (bf16).  The per-head sums
+dtau = <q_hat, dq_core> and dgamma = <dy, o_hat g (1 - g)> are inner products
+over all rows of a head; the gradient bar on their factor (relative L2 <= tol)
+bounds their error by tol |a| |b| (Cauchy-Schwarz), which is the bar used
+for them.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import layer as LY
+from paper_2608_09307_amd import linsimp as L
+from paper_2608_09307_amd.workloads import Workload, make_head_params, make_inputs
+
+from helpers import f64, rel_l2
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+NAMES = ("dq", "dk", "dv", "dr", "du")
+
+
+def _oracle(x, p, wl, pairs, channel):
+    ys, grads, scale = {}, {}, {}
+    for b, h in pairs:
+        args = [f64(x[nm][b, h]) for nm in ("q", "k", "v", "r", "u")]
+        om = f64(x["omega"][h])
+        tau = float(p["tau"][h])
+        gate = f64(p["gate"][b, h]) if channel else float(p["gate"][h])
+        ys[(b, h)], _ = LY.head_forward(*args, om, wl.w, tau, gate)
+        parts = {}
+        grads[(b, h)] = LY.head_backward(*args, om, wl.w, tau, gate, f64(x["dO"][b, h]), parts=parts)
+        scale[(b, h)] = {k: float(np.sum(v * v)) for k, v in parts.items()}
+    return ys, grads, scale
+
+
+def _cs_scale(scale, pairs, H, a, b):
+    """Cauchy-Schwarz scale |a| |b| of a per-head inner product over its rows."""
+    sa, sb = np.zeros(H), np.zeros(H)
+    for (bb, h) in pairs:
+        sa[h] += scale[(bb, h)][a]
+        sb[h] += scale[(bb, h)][b]
+    return np.sqrt(sa * sb)
+
+
+def _run(wl: Workload, channel: bool, zero_rows: bool = False):
+    print(f"[head] {wl} channel={channel} zero_rows={zero_rows}", flush=True)
+    x = make_inputs(wl, device=DEV, with_grad=True)
+    p = make_head_params(wl, device=DEV, channel_gate=channel)
+    if zero_rows:                       # rows below the norm floor
+        x["q"][:, :, 3] = 0
+        x["r"][:, :, 5] = 0
+        x["k"][:, :, 7] = 0
+    y, saved = L.head_fwd(x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w, p["tau"], p["gate"])
+    g = L.head_bwd(x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w, p["tau"], p["gate"],
+                   saved, x["dO"])
+    torch.cuda.synchronize()
+    pairs = [(b, h) for b in range(wl.B) for h in range(wl.H)]
+    ys, ref, scale = _oracle(x, p, wl, pairs, channel)
+    tol = TOL[wl.dtype]
+    errs = {"y": rel_l2(np.stack([f64(y[b, h]) for b, h in pairs]), np.stack([ys[q] for q in pairs]))}
+    for gi, nm in enumerate(NAMES):
+        got = np.stack([f64(g[gi][b, h]) for b, h in pairs])
+        assert np.all(np.isfinite(got)), nm
+        errs[nm] = rel_l2(got, np.stack([ref[q][gi] for q in pairs]))
+    dtau_ref = np.zeros(wl.H)
+    for (b, h) in pairs:
+        dtau_ref[h] += ref[(b, h)][5]
+    cs = _cs_scale(scale, pairs, wl.H, "q_hat", "dq_core")
+    errs["dtau"] = float(np.max(np.abs(g[5].cpu().double().numpy() - dtau_ref) / cs))
+    if channel:
+        got = np.stack([f64(g[6][b, h]) for b, h in pairs])
+        errs["dgate"] = rel_l2(got, np.stack([ref[q][6] for q in pairs]))
+    else:
+        dg_ref = np.zeros(wl.H)
+        for (b, h) in pairs:
+            dg_ref[h] += ref[(b, h)][6]
+        cs = _cs_scale(scale, pairs, wl.H, "dy", "gate_factor")
+        errs["dgamma"] = float(np.max(np.abs(g[6].cpu().double().numpy() - dg_ref) / cs))
+    print("      " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()), flush=True)
+    for nm, e in errs.items():
+        assert e <= tol, (nm, e)
+    return x, p, y, saved, g
+
+
+@pytest.mark.parametrize("channel", [False, True])
+@pytest.mark.parametrize("D,m,n,w,B,H,dt", [
+    (32, 32, 100, 20, 1, 2, "f32"),
+    (64, 64, 77, 64, 2, 1, "f32"),
+    (128, 128, 300, 64, 1, 2, "bf16"),
+    (64, 64, 257, 48, 2, 2, "bf16"),
+    (32, 32, 130, 64, 1, 1, "bf16"),
+])
+def test_head_parity(D, m, n, w, B, H, dt, channel):
+    _run(Workload("head", B, H, n, D, D, m, w, dt, "fwdbwd", seed=61), channel)
+
+
+def test_head_rows_below_the_norm_floor():
+    _run(Workload("head0", 1, 2, 40, 32, 32, 32, 16, "f32", "fwdbwd", seed=62), False, zero_rows=True)
+
+
+def test_head_backward_is_bitwise_reproducible():
+    wl = Workload("head_det", 2, 2, 500, 128, 128, 128, 64, "bf16", "fwdbwd", seed=63)
+    x = make_inputs(wl, device=DEV, with_grad=True)
+    p = make_head_params(wl, device=DEV)
+    args = (x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w, p["tau"], p["gate"])
+    y, saved = L.head_fwd(*args)
+    g1 = L.head_bwd(*args, saved, x["dO"])
+    g2 = L.head_bwd(*args, saved, x["dO"])
+    torch.cuda.synchronize()
+    for a, b in zip(g1, g2):
+        assert torch.equal(a, b)
