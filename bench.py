@@ -7,7 +7,12 @@ the whole hot path: forward (key feature map, chunk states, chunk scan,
 anchor-window readout) and backward (query sweeps, state sweep, reverse scan,
 key side) on the same batch.
 
-    python bench.py [--steps K] [--warmup W] [--gpus 1]
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--head]
+
+With --head the step is the full head instead of the core: L2 normalisation
+and query temperature, core, gated RMSNorm (per-head gate), and the backward
+of all three; the line then also reports the streaming head kernels against
+the HBM peak (`head_streams`).
 
 Prints one JSON line.  `value` is tokens/s (B*n per step time).  `roofline`
 reports the dominant kernel (largest share of the timed region) against the
@@ -30,6 +35,7 @@ sys.path.insert(0, ROOT)
 
 WORKLOAD = "layer16k_bf16"
 PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 matrix-core peak
+PEAK_HBM_GBS = 8000.0              # MI355X HBM3E peak
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer16k_bf16.json")
 
 
@@ -53,6 +59,19 @@ def kernel_flops(wl):
         "bwd_du": f * (wl.D + wl.Dv),
         "bwd_dqdr": f * (wl.Dv + wl.D),
         "bwd_state": f * wl.Dv,
+    }
+
+
+def head_stream_bytes(wl, es=2):
+    """Algorithmic HBM bytes per launch of the streaming head kernels (each
+    row read and written once; per-row float32 scalars included)."""
+    rows = wl.B * wl.H * wl.n
+    D, Dv = wl.D, wl.Dv
+    return {
+        "head_prenorm": rows * 6 * D * es,                        # q, k, r in; q', k', r' out
+        "head_gate": rows * (2 * Dv * es + 4),                    # o~ in; y, rho out
+        "head_gate_bwd": rows * (3 * Dv * es + 2 * 4),            # o~, dy in; d o~ out; rho in, part out
+        "head_prenorm_bwd": rows * (9 * D * es + 4),              # q, k, r, core grads in; grads out
     }
 
 
@@ -146,6 +165,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (for scaling HBM counters)")
+    ap.add_argument("--head", action="store_true",
+                    help="time the full head (normalisation, core, gated RMSNorm) instead of the core")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
@@ -154,7 +175,7 @@ def main():
 
     import torch
     from paper_2608_09307_amd import linsimp as L
-    from paper_2608_09307_amd.workloads import WORKLOADS, make_inputs
+    from paper_2608_09307_amd.workloads import WORKLOADS, make_head_params, make_inputs
 
     dev = "cuda:0"
     torch.cuda.set_device(0)
@@ -175,6 +196,18 @@ def main():
               workspace=ws_f)
         L.bwd(x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w, out, stats, x["dO"],
               grads=grads, workspace=ws_b)
+
+    if args.head:
+        import ctypes
+        hp = make_head_params(wl, device=dev)
+        hargs = (x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w, hp["tau"], hp["gate"])
+        del ws_f, ws_b
+        hws = L._aligned_bytes(int(L.lib().linsimp_head_workspace_size(ctypes.byref(d), 1)), dev)
+        y, saved = L.head_fwd(*hargs, workspace=hws)
+
+        def step():  # noqa: F811  (the full head instead of the core)
+            L.head_fwd(*hargs, y=y, saved=saved, workspace=hws)
+            L.head_bwd(*hargs, saved, x["dO"], workspace=hws)
 
     for _ in range(args.warmup):
         step()
@@ -211,8 +244,19 @@ def main():
                         "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                         "traffic": traffic_for(dominant), "kernel": dominant,
                         "avg_ms": round(tot / cnt, 4)}
+    head_streams = None
+    if args.head:
+        hb = head_stream_bytes(wl)
+        head_streams = {}
+        for k, b in hb.items():
+            if k in kt:
+                gbs = b / (kt[k][0] / kt[k][1] * 1e-3) / 1e9
+                head_streams[k] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                                   "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                                   "bytes": b, "avg_ms": round(kt[k][0] / kt[k][1], 4)}
     line = {
-        "metric": "LinSimp fwd+bwd tokens/s at n=16k; % of MI355X bf16 MFMA peak",
+        "metric": ("LinSimp head fwd+bwd tokens/s at n=16k" if args.head else
+                   "LinSimp fwd+bwd tokens/s at n=16k; % of MI355X bf16 MFMA peak"),
         "value": round(tokens / (ms * 1e-3), 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -224,13 +268,15 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1)*d^-1/4 streams, N(0,1) feature bank and dO)",
-        "config": {"workload": WORKLOAD, "B": wl.B, "H": wl.H, "n": wl.n, "d": wl.D, "m": wl.m,
-                   "w": wl.w},
+        "config": {"workload": WORKLOAD + ("_head" if args.head else ""), "B": wl.B, "H": wl.H,
+                   "n": wl.n, "d": wl.D, "m": wl.m, "w": wl.w},
         "mfma_frac_step": round(step_tflops / PEAK_BF16_TFLOPS, 4),
         "algorithmic_tflops_step": round(step_tflops, 2),
         "roofline": roofline,
         "kernels_avg_ms": kernels_ms,
     }
+    if head_streams is not None:
+        line["head_streams"] = head_streams
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(x, wl, args.cpu_seconds)
     print(json.dumps(line), flush=True)
