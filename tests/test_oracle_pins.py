@@ -343,3 +343,66 @@ def test_orthogonal_bank_structure_and_sign_fix():
     Om = features.orthogonal_bank(rng, 120_000, D)
     est = montecarlo.kernel_estimate(x, y, Om)
     assert abs(est / math.exp(x @ y) - 1) < 5e-3
+
+
+def test_orthogonal_block_reconstructs_and_has_positive_diagonal():
+    rng = np.random.default_rng(70)
+    D = 16
+    G = rng.standard_normal((D, D))
+    radii = np.sqrt(rng.chisquare(D, size=D))
+    Om = features.orthogonal_block(G, radii)
+    # row norms are the radii; directions are orthonormal
+    assert np.allclose(np.linalg.norm(Om, axis=1), radii, rtol=1e-13)
+    Qt = Om / radii[:, None]
+    assert np.allclose(Qt @ Qt.T, np.eye(D), atol=1e-13)
+    # Q^T G is upper triangular with a positive diagonal (the sign-fixed R):
+    # a Gram-Schmidt of G's columns, computed independently, gives the same Q
+    R = Qt @ G
+    assert np.allclose(np.tril(R, -1), 0, atol=1e-12)
+    assert np.all(np.diag(R) > 0)
+    Qgs = np.zeros((D, D))
+    for a in range(D):
+        x = G[:, a].copy()
+        for b in range(a):
+            x -= (Qgs[:, b] @ G[:, a]) * Qgs[:, b]
+        for b in range(a):                       # second pass (re-orthogonalise)
+            x -= (Qgs[:, b] @ x) * Qgs[:, b]
+        Qgs[:, a] = x / np.linalg.norm(x)
+    assert np.allclose(Qgs.T, Qt, atol=1e-11)
+    # without the fix the factor is Householder's: first column of Q is
+    # -sign(G[0,0]) G[:,0] / |G[:,0]| (R_00 = -sign(G_00)|G_:0|)
+    raw = features.orthogonal_block(G, np.ones(D), sign_correct=False)
+    assert np.allclose(raw[0], -np.sign(G[0, 0]) * G[:, 0] / np.linalg.norm(G[:, 0]), atol=1e-13)
+
+
+def _kernel_error(rng, m, D, sign_correct, pairs):
+    """RMS relative error of the kernel estimate of Lemma 1 over fixed pairs,
+    one bank of m rows."""
+    Om = features.orthogonal_bank(rng, m, D, sign_correct)
+    errs = []
+    for x, y in pairs:
+        est = montecarlo.kernel_estimate(x, y, Om)
+        errs.append(est / montecarlo.exact_kernel(x, y) - 1.0)
+    return float(np.sqrt(np.mean(np.square(errs))))
+
+
+def test_sign_fix_gives_the_inverse_sqrt_m_trend():
+    """App. B.1 diagnostic: with the sign correction the kernel error falls like
+    m^{-1/2}; without it (Householder factor) it stays at a bias floor."""
+    D = 16
+    prng = np.random.default_rng(71)
+    pairs = []
+    for _ in range(16):
+        x, y = prng.standard_normal(D), prng.standard_normal(D)
+        pairs.append((0.5 * x / np.linalg.norm(x), 0.5 * y / np.linalg.norm(y)))
+    ms = [256, 4096, 65536]
+    fixed = [np.mean([_kernel_error(np.random.default_rng(100 + 7 * s + i), m, D, True, pairs)
+                      for s in range(4)]) for i, m in enumerate(ms)]
+    raw = [np.mean([_kernel_error(np.random.default_rng(200 + 7 * s + i), m, D, False, pairs)
+                    for s in range(4)]) for i, m in enumerate(ms)]
+    slope = np.polyfit(np.log(ms), np.log(fixed), 1)[0]
+    assert -0.65 < slope < -0.35, (slope, fixed)
+    # the raw factor's error does not keep falling: it is far above the fixed
+    # one at large m and drops by much less than 16x over a 256x range
+    assert raw[-1] > 4 * fixed[-1], (raw, fixed)
+    assert raw[0] / raw[-1] < 4, raw
