@@ -21,7 +21,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIBDIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIBDIR, "liblinsimp.so")
 
-SOURCES = ["api.cpp", "fwd.hip", "bwd.hip", "decode.hip", "head.hip"]
+SOURCES = ["api.cpp", "fwd.hip", "bwd.hip", "decode.hip", "head.hip", "bank.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

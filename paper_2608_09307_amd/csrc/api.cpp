@@ -1,7 +1,9 @@
 // C ABI of the LinSimp library: argument validation, workspace carving and
 // dispatch to the HIP kernels.  Declarations and contracts: include/linsimp.h
-// (the core) and include/linsimp_head.h (the full head around it).
+// (the core), include/linsimp_head.h (the full head around it) and
+// include/linsimp_bank.h (the feature-bank sampler).
 #include "../../include/linsimp.h"
+#include "../../include/linsimp_bank.h"
 #include "../../include/linsimp_head.h"
 
 #include <stdarg.h>
@@ -455,6 +457,31 @@ int linsimp_head_bwd(const linsimp_dims* dims, const linsimp_head_opts* opts, co
   if ((rc = launch_head_reduce(s, part_t, dtau, st))) return rc;
   if (!channel && (rc = launch_head_reduce(s, part_g, (float*)dgate, st))) return rc;
   return LINSIMP_OK;
+}
+
+int linsimp_feature_bank(int32_t H, int32_t m, int32_t D, const float* gauss, const float* radii,
+                         float* omega, int32_t sign_correct, void* stream) {
+  if (H < 1 || m < 1 || D < 1) {
+    set_error("feature bank: H, m and D must be positive (H=%d m=%d D=%d)", H, m, D);
+    return LINSIMP_E_INVALID_ARG;
+  }
+  if (D != 32 && D != 64 && D != 128) {
+    set_error("feature bank: D=%d not in {32, 64, 128}", D);
+    return LINSIMP_E_UNSUPPORTED;
+  }
+  if (sign_correct != 0 && sign_correct != 1) {
+    set_error("feature bank: sign_correct must be 0 or 1");
+    return LINSIMP_E_INVALID_ARG;
+  }
+  if ((int64_t)H * ((m + D - 1) / D) > 65535) {
+    set_error("feature bank: H * ceil(m / D) = %lld blocks is above 65535",
+              (long long)H * ((m + D - 1) / D));
+    return LINSIMP_E_UNSUPPORTED;
+  }
+  const void* ps[] = {gauss, radii, omega};
+  int rc = check_ptrs("gauss,radii,omega", ps, 3);
+  if (rc) return rc;
+  return launch_feature_bank(H, m, D, gauss, radii, omega, sign_correct, (hipStream_t)stream);
 }
 
 const char* linsimp_last_error(void) { return g_err; }

@@ -83,6 +83,10 @@ int launch_head_prenorm_bwd(const Shape& s, const void* q, const void* k, const 
                             float norm_eps, hipStream_t st);
 int launch_head_reduce(const Shape& s, const float* part, float* out, hipStream_t st);
 
+// orthogonal random-feature bank (bank.hip)
+int launch_feature_bank(int H, int m, int D, const float* gauss, const float* radii, float* omega,
+                        int sign_correct, hipStream_t st);
+
 void set_error(const char* fmt, ...);
 bool shape_supported(const Shape& s, bool backward);
 

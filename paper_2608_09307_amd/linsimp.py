@@ -1,5 +1,5 @@
-"""Thin ctypes binding of liblinsimp.so (the C ABI in include/linsimp.h and
-include/linsimp_head.h).
+"""Thin ctypes binding of liblinsimp.so (the C ABI in include/linsimp.h,
+include/linsimp_head.h and include/linsimp_bank.h).
 
 Argument marshalling only: torch tensors are turned into device pointers and
 the current HIP stream is passed through.  Every step of the computation runs
@@ -46,6 +46,7 @@ EXPORTS = ("linsimp_workspace_size", "linsimp_fwd", "linsimp_bwd", "linsimp_pref
            "linsimp_last_error", "linsimp_version")
 HEAD_EXPORTS = ("linsimp_head_saved_size", "linsimp_head_workspace_size", "linsimp_head_fwd",
                 "linsimp_head_bwd")
+BANK_EXPORTS = ("linsimp_feature_bank",)
 
 
 def lib_path() -> str:
@@ -90,6 +91,8 @@ def lib():
     L.linsimp_head_fwd.restype = ctypes.c_int
     L.linsimp_head_bwd.argtypes = [pd, po] + [vp] * 17 + [vp, sz, vp]
     L.linsimp_head_bwd.restype = ctypes.c_int
+    L.linsimp_feature_bank.argtypes = [i32, i32, i32, vp, vp, vp, i32, vp]
+    L.linsimp_feature_bank.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -304,3 +307,22 @@ def head_bwd(q, k, v, r, u, omega, w, tau, gate, saved, dy, eps=EPS, norm_eps=NO
                               _ptr(dtau, "dtau"), _ptr(dgate, "dgate"),
                               _ptr(workspace, "workspace"), workspace.numel(), _stream()))
     return (*grads, dtau, dgate)
+
+
+# ---------------------------------------------------------------------------
+# Orthogonal random-feature bank (include/linsimp_bank.h)
+# ---------------------------------------------------------------------------
+
+def feature_bank(gauss, radii, m, sign_correct=True, omega=None):
+    """Bank [H, m, D] float32 from draws gauss [H, nb, D, D] and radii
+    [H, nb, D] (float32, on the GPU).  See linsimp_feature_bank."""
+    H, nb, D, _ = gauss.shape
+    if gauss.dtype != torch.float32 or radii.dtype != torch.float32:
+        raise TypeError("gauss and radii must be float32")
+    if radii.shape != (H, nb, D) or nb != (m + D - 1) // D:
+        raise ValueError("gauss must be [H, ceil(m/D), D, D] and radii [H, ceil(m/D), D]")
+    if omega is None:
+        omega = torch.empty(H, m, D, dtype=torch.float32, device=gauss.device)
+    _check(lib().linsimp_feature_bank(H, m, D, _ptr(gauss, "gauss"), _ptr(radii, "radii"),
+                                      _ptr(omega, "omega"), 1 if sign_correct else 0, _stream()))
+    return omega

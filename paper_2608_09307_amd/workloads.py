@@ -117,6 +117,17 @@ def make_head_params(wl: Workload, device="cpu", channel_gate: bool = False):
     return {"tau": tau, "gate": gate}
 
 
+def make_bank_draws(H: int, m: int, D: int, seed: int = 0, device="cpu"):
+    """Random draws of the orthogonal feature-bank sampler: gauss [H, nb, D, D]
+    iid N(0,1) float32 (nb = ceil(m / D)) and radii [H, nb, D], each the norm
+    of a fresh D-dimensional N(0, I) vector (a chi_D draw)."""
+    g = _gen(device, seed)
+    nb = (m + D - 1) // D
+    gauss = _normal((H, nb, D, D), g, device)
+    radii = torch.linalg.vector_norm(_normal((H, nb, D, D), g, device), dim=-1)
+    return gauss, radii
+
+
 def make_decode_inputs(wl: Workload, device="cpu"):
     """Draw a decode workload: a prefix of ``n_prefix`` tokens per sequence
     (k, v, r, u [S, H, n_prefix, *]) and one new token per sequence

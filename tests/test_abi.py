@@ -20,8 +20,9 @@ def _declared(header):
 
 def test_library_exports_every_declared_symbol():
     lib = L.lib()
-    assert sorted(os.listdir(INCLUDE)) == ["linsimp.h", "linsimp_head.h"]
-    for header, exports in (("linsimp.h", L.EXPORTS), ("linsimp_head.h", L.HEAD_EXPORTS)):
+    assert sorted(os.listdir(INCLUDE)) == ["linsimp.h", "linsimp_bank.h", "linsimp_head.h"]
+    for header, exports in (("linsimp.h", L.EXPORTS), ("linsimp_head.h", L.HEAD_EXPORTS),
+                            ("linsimp_bank.h", L.BANK_EXPORTS)):
         names = _declared(header)
         assert set(names) == set(exports), header
         for name in names:
@@ -100,3 +101,14 @@ def test_binding_refuses_cpu_tensors():
     om = torch.zeros(1, 32, 32)
     with pytest.raises((ValueError, RuntimeError)):
         L.fwd(x, x, x, x, x, om, 4, workspace=torch.zeros(1 << 16, dtype=torch.uint8))
+
+
+def test_feature_bank_argument_errors():
+    lib = L.lib()
+    vp = ctypes.c_void_p
+    ok = [vp(4096 * (i + 1)) for i in range(3)]
+    assert lib.linsimp_feature_bank(1, 64, 48, *ok, 1, vp(0)) == -2
+    assert lib.linsimp_feature_bank(1, 0, 64, *ok, 1, vp(0)) == -1
+    assert lib.linsimp_feature_bank(1, 64, 64, *ok, 2, vp(0)) == -1
+    assert lib.linsimp_feature_bank(1, 64, 64, vp(0), ok[1], ok[2], 1, vp(0)) == -1
+    assert lib.linsimp_feature_bank(70000, 64, 64, *ok, 1, vp(0)) == -2
