@@ -130,6 +130,21 @@ int linsimp_decode_step(int64_t S, int32_t H, int32_t D, int32_t Dv, int32_t m, 
                         float* rho, void* ring_r, void* ring_u, int64_t* pos, void* out,
                         void* stream);
 
+/* T consecutive decode steps in one call (Theorem 1 applied T times): token j
+ * of sequence s is position pos[s] + j; the result equals T calls of
+ * linsimp_decode_step.  The state stays on chip for the whole chunk (M, for
+ * m <= 128, in registers; the ring and a in LDS/registers), so it is read and
+ * written once per call instead of once per token.
+ *   q, k, r : [S, H, T, D] dtype;  v, u : [S, H, T, Dv] dtype; omega [H, m, D] f32
+ *   M, a, rho, ring_r, ring_u, pos : in/out, layouts as in linsimp_prefill
+ *   out : [S, H, T, Dv] dtype
+ * 1 <= T <= 4096.  Uses no workspace.  Same shape support as the forward. */
+int linsimp_decode_chunk(int64_t S, int32_t H, int32_t T, int32_t D, int32_t Dv, int32_t m,
+                         int32_t w, int32_t dtype, float eps, const void* q, const void* k,
+                         const void* v, const void* r, const void* u, const float* omega, float* M,
+                         float* a, float* rho, void* ring_r, void* ring_u, int64_t* pos, void* out,
+                         void* stream);
+
 /* Per-kernel timing, for tuning and roofline reports.  While enabled
  * (on != 0), every kernel the library launches is bracketed by two HIP events
  * recorded on its stream; enabling costs two event records per launch and

@@ -260,7 +260,27 @@ int linsimp_decode_step(int64_t S, int32_t H, int32_t D, int32_t Dv, int32_t m, 
   if (rc) return rc;
   const void* ps[] = {q, k, v, r, u, omega, M, a, rho, ring_r, ring_u, pos, out};
   if ((rc = check_ptrs("q,k,v,r,u,omega,M,a,rho,ring_r,ring_u,pos,out", ps, 13))) return rc;
-  return launch_decode(S, H, D, Dv, m, w, dtype, eps, q, k, v, r, u, omega, M, a, rho, ring_r,
+  return launch_decode(S, H, 1, D, Dv, m, w, dtype, eps, q, k, v, r, u, omega, M, a, rho, ring_r,
+                       ring_u, pos, out, (hipStream_t)stream);
+}
+
+int linsimp_decode_chunk(int64_t S, int32_t H, int32_t T, int32_t D, int32_t Dv, int32_t m,
+                         int32_t w, int32_t dtype, float eps, const void* q, const void* k,
+                         const void* v, const void* r, const void* u, const float* omega, float* M,
+                         float* a, float* rho, void* ring_r, void* ring_u, int64_t* pos, void* out,
+                         void* stream) {
+  if (T < 1 || T > 4096) {
+    set_error("decode_chunk: T=%d not in [1, 4096]", T);
+    return LINSIMP_E_INVALID_ARG;
+  }
+  linsimp_dims d;
+  d.B = S; d.H = H; d.n = T; d.D = D; d.Dv = Dv; d.m = m; d.w = w; d.dtype = dtype; d.eps = eps;
+  Shape s;
+  int rc = check_dims(&d, &s, false);
+  if (rc) return rc;
+  const void* ps[] = {q, k, v, r, u, omega, M, a, rho, ring_r, ring_u, pos, out};
+  if ((rc = check_ptrs("q,k,v,r,u,omega,M,a,rho,ring_r,ring_u,pos,out", ps, 13))) return rc;
+  return launch_decode(S, H, T, D, Dv, m, w, dtype, eps, q, k, v, r, u, omega, M, a, rho, ring_r,
                        ring_u, pos, out, (hipStream_t)stream);
 }
 

@@ -248,17 +248,271 @@ __global__ __launch_bounds__(256) void k_decode(DecArgs A) {
   if (tid == 0) A.rho[sh] = Rn;
 }
 
-// pos[s] += 1 after every head of sequence s has read it
-__global__ __launch_bounds__(256) void k_decode_advance(int64_t* pos, int64_t S) {
+// ---------------------------------------------------------------------------
+// Chunked decode: NT tokens per sequence in one launch (token j of sequence s
+// is position pos[s] + j).  The same per-token step as k_decode, but the
+// state stays on chip for the whole chunk: the ring anchors live in LDS and
+// are overwritten slot by slot, a lives in the registers of the threads that
+// own a feature, and M (for m <= 128) lives in the registers of the threads
+// that update it, so each state element is read and written once per chunk
+// instead of once per token.  For m = 256 M is streamed through global memory
+// per token as in k_decode.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int DV, int M, int NA>
+__global__ __launch_bounds__(256) void k_decode_chunk(DecArgs A, int NTOK) {
+  using F = MF<T>;
+  using C = DCfg<T, D, DV, M, NA>;
+  constexpr int PAD = C::PAD, W = C::W;
+  constexpr int PT = M / 32;                  // feature tiles
+  constexpr int PTW = (PT + 3) / 4;           // feature tiles per wave
+  constexpr bool RES = PTW == 1;              // M held in registers across the chunk
+  static_assert(C::BYTES <= 160 * 1024, "decode LDS budget");
+  __shared__ __align__(16) char smem[C::BYTES];
+  T* sOm = (T*)(smem + C::oOm);
+  T* sRr = (T*)(smem + C::oRr);
+  T* sUt = (T*)(smem + C::oUt);
+  float* sq = (float*)(smem + C::oQ);
+  float* sk = (float*)(smem + C::oK);
+  float* sv = (float*)(smem + C::oV);
+  float* schi = (float*)(smem + C::oChi);
+  float* san = (float*)(smem + C::oAn);
+  float* snz = (float*)(smem + C::oNz);
+  float* sred = (float*)(smem + C::oRed);
+  float* sN = (float*)(smem + C::oN);
+
+  const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
+  const int sh = blockIdx.x, H = A.H, w = A.w;
+  const int s = sh / H, hh = sh % H;
+  const int64_t t0 = A.pos[s];
+  T* rr = (T*)A.ring_r + (size_t)sh * w * D;
+  T* ru = (T*)A.ring_u + (size_t)sh * w * DV;
+  const float* om = A.omega + (size_t)hh * M * D;
+  float* Ms = A.M + (size_t)sh * M * DV;
+  float* as = A.a + (size_t)sh * M;
+
+  // ring, Omega and the state, once per chunk
+  for (int i = tid; i < W * D; i += 256) {
+    const int c = i / D, e = i % D;
+    sRr[c * (D + PAD) + e] = (c < w) ? rr[(size_t)c * D + e] : (T)0.0f;
+  }
+  for (int i = tid; i < W * DV; i += 256) {
+    const int c = i / DV, e = i % DV;
+    sUt[e * (W + PAD) + F::sigma(c)] = (c < w) ? ru[(size_t)c * DV + e] : (T)0.0f;
+  }
+  for (int i = tid; i < M * D; i += 256) sOm[(i / D) * (D + PAD) + (i % D)] = (T)(om[i] * kLog2e);
+  float areg = (tid < M) ? as[tid] : 0.0f;
+  float R = A.rho[sh];
+  float Mreg[RES ? DV / 32 : 1][16];
+  if constexpr (RES) {
+    if (wv < PT) {
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt)
+#pragma unroll
+        for (int vv = 0; vv < 16; ++vv) Mreg[dt][vv] = Ms[(size_t)(wv * 32 + crow(vv, h)) * DV + dt * 32 + col];
+    }
+  }
+
+#pragma unroll 1
+  for (int j = 0; j < NTOK; ++j) {
+    const int64_t t = t0 + j;
+    const int slot = (int)(t % w);
+    const int nvalid = (int)((t + 1 < w) ? t + 1 : w);
+    const size_t tok = (size_t)sh * NTOK + j;
+    const T* qt = (const T*)A.q + tok * D;
+    const T* kt = (const T*)A.k + tok * D;
+    const T* vt = (const T*)A.v + tok * DV;
+    const T* rt = (const T*)A.r + tok * D;
+    const T* ut = (const T*)A.u + tok * DV;
+    __syncthreads();                              // the previous token is done with LDS
+    for (int i = tid; i < D; i += 256) {
+      sq[i] = tof(qt[i]);
+      sk[i] = tof(kt[i]);
+      sRr[slot * (D + PAD) + i] = rt[i];
+    }
+    for (int i = tid; i < DV; i += 256) {
+      sv[i] = tof(vt[i]);
+      sUt[i * (W + PAD) + F::sigma(slot)] = ut[i];
+    }
+    __syncthreads();
+
+    // key features of k_t and the frame update
+    float nk = 0.0f;
+    for (int e = 0; e < D; ++e) nk += sk[e] * sk[e];
+    float lam = kNegInf;
+    if (tid < M) {
+      const float* orow = om + (size_t)tid * D;
+      float acc = 0.0f;
+      for (int e = 0; e < D; ++e) acc += orow[e] * sk[e];
+      lam = (acc - 0.5f * nk) * kLog2e;
+    }
+    float mx = wave_max(lam);
+    if (l == 0) sred[wv] = mx;
+    __syncthreads();
+    const float rho_t = fmaxf(fmaxf(sred[0], sred[1]), fmaxf(sred[2], sred[3]));
+    const float Rn = fmaxf(R, rho_t);
+    const float sa = fast_exp2(R - Rn);
+    if (tid < M) {
+      const float chi = fast_exp2(lam - Rn) * rsqrtf((float)M);
+      schi[tid] = chi;
+      areg = sa * areg + chi;
+      san[tid] = areg;
+    }
+    // composite-query logits (lanes <-> feature, registers <-> anchor)
+    f32x16 acc[PTW][NA];
+    float nz[NA];
+#pragma unroll
+    for (int pi = 0; pi < PTW; ++pi)
+#pragma unroll
+      for (int ct = 0; ct < NA; ++ct) acc[pi][ct] = zero16();
+#pragma unroll
+    for (int ct = 0; ct < NA; ++ct) nz[ct] = 0.0f;
+#pragma unroll
+    for (int ct = 0; ct < NA; ++ct) {
+      const int c = ct * 32 + col;
+      const bool valid = c < nvalid;
+#pragma unroll 2
+      for (int ks = 0; ks < D / F::KS; ++ks) {
+        const int k0 = ks * F::KS + h * F::KPL;
+        typename F::frag rf = F::ld(sRr + c * (D + PAD), k0), zf;
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float p = valid ? sq[k0 + e] * fel(rf, e) : 0.0f;
+            nz[ct] += p * p;
+            zf[e] = (bf16)p;
+          }
+        } else {
+          const float p = valid ? sq[k0] * rf : 0.0f;
+          nz[ct] += p * p;
+          zf = p;
+        }
+#pragma unroll
+        for (int pi = 0; pi < PTW; ++pi) {
+          const int pt = wv + 4 * pi;
+          if (pt < PT)
+            acc[pi][ct] = F::mma(zf, F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), acc[pi][ct]);
+        }
+      }
+      nz[ct] = half_swap_add(nz[ct]);
+      if (wv == 0 && h == 0) snz[c] = valid ? -0.5f * kLog2e * nz[ct] : kNegInf;
+    }
+    __syncthreads();
+    float tm = kNegInf;
+#pragma unroll
+    for (int pi = 0; pi < PTW; ++pi) {
+      if (wv + 4 * pi >= PT) continue;
+#pragma unroll
+      for (int ct = 0; ct < NA; ++ct)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float x = acc[pi][ct][v] + snz[ct * 32 + crow(v, h)];
+          acc[pi][ct][v] = x;
+          tm = fmaxf(tm, x);
+        }
+    }
+    tm = wave_max(tm);
+    if (l == 0) sred[8 + wv] = tm;
+    __syncthreads();
+    const float L = fmaxf(fmaxf(sred[8], sred[9]), fmaxf(sred[10], sred[11]));
+    float zpart = 0.0f;
+    float npart[DV / 32];
+#pragma unroll
+    for (int dt = 0; dt < DV / 32; ++dt) npart[dt] = 0.0f;
+#pragma unroll
+    for (int pi = 0; pi < PTW; ++pi) {
+      const int pt = wv + 4 * pi;
+      if (pt >= PT) continue;
+      const float anp = san[pt * 32 + col];
+#pragma unroll
+      for (int ct = 0; ct < NA; ++ct)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float psi = fast_exp2(acc[pi][ct][v] - L);
+          acc[pi][ct][v] = psi;
+          zpart += psi * anp;
+        }
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt) {
+        f32x16 accW = zero16();
+        const T* urow = sUt + (dt * 32 + col) * (W + PAD);
+#pragma unroll
+        for (int ct = 0; ct < NA; ++ct)
+#pragma unroll
+          for (int sp = 0; sp < F::CSTEPS; ++sp)
+            accW = F::mma(F::cfrag(acc[pi][ct], sp), F::ldc(urow, ct * 32, sp, h), accW);
+        const int d = dt * 32 + col;
+        const float vd = sv[d];
+        float np = 0.0f;
+#pragma unroll
+        for (int vv = 0; vv < 16; ++vv) {
+          const int p = pt * 32 + crow(vv, h);
+          float mnew;
+          if constexpr (RES) {
+            mnew = sa * Mreg[dt][vv] + schi[p] * vd;
+            Mreg[dt][vv] = mnew;
+          } else {
+            float* mp = Ms + (size_t)p * DV + d;
+            mnew = sa * (*mp) + schi[p] * vd;
+            *mp = mnew;
+          }
+          np += mnew * accW[vv];
+        }
+        npart[dt] += np;
+      }
+    }
+    zpart = wave_sum(zpart);
+    if (l == 0) sred[16 + wv] = zpart;
+#pragma unroll
+    for (int dt = 0; dt < DV / 32; ++dt) {
+      const float nn = half_swap_add(npart[dt]);
+      if (h == 0) sN[wv * DV + dt * 32 + col] = nn;
+    }
+    __syncthreads();
+    const float Z = (sred[16] + sred[17]) + (sred[18] + sred[19]);
+    const float inv = 1.0f / (Z + A.eps);
+    for (int d = tid; d < DV; d += 256) {
+      const float N = (sN[d] + sN[DV + d]) + (sN[2 * DV + d] + sN[3 * DV + d]);
+      ((T*)A.out)[tok * DV + d] = (T)(N * inv);
+    }
+    R = Rn;
+  }
+
+  // state and ring back to global memory
+  if constexpr (RES) {
+    if (wv < PT) {
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt)
+#pragma unroll
+        for (int vv = 0; vv < 16; ++vv) Ms[(size_t)(wv * 32 + crow(vv, h)) * DV + dt * 32 + col] = Mreg[dt][vv];
+    }
+  }
+  if (tid < M) as[tid] = areg;
+  if (tid == 0) A.rho[sh] = R;
+  const int jlo = NTOK > w ? NTOK - w : 0;        // the last min(NTOK, w) tokens stay in the ring
+  for (int j = jlo; j < NTOK; ++j) {
+    const int slot = (int)((t0 + j) % w);
+    const size_t tok = (size_t)sh * NTOK + j;
+    for (int e = tid; e < D; e += 256) rr[(size_t)slot * D + e] = ((const T*)A.r)[tok * D + e];
+    for (int e = tid; e < DV; e += 256) ru[(size_t)slot * DV + e] = ((const T*)A.u)[tok * DV + e];
+  }
+}
+
+// pos[s] += step after every head of sequence s has read it
+__global__ __launch_bounds__(256) void k_decode_advance(int64_t* pos, int64_t S, int step) {
   int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < S) pos[i] += 1;
+  if (i < S) pos[i] += step;
 }
 
 template <typename T, int D, int DV, int M, int NA>
-static int run_decode(int64_t S, DecArgs a, hipStream_t st) {
-  { ProfScope ps("decode", st);
-  k_decode<T, D, DV, M, NA><<<(unsigned)(S * a.H), 256, 0, st>>>(a); }
-  k_decode_advance<<<(unsigned)((S + 255) / 256), 256, 0, st>>>(a.pos, S);
+static int run_decode(int64_t S, DecArgs a, int ntok, hipStream_t st) {
+  if (ntok == 1) {
+    ProfScope ps("decode", st);
+    k_decode<T, D, DV, M, NA><<<(unsigned)(S * a.H), 256, 0, st>>>(a);
+  } else {
+    ProfScope ps("decode_chunk", st);
+    k_decode_chunk<T, D, DV, M, NA><<<(unsigned)(S * a.H), 256, 0, st>>>(a, ntok);
+  }
+  k_decode_advance<<<(unsigned)((S + 255) / 256), 256, 0, st>>>(a.pos, S, ntok);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) {
     set_error("decode launch failed: %s", hipGetErrorString(e));
@@ -279,7 +533,7 @@ static int run_decode(int64_t S, DecArgs a, hipStream_t st) {
   X(float, 64, 64, 32)    \
   X(float, 64, 64, 64)
 
-int launch_decode(int64_t S, int H, int D, int Dv, int m, int w, int dtype, float eps,
+int launch_decode(int64_t S, int H, int ntok, int D, int Dv, int m, int w, int dtype, float eps,
                   const void* q, const void* k, const void* v, const void* r, const void* u,
                   const float* omega, float* M, float* a, float* rho, void* ring_r, void* ring_u,
                   int64_t* pos, void* out, hipStream_t st) {
@@ -290,8 +544,8 @@ int launch_decode(int64_t S, int H, int D, int Dv, int m, int w, int dtype, floa
   const int NA = (w + 31) / 32;
 #define X(T, D_, DV_, M_)                                                              \
   if (dtype == (sizeof(T) == 2 ? 1 : 0) && D == D_ && Dv == DV_ && m == M_) {          \
-    if (NA == 1) return run_decode<T, D_, DV_, M_, 1>(S, A, st);                       \
-    return run_decode<T, D_, DV_, M_, 2>(S, A, st);                                    \
+    if (NA == 1) return run_decode<T, D_, DV_, M_, 1>(S, A, ntok, st);                 \
+    return run_decode<T, D_, DV_, M_, 2>(S, A, ntok, st);                              \
   }
   LS_DEC_CASES(X)
 #undef X

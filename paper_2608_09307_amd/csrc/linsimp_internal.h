@@ -65,7 +65,7 @@ int launch_backward(const Shape& s, const void* q, const void* k, const void* v,
                     const void* dout, void* dq, void* dk, void* dv, void* dr, void* du,
                     const Workspace& ws, hipStream_t st);
 
-int launch_decode(int64_t S, int H, int D, int Dv, int m, int w, int dtype, float eps,
+int launch_decode(int64_t S, int H, int ntok, int D, int Dv, int m, int w, int dtype, float eps,
                   const void* q, const void* k, const void* v, const void* r, const void* u,
                   const float* omega, float* M, float* a, float* rho, void* ring_r, void* ring_u,
                   int64_t* pos, void* out, hipStream_t st);

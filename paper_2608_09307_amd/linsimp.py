@@ -42,8 +42,8 @@ GATE_HEAD, GATE_CHANNEL = 0, 1
 NORM_EPS, RMS_EPS = 1e-12, 1e-6
 
 EXPORTS = ("linsimp_workspace_size", "linsimp_fwd", "linsimp_bwd", "linsimp_prefill",
-           "linsimp_decode_step", "linsimp_timing_enable", "linsimp_timing_read",
-           "linsimp_last_error", "linsimp_version")
+           "linsimp_decode_step", "linsimp_decode_chunk", "linsimp_timing_enable",
+           "linsimp_timing_read", "linsimp_last_error", "linsimp_version")
 HEAD_EXPORTS = ("linsimp_head_saved_size", "linsimp_head_workspace_size", "linsimp_head_fwd",
                 "linsimp_head_bwd")
 BANK_EXPORTS = ("linsimp_feature_bank",)
@@ -73,6 +73,8 @@ def lib():
     L.linsimp_prefill.restype = ctypes.c_int
     L.linsimp_decode_step.argtypes = [i64, i32, i32, i32, i32, i32, i32, f32] + [vp] * 13 + [vp]
     L.linsimp_decode_step.restype = ctypes.c_int
+    L.linsimp_decode_chunk.argtypes = [i64, i32, i32, i32, i32, i32, i32, i32, f32] + [vp] * 13 + [vp]
+    L.linsimp_decode_chunk.restype = ctypes.c_int
     L.linsimp_timing_enable.argtypes = [ctypes.c_int]
     L.linsimp_timing_enable.restype = ctypes.c_int
     L.linsimp_timing_read.argtypes = [ctypes.c_char_p, ctypes.c_int, ctypes.POINTER(ctypes.c_float),
@@ -236,6 +238,25 @@ def decode_step(state, q, k, v, r, u, omega, w, eps=EPS, out=None):
                                      _ptr(state["ring_r"], "ring_r"),
                                      _ptr(state["ring_u"], "ring_u"), _ptr(state["pos"], "pos"),
                                      _ptr(out, "out"), _stream()))
+    return out
+
+
+
+def decode_chunk(state, q, k, v, r, u, omega, w, eps=EPS, out=None):
+    """T consecutive decode steps for S sequences (q, k, v, r, u: [S, H, T, *]);
+    updates ``state`` in place and returns out [S, H, T, Dv]."""
+    S, H, T, D = q.shape
+    Dv = v.shape[-1]
+    m = omega.shape[1]
+    if out is None:
+        out = torch.empty(S, H, T, Dv, dtype=q.dtype, device=q.device)
+    _check(lib().linsimp_decode_chunk(S, H, T, D, Dv, m, w, _dtype_code(q), eps, _ptr(q, "q"),
+                                      _ptr(k, "k"), _ptr(v, "v"), _ptr(r, "r"), _ptr(u, "u"),
+                                      _ptr(omega, "omega"), _ptr(state["M"], "M"),
+                                      _ptr(state["a"], "a"), _ptr(state["rho"], "rho"),
+                                      _ptr(state["ring_r"], "ring_r"),
+                                      _ptr(state["ring_u"], "ring_u"), _ptr(state["pos"], "pos"),
+                                      _ptr(out, "out"), _stream()))
     return out
 
 

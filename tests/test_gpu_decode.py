@@ -104,3 +104,50 @@ def test_decode_s256_h16_prefix8192_sampled():
         errs.append(rel_l2(f64(out[s, h]), ref))
     print("      rel_l2", errs, flush=True)
     assert max(errs) < 2e-2
+
+
+@pytest.mark.parametrize("dtype,D,m,w,P,T", [("f32", 32, 32, 8, 5, 20), ("bf16", 128, 128, 64, 40, 7),
+                                              ("bf16", 128, 128, 64, 3, 90), ("bf16", 64, 128, 33, 0, 40),
+                                              ("bf16", 128, 256, 64, 10, 12)])
+def test_decode_chunk_matches_steps_and_forward(dtype, D, m, w, P, T):
+    """T tokens in one chunked call equal T single decode steps (to float32
+    rounding) and forward rows P .. P+T-1; the final state equals the prefill
+    state of all P + T tokens.  P = 0 starts from an empty state."""
+    wl = Workload("decchunk", 2, 2, P + T, D, D, m, w, dtype, "fwd", seed=23)
+    print(f"[decode_chunk] {wl} T={T}", flush=True)
+    x = make_inputs(wl, device=DEV, with_grad=False)
+
+    def fresh():
+        if P > 0:
+            return L.prefill(*(x[nm][:, :, :P].contiguous() for nm in ("k", "v", "r", "u")), x["omega"], w)
+        dt = x["k"].dtype
+        return {"M": torch.zeros(wl.B, wl.H, m, D, device=DEV), "a": torch.zeros(wl.B, wl.H, m, device=DEV),
+                "rho": torch.full((wl.B, wl.H), float("-inf"), device=DEV),
+                "ring_r": torch.zeros(wl.B, wl.H, w, D, dtype=dt, device=DEV),
+                "ring_u": torch.zeros(wl.B, wl.H, w, D, dtype=dt, device=DEV),
+                "pos": torch.zeros(wl.B, dtype=torch.int64, device=DEV)}
+
+    st_c = fresh()
+    toks = {nm: x[nm][:, :, P:P + T].contiguous() for nm in ("q", "k", "v", "r", "u")}
+    oc = L.decode_chunk(st_c, toks["q"], toks["k"], toks["v"], toks["r"], toks["u"], x["omega"], w)
+    st_s = fresh()
+    os_ = []
+    for t in range(P, P + T):
+        tk = {nm: x[nm][:, :, t].contiguous() for nm in ("q", "k", "v", "r", "u")}
+        os_.append(L.decode_step(st_s, tk["q"], tk["k"], tk["v"], tk["r"], tk["u"], x["omega"], w).clone())
+    torch.cuda.synchronize()
+    osteps = torch.stack(os_, dim=2)
+    assert torch.equal(st_c["pos"], st_s["pos"])
+    assert rel_l2(f64(oc), f64(osteps)) < 1e-6
+    for nm in ("M", "a", "rho"):
+        assert rel_l2(f64(st_c[nm]), f64(st_s[nm])) < 1e-6, nm
+    for nm in ("ring_r", "ring_u"):
+        assert torch.equal(st_c[nm], st_s[nm]), nm
+    errs = []
+    for b in range(wl.B):
+        for h in range(wl.H):
+            ref = O.forward_recurrent(f64(x["q"][b, h]), f64(x["k"][b, h]), f64(x["v"][b, h]),
+                                      f64(x["r"][b, h]), f64(x["u"][b, h]), f64(x["omega"][h]), w)
+            errs.append(rel_l2(f64(oc[b, h]), ref[P:]))
+    print("      max rel_l2 over heads", max(errs), flush=True)
+    assert max(errs) < TOL[dtype]
