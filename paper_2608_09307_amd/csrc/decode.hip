@@ -46,6 +46,59 @@ struct DCfg {
   static constexpr int BYTES = oN + a16(4 * DV * 4);
 };
 
+// LDS staging in which every thread issues all of its 16-byte global loads
+// before its first LDS store (one memory round trip per call, not per element).
+// Ring rows c < w come from `ring` ([w][COLS]), row `slot` from `fresh` when it
+// is given, rows w .. ROWS-1 are zero.  TRANS stores column-major with the
+// row index permuted by MF<T>::sigma (the readout's anchor operand layout).
+template <typename T, int ROWS, int COLS, bool TRANS>
+LS_DEV void stage_ring(T* dst, int ldst, const T* ring, const T* fresh, int slot, int w, int tid) {
+  constexpr int VE = 16 / sizeof(T);
+  constexpr int CPR = COLS / VE;
+  constexpr int N = ROWS * CPR;
+  constexpr int IT = (N + 255) / 256;
+  typedef T V __attribute__((ext_vector_type(VE)));
+  V x[IT];
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    // unconditional loads (row clamped into the ring); rows past w are zeroed below
+    const int idx = min(tid + 256 * it, N - 1), c = idx / CPR, e = (idx % CPR) * VE;
+    const int cr = c < w ? c : w - 1;
+    x[it] = *(const V*)((fresh != nullptr && cr == slot) ? fresh + e : ring + (size_t)cr * COLS + e);
+  }
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int idx = tid + 256 * it, c = idx / CPR, e = (idx % CPR) * VE;
+    if (idx >= N) continue;
+    if (c >= w) {
+#pragma unroll
+      for (int k = 0; k < VE; ++k) x[it][k] = (T)0.0f;
+    }
+    if constexpr (TRANS) {
+#pragma unroll
+      for (int k = 0; k < VE; ++k) dst[(e + k) * ldst + MF<T>::sigma(c)] = x[it][k];
+    } else {
+#pragma unroll
+      for (int k = 0; k < VE; ++k) dst[c * ldst + e + k] = x[it][k];
+    }
+  }
+}
+
+// Omega * log2(e) of one head into LDS rows of pitch D + PAD, operand type
+template <typename T, int D, int M>
+LS_DEV void stage_omega(T* dst, const float* om, int tid) {
+  constexpr int N = M * D / 4;
+  constexpr int IT = N / 256;
+  static_assert(N % 256 == 0, "Omega staging");
+#pragma unroll 8
+  for (int it = 0; it < IT; ++it) {
+    const int idx = tid + 256 * it, p = idx / (D / 4), e = (idx % (D / 4)) * 4;
+    const f32x4 x = *(const f32x4*)(om + (size_t)p * D + e);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) dst[p * (D + MF<T>::PAD) + e + k] = (T)(x[k] * kLog2e);
+  }
+}
+
 template <typename T, int D, int DV, int M, int NA>
 __global__ __launch_bounds__(256) void k_decode(DecArgs A) {
   using F = MF<T>;
@@ -87,19 +140,9 @@ __global__ __launch_bounds__(256) void k_decode(DecArgs A) {
   // ---- stage the token, the ring (slot t mod w replaced by the new token) and Omega ----
   for (int i = tid; i < D; i += 256) { sq[i] = tof(qt[i]); sk[i] = tof(kt[i]); }
   for (int i = tid; i < DV; i += 256) sv[i] = tof(vt[i]);
-  for (int i = tid; i < W * D; i += 256) {
-    int c = i / D, e = i % D;
-    T x = (T)0.0f;
-    if (c < w) x = (c == slot) ? rt[e] : rr[(size_t)c * D + e];
-    sRr[c * (D + PAD) + e] = x;
-  }
-  for (int i = tid; i < W * DV; i += 256) {
-    int c = i / DV, e = i % DV;
-    T x = (T)0.0f;
-    if (c < w) x = (c == slot) ? ut[e] : ru[(size_t)c * DV + e];
-    sUt[e * (W + PAD) + F::sigma(c)] = x;
-  }
-  for (int i = tid; i < M * D; i += 256) sOm[(i / D) * (D + PAD) + (i % D)] = (T)(om[i] * kLog2e);
+  stage_ring<T, W, D, false>(sRr, D + PAD, rr, rt, slot, w, tid);
+  stage_ring<T, W, DV, true>(sUt, W + PAD, ru, ut, slot, w, tid);
+  stage_omega<T, D, M>(sOm, om, tid);
   const float Rold = A.rho[sh];
   __syncthreads();
 
@@ -291,15 +334,9 @@ __global__ __launch_bounds__(256) void k_decode_chunk(DecArgs A, int NTOK) {
   float* as = A.a + (size_t)sh * M;
 
   // ring, Omega and the state, once per chunk
-  for (int i = tid; i < W * D; i += 256) {
-    const int c = i / D, e = i % D;
-    sRr[c * (D + PAD) + e] = (c < w) ? rr[(size_t)c * D + e] : (T)0.0f;
-  }
-  for (int i = tid; i < W * DV; i += 256) {
-    const int c = i / DV, e = i % DV;
-    sUt[e * (W + PAD) + F::sigma(c)] = (c < w) ? ru[(size_t)c * DV + e] : (T)0.0f;
-  }
-  for (int i = tid; i < M * D; i += 256) sOm[(i / D) * (D + PAD) + (i % D)] = (T)(om[i] * kLog2e);
+  stage_ring<T, W, D, false>(sRr, D + PAD, rr, nullptr, 0, w, tid);
+  stage_ring<T, W, DV, true>(sUt, W + PAD, ru, nullptr, 0, w, tid);
+  stage_omega<T, D, M>(sOm, om, tid);
   float areg = (tid < M) ? as[tid] : 0.0f;
   float R = A.rho[sh];
   float Mreg[RES ? DV / 32 : 1][16];
