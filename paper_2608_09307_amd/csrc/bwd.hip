@@ -322,12 +322,19 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
 
   if constexpr (sizeof(T) == 2) {
-    copy_rows_f16<float>((f16*)sOm, D + PAD, a.omega + ((size_t)hh * M + (size_t)fb * FB) * D, D, FB, D, 0, 0, FB,
-                         tid, NT, kLog2e);
-    copy_rows_f16<T>((f16*)sR, D + PAD, rs_, D, 32, D, c0, 0, n, tid, NT);
+    StageRows<float, FB, D, NT> so;
+    StageRows<T, 32, D, NT> sr;
+    so.load(a.omega + ((size_t)hh * M + (size_t)fb * FB) * D, D, 0, 0, FB, tid);
+    sr.load(rs_, D, c0, 0, n, tid);
+    so.store((f16*)sOm, D + PAD, 0, 0, FB, tid, kLog2e);
+    sr.store((f16*)sR, D + PAD, c0, 0, n, tid);
   } else {
-    copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
-    copy_rows<T>(sR, D + PAD, rs_, D, 32, D, c0, 0, n, tid, NT);
+    StageRows<T, FB, D, NT> so;
+    StageRows<T, 32, D, NT> sr;
+    so.load(omq_h + (size_t)fb * FB * D, D, 0, 0, FB, tid);
+    sr.load(rs_, D, c0, 0, n, tid);
+    so.store(sOm, D + PAD, 0, 0, FB, tid);
+    sr.store(sR, D + PAD, c0, 0, n, tid);
   }
   f32x16 du[DV / 32];
 #pragma unroll
@@ -339,21 +346,29 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
     const int s0 = ch * 32;
     const bool has_bnd = ch > 0;
     const float Rexb = a.rex[(size_t)bh * (nch + 1) + ch];
-    __syncthreads();
-    if (has_bnd) {
-      const float* bst = a.states + ((size_t)bh * nch + ch) * S;
-      for (int idx = tid; idx < FB * (DV / 4); idx += NT) {
-        int p = idx % FB, d0 = (idx / FB) * 4;
-        f32x4 x = *(const f32x4*)(bst + (size_t)(fb * FB + p) * DV + d0);
+    {
+      // every global load of the chunk first, then the LDS stores
+      StageState<FB, DV, NT, true> sm;
+      StageRows<T, 32, FB, NT> sc;
+      StageRows<T, 32, DV, NT> sv;
+      StageRows<T, 32, D, NT> sq;
+      if (has_bnd) sm.load(a.states + ((size_t)bh * nch + ch) * S + (size_t)fb * FB * DV, tid);
+      sc.load(chis, M, s0, 0, n, tid);
+      sv.load(vs, DV, s0, 0, n, tid);
+      sq.load(qs, D, s0, 0, n, tid);
+      const float rjv = (tid < 32) ? a.rj[seq + min(s0 + tid, n - 1)] : 0.0f;
+      __syncthreads();
+      if (has_bnd)
+        sm.store(tid, [&](int p, int d0, const f32x4& x) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = (T)x[e];
-      }
+          for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = (T)x[e];
+        });
+      sc.store(sChi, C::CST, s0, 0, n, tid);
+      sv.store(sV, C::VST, s0, 0, n, tid);
+      if constexpr (sizeof(T) == 2) sq.store((f16*)sQ, D + PAD, s0, 0, n, tid);
+      else sq.store(sQ, D + PAD, s0, 0, n, tid);
+      if (tid < 32) sRj[tid] = (s0 + tid < n) ? rjv : 0.0f;
     }
-    copy_rows<T>(sChi, C::CST, chis, M, 32, FB, s0, 0, n, tid, NT);
-    copy_rows<T>(sV, C::VST, vs, DV, 32, DV, s0, 0, n, tid, NT);
-    if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
-    else copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
-    for (int j = tid; j < 32; j += NT) sRj[j] = (s0 + j < n) ? a.rj[seq + s0 + j] : 0.0f;
     __syncthreads();
 
 #pragma unroll 1
@@ -464,17 +479,25 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
 
   T* sOb = (T*)(smem + C::oOb);
-  copy_rows_as<T>(sOb, D + C::TPD, a.omega + ((size_t)hh * M + (size_t)fb * FB) * D, D, FB, D, 0, 0, FB, tid, NT);
-  if constexpr (sizeof(T) == 2) {
-    copy_rows_f16<float>((f16*)sOm, D + PAD, a.omega + ((size_t)hh * M + (size_t)fb * FB) * D, D, FB, D, 0, 0, FB,
-                         tid, NT, kLog2e);
-    copy_rows_f16<T>((f16*)sR, C::RST, rs_, D, 32, D, c0, 0, n, tid, NT);
-  } else {
-    copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fb * FB * D, D, FB, D, 0, 0, FB, tid, NT);
-    copy_rows<T>(sR, C::RST, rs_, D, 32, D, c0, 0, n, tid, NT);
+  {
+    // Omega (float32) once for both LDS copies, r and u of the anchor tile
+    StageRows<float, FB, D, NT> so;
+    StageRows<T, 32, D, NT> sr;
+    StageRows<T, 32, DV, NT> su;
+    so.load(a.omega + ((size_t)hh * M + (size_t)fb * FB) * D, D, 0, 0, FB, tid);
+    sr.load(rs_, D, c0, 0, n, tid);
+    su.load(us, DV, c0, 0, n, tid);
+    so.store(sOb, D + C::TPD, 0, 0, FB, tid);
+    if constexpr (sizeof(T) == 2) {
+      so.store((f16*)sOm, D + PAD, 0, 0, FB, tid, kLog2e);
+      sr.store((f16*)sR, C::RST, c0, 0, n, tid);
+      su.store((f16*)sU, DV + PAD, c0, 0, n, tid);
+    } else {
+      so.store(sOm, D + PAD, 0, 0, FB, tid, kLog2e);
+      sr.store(sR, C::RST, c0, 0, n, tid);
+      su.store(sU, DV + PAD, c0, 0, n, tid);
+    }
   }
-  if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sU, DV + PAD, us, DV, 32, DV, c0, 0, n, tid, NT);
-  else copy_rows<T>(sU, DV + PAD, us, DV, 32, DV, c0, 0, n, tid, NT);
   f32x16 dr[D / 32];
 #pragma unroll
   for (int Dt = 0; Dt < D / 32; ++Dt) dr[Dt] = zero16();
@@ -485,22 +508,43 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
     const int s0 = ch * 32;
     const bool has_bnd = ch > 0;
     const float Rexb = a.rex[(size_t)bh * (nch + 1) + ch];
-    __syncthreads();
-    if (has_bnd) {
+    {
+      // the chunk's global loads in two batches (the second half of the state
+      // with the chunk rows), each issued in full before its LDS stores
+      constexpr int FH = FB / 2;
+      StageState<FH, DV, NT, false> sm;
       const float* bst = a.states + ((size_t)bh * nch + ch) * S;
-      for (int idx = tid; idx < FB * (DV / 4); idx += NT) {
-        int p = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
-        f32x4 x = *(const f32x4*)(bst + (size_t)(fb * FB + p) * DV + d0);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) sMp[p * (DV + PAD) + d0 + e] = (T)x[e];
+      float av = 0.0f;
+      if (has_bnd) {
+        sm.load(bst + (size_t)fb * FB * DV, tid);
+        if (tid < FB) av = bst[(size_t)M * DV + fb * FB + tid];
       }
-      for (int p = tid; p < FB; p += NT) sA[p] = bst[(size_t)M * DV + fb * FB + p];
+      __syncthreads();
+      auto put = [&](int p0) {
+        return [&, p0](int p, int d0, const f32x4& x) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) sMp[(p0 + p) * (DV + PAD) + d0 + e] = (T)x[e];
+        };
+      };
+      if (has_bnd) {
+        sm.store(tid, put(0));
+        if (tid < FB) sA[tid] = av;
+        sm.load(bst + (size_t)(fb * FB + FH) * DV, tid);
+      }
+      StageRows<T, 32, FB, NT> sc;
+      StageRows<T, 32, DV, NT> sv;
+      StageRows<T, 32, D, NT> sq;
+      sc.load(chis, M, s0, 0, n, tid);
+      sv.load(vs, DV, s0, 0, n, tid);
+      sq.load(qs, D, s0, 0, n, tid);
+      const float rjv = (tid < 32) ? a.rj[seq + min(s0 + tid, n - 1)] : 0.0f;
+      if (has_bnd) sm.store(tid, put(FH));
+      sc.store(sChi, C::CST, s0, 0, n, tid);
+      sv.store(sV, C::VST, s0, 0, n, tid);
+      if constexpr (sizeof(T) == 2) sq.store((f16*)sQ, D + PAD, s0, 0, n, tid);
+      else sq.store(sQ, D + PAD, s0, 0, n, tid);
+      if (tid < 32) sRj[tid] = (s0 + tid < n) ? rjv : 0.0f;
     }
-    copy_rows<T>(sChi, C::CST, chis, M, 32, FB, s0, 0, n, tid, NT);
-    copy_rows<T>(sV, C::VST, vs, DV, 32, DV, s0, 0, n, tid, NT);
-    if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
-    else copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
-    for (int j = tid; j < 32; j += NT) sRj[j] = (s0 + j < n) ? a.rj[seq + s0 + j] : 0.0f;
     __syncthreads();
 
     // upstream-gradient rows are fetched one row ahead
@@ -797,10 +841,18 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
   const int w = a.w;
   const int pw = fb * FB + wv * 32;            // first feature of this wave's tile
 
-  if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sR, D + PAD, rs_, D, 32 * C::NT32, D, wb, 0, n, tid, NT);
-  else copy_rows<T>(sR, D + PAD, rs_, D, 32 * C::NT32, D, wb, 0, n, tid, NT);
-  copy_rows<T>(sU, DV + C::TP, us, DV, WIN, DV, wb, 0, n, tid, NT);
-  if (tid < 32) sL[tid] = (s0 + tid < n) ? a.stats[(seq + s0 + tid) * 2] : 0.0f;
+  {
+    // every global load of the window first, then the LDS stores
+    StageRows<T, 32 * C::NT32, D, NT> sr;
+    StageRows<T, WIN, DV, NT> su;
+    sr.load(rs_, D, wb, 0, n, tid);
+    su.load(us, DV, wb, 0, n, tid);
+    const float lv = (tid < 32) ? a.stats[(seq + min(s0 + tid, n - 1)) * 2] : 0.0f;
+    if constexpr (sizeof(T) == 2) sr.store((f16*)sR, D + PAD, wb, 0, n, tid);
+    else sr.store(sR, D + PAD, wb, 0, n, tid);
+    su.store(sU, DV + C::TP, wb, 0, n, tid);
+    if (tid < 32) sL[tid] = (s0 + tid < n) ? lv : 0.0f;
+  }
   __syncthreads();
   // wave 0: chunk key features and frames; the others: the |z|^2 table
   if (wv == 0)

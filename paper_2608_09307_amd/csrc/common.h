@@ -348,3 +348,117 @@ LS_DEV f16x8 tld_crow_f16(const f16* mat, int ld, int kbase, int sp, int n0) {
   return __builtin_bit_cast(f16x8, cat44(lds_tr4(tr_addr(m, ld, kbase + 16 * sp + 4 * h, n0)),
                                          lds_tr4(tr_addr(m, ld, kbase + 16 * sp + 8 + 4 * h, n0))));
 }
+
+// ---- batched global -> LDS staging ----
+// A copy is split into load() (every global load of the calling thread, into
+// registers) and store() (its LDS writes), so a kernel can issue the loads of
+// several copies back to back and pay one memory round trip for all of them.
+// Rows row0 .. row0 + ROWS - 1 of a [*, gstride] matrix are copied; rows
+// outside [lo, hi) become zero (their loads read a clamped valid row).
+template <typename T, int ROWS, int COLS, int NT>
+struct StageRows {
+  static constexpr int VE = 16 / (int)sizeof(T);
+  static constexpr int CPR = COLS / VE;
+  static constexpr int N = ROWS * CPR;
+  static constexpr int IT = (N + NT - 1) / NT;
+  static_assert(COLS % VE == 0, "16-byte pieces");
+  typedef T V __attribute__((ext_vector_type(VE)));
+  V x[IT];
+  LS_DEV void load(const T* g, int gstride, int row0, int lo, int hi, int tid) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = min(tid + NT * it, N - 1);
+      const int r = idx / CPR, c = (idx % CPR) * VE;
+      const int gr = min(max(row0 + r, lo), hi - 1);
+      x[it] = *(const V*)(g + (size_t)gr * gstride + c);
+    }
+  }
+  // stores as Tout (the same type, or f16), times `scale` when converting
+  template <typename Tout>
+  LS_DEV void store(Tout* lds, int lstride, int row0, int lo, int hi, int tid, float scale = 1.0f) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + NT * it;
+      if (N % NT != 0 && idx >= N) continue;
+      const int r = idx / CPR, c = (idx % CPR) * VE;
+      const bool ok = row0 + r >= lo && row0 + r < hi;
+      typedef Tout VO __attribute__((ext_vector_type(VE)));
+      VO y;
+#pragma unroll
+      for (int e = 0; e < VE; ++e) y[e] = ok ? (Tout)((float)x[it][e] * scale) : (Tout)0.0f;
+      if ((lstride * (int)sizeof(Tout)) % (VE * (int)sizeof(Tout)) == 0) {
+        *(VO*)(lds + r * lstride + c) = y;
+      } else {
+#pragma unroll
+        for (int e = 0; e < VE; ++e) lds[r * lstride + c + e] = y[e];
+      }
+    }
+  }
+};
+
+// FB x DV float32 block of a state (row stride DV), staged like StageRows.
+// PFAST picks the piece order: row index fastest across lanes (for transposed
+// LDS layouts) or the natural row-major order.
+template <int FB, int DV, int NT, bool PFAST>
+struct StageState {
+  static constexpr int N = FB * (DV / 4);
+  static constexpr int IT = (N + NT - 1) / NT;
+  f32x4 x[IT];
+  LS_DEV static void where(int idx, int& p, int& d0) {
+    if (PFAST) { p = idx % FB; d0 = (idx / FB) * 4; }
+    else { p = idx / (DV / 4); d0 = (idx % (DV / 4)) * 4; }
+  }
+  LS_DEV void load(const float* g, int tid) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      int p, d0;
+      where(min(tid + NT * it, N - 1), p, d0);
+      x[it] = *(const f32x4*)(g + (size_t)p * DV + d0);
+    }
+  }
+  // put(p, d0, x): store four consecutive columns of row p
+  template <class Put> LS_DEV void store(int tid, Put put) const {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + NT * it;
+      if (N % NT != 0 && idx >= N) continue;
+      int p, d0;
+      where(idx, p, d0);
+      put(p, d0, x[it]);
+    }
+  }
+};
+
+// Like StageRows, in 4-element pieces with the row index fastest across
+// lanes, for stores into transposed LDS layouts (the 2-byte writes of one
+// instruction then fall in one LDS row).  put(r, c0, x) stores the four
+// values of row r, columns c0 .. c0 + 3 (zero for rows outside [lo, hi)).
+template <typename T, int ROWS, int COLS, int NT>
+struct StageRowsT {
+  static constexpr int N = ROWS * (COLS / 4);
+  static constexpr int IT = (N + NT - 1) / NT;
+  typedef T V4 __attribute__((ext_vector_type(4)));
+  V4 x[IT];
+  LS_DEV void load(const T* g, int gstride, int row0, int lo, int hi, int tid) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = min(tid + NT * it, N - 1);
+      const int r = idx % ROWS, c0 = (idx / ROWS) * 4;
+      const int gr = min(max(row0 + r, lo), hi - 1);
+      x[it] = *(const V4*)(g + (size_t)gr * gstride + c0);
+    }
+  }
+  template <class Put> LS_DEV void store(int row0, int lo, int hi, int tid, Put put) const {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + NT * it;
+      if (N % NT != 0 && idx >= N) continue;
+      const int r = idx % ROWS, c0 = (idx / ROWS) * 4;
+      const bool ok = row0 + r >= lo && row0 + r < hi;
+      V4 y;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) y[e] = ok ? x[it][e] : (T)0.0f;
+      put(r, c0, y);
+    }
+  }
+};

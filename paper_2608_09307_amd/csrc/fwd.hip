@@ -15,6 +15,8 @@
 // carries its frame, so neither side can overflow and a row never sees a
 // future token's scale.  The 1/sqrt(m) of the query feature is dropped (it
 // cancels in the ratio, App. A "Feature scaling").
+#include <type_traits>
+
 #include "common.h"
 #include "linsimp_internal.h"
 #include "prof.h"
@@ -246,39 +248,52 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
   if (wv == 0) chunk_key_features<T, D, M>(ks, s0, n, omk_h, Rexb, sChi, M + PAD, sRj);
   // ---- prologue: everything else (all waves) ----
   const int fbk = blockIdx.z;
-  if constexpr (sizeof(T) == 2)
-    copy_rows_f16<float>((f16*)sOm, D + PAD, a.omega + ((size_t)hh * M + (size_t)fbk * FB) * D, D, FB, D, 0, 0, FB,
-                         tid, NT, kLog2e);
-  else
-    copy_rows<T>(sOm, D + PAD, omq_h + (size_t)fbk * FB * D, D, FB, D, 0, 0, FB, tid, NT);
-  // transposed copies: consecutive lanes take consecutive p (or j), so the
-  // 2-byte LDS writes of one instruction fall in one row
-  for (int idx = tid; idx < FB * (DV / 4); idx += NT) {
-    int p = idx % FB, d0 = (idx / FB) * 4;
-    f32x4 x = has_bnd ? *(const f32x4*)(bst + (size_t)(fbk * FB + p) * DV + d0)
-                      : f32x4{0.f, 0.f, 0.f, 0.f};
+  {
+    // every global load of the prologue first, then the LDS stores; the
+    // transposed copies take the row index fastest across lanes, so the
+    // 2-byte LDS writes of one instruction fall in one row
+    using OmT = typename std::conditional<sizeof(T) == 2, float, T>::type;
+    StageRows<OmT, FB, D, NT> so;
+    StageState<FB, DV, NT, true> sm;
+    StageRowsT<T, 32, DV, NT> sv;
+    StageRows<T, WIN, D, NT> sr;
+    StageRowsT<T, WIN, DV, NT> su;
+    StageRows<T, 32, D, NT> sq;
+    if constexpr (sizeof(T) == 2) so.load(a.omega + ((size_t)hh * M + (size_t)fbk * FB) * D, D, 0, 0, FB, tid);
+    else so.load(omq_h + (size_t)fbk * FB * D, D, 0, 0, FB, tid);
+    if (has_bnd) sm.load(bst + (size_t)fbk * FB * DV, tid);
+    sv.load(vs, DV, s0, 0, n, tid);
+    sr.load(rs_, D, wb, 0, n, tid);
+    su.load(us, DV, wb, 0, n, tid);
+    sq.load(qs, D, s0, 0, n, tid);
+    float av[(M + NT - 1) / NT];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = (T)x[e];
-  }
-  for (int p = tid; p < M; p += NT) sA[p] = has_bnd ? bst[(size_t)M * DV + p] : 0.0f;
-  for (int idx = tid; idx < 32 * (DV / 4); idx += NT) {
-    int jj = idx % 32, d0 = (idx / 32) * 4;
-    bool ok = s0 + jj < n;
+    for (int k = 0; k < (M + NT - 1) / NT; ++k) {
+      const int p = tid + NT * k;
+      av[k] = (has_bnd && p < M) ? bst[(size_t)M * DV + p] : 0.0f;
+    }
+    if constexpr (sizeof(T) == 2) so.store((f16*)sOm, D + PAD, 0, 0, FB, tid, kLog2e);
+    else so.store(sOm, D + PAD, 0, 0, FB, tid);
+    sm.store(tid, [&](int p, int d0, const f32x4& x) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      sVt[(d0 + e) * (32 + PAD) + F::sigma(jj)] = ok ? vs[(size_t)(s0 + jj) * DV + d0 + e] : (T)0.0f;
-  }
-  if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sR, D + PAD, rs_, D, WIN, D, wb, 0, n, tid, NT);
-  else copy_rows<T>(sR, D + PAD, rs_, D, WIN, D, wb, 0, n, tid, NT);
-  for (int idx = tid; idx < WIN * (DV / 4); idx += NT) {
-    int wi = idx / (DV / 4), d0 = (idx % (DV / 4)) * 4;
-    int c = wb + wi;
-    bool ok = c >= 0 && c < n;
+      for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = has_bnd ? (T)x[e] : (T)0.0f;
+    });
 #pragma unroll
-    for (int e = 0; e < 4; ++e) sUt[(d0 + e) * UST + wi] = ok ? us[(size_t)c * DV + d0 + e] : (T)0.0f;
+    for (int k = 0; k < (M + NT - 1) / NT; ++k)
+      if (tid + NT * k < M) sA[tid + NT * k] = av[k];
+    sv.store(s0, 0, n, tid, [&](int jj, int d0, const typename StageRowsT<T, 32, DV, NT>::V4& x) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sVt[(d0 + e) * (32 + PAD) + F::sigma(jj)] = x[e];
+    });
+    if constexpr (sizeof(T) == 2) sr.store((f16*)sR, D + PAD, wb, 0, n, tid);
+    else sr.store(sR, D + PAD, wb, 0, n, tid);
+    su.store(wb, 0, n, tid, [&](int wi, int d0, const typename StageRowsT<T, WIN, DV, NT>::V4& x) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sUt[(d0 + e) * UST + wi] = x[e];
+    });
+    if constexpr (sizeof(T) == 2) sq.store((f16*)sQ, D + PAD, s0, 0, n, tid);
+    else sq.store(sQ, D + PAD, s0, 0, n, tid);
   }
-  if constexpr (sizeof(T) == 2) copy_rows_f16<T>((f16*)sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
-  else copy_rows<T>(sQ, D + PAD, qs, D, 32, D, s0, 0, n, tid, NT);
   __syncthreads();
 
   const int fb = blockIdx.z;       // feature block handled by this workgroup
