@@ -1151,7 +1151,11 @@ __global__ __launch_bounds__(512) void k_bwd_keys(BwdArgs a, int nfb) {
   const int bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch;
   const int cb = blockIdx.x * C::CPB + cw;
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
-  copy_rows<T>(sOm, D + TP, omq_h, D, M, D, 0, 0, M, tid, 64 * C::CPB * WPC);
+  {
+    StageRows<T, M, D, 64 * C::CPB * WPC> so;
+    so.load(omq_h, D, 0, 0, M, tid);
+    so.store(sOm, D + TP, 0, 0, M, tid);
+  }
   const bool active = cb < nch;                       // wave-uniform
   const int cbx = active ? cb : nch - 1;
   const int s0 = cbx * 32;
@@ -1171,7 +1175,7 @@ __global__ __launch_bounds__(512) void k_bwd_keys(BwdArgs a, int nfb) {
     f32x16 X = zero16();
     if (has_after) {
       const float* grow = G + (size_t)(pt * 32 + col) * DV;
-#pragma unroll 2
+#pragma unroll
       for (int s = 0; s < DV / F::KS; ++s) {
         const int k0 = s * F::KS + h * F::KPL;
         typename F::frag hi, lo;
