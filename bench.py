@@ -75,10 +75,18 @@ def head_stream_bytes(wl, es=2):
     }
 
 
-def src_digest():
+HEADERS = ["common.h", "keyfeat.h", "linsimp_internal.h", "prof.h"]
+KERNEL_FILES = {"fwd_readout": ["fwd.hip"] + HEADERS, "bwd_du": ["bwd.hip"] + HEADERS,
+                "bwd_dqdr": ["bwd.hip"] + HEADERS, "bwd_state": ["bwd.hip"] + HEADERS,
+                "bwd_keys": ["bwd.hip"] + HEADERS}
+
+
+def src_digest(files=None):
+    """sha256 prefix of the named kernel sources (all of csrc/ by default)."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2608_09307_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
+    names = sorted(files) if files else sorted(os.listdir(csrc))
+    for name in names:
         if name.endswith((".hip", ".h", ".cpp")):
             with open(os.path.join(csrc, name), "rb") as fh:
                 h.update(name.encode())
@@ -92,17 +100,17 @@ KERNEL_SYMBOLS = {"fwd_readout": "k_readout", "bwd_du": "k_bwd_du", "bwd_dqdr": 
 
 def traffic_for(kernel):
     """Calibrated HBM bytes (FETCH_SIZE + WRITE_SIZE) per launch of `kernel`
-    from the committed counter runs, if they were taken on the current kernel
-    sources; else None."""
+    from the committed counter runs, if they were taken on the kernel's
+    current sources (its .hip file and the headers it includes); else None."""
     try:
         with open(TRAFFIC_FILE) as fh:
             t = json.load(fh)
     except (OSError, ValueError):
         return None
-    if t.get("src_sha") != src_digest():
-        return None
     per = t.get("per_kernel", {}).get(KERNEL_SYMBOLS.get(kernel, ""))
-    if per is None:
+    if per is None or kernel not in KERNEL_FILES:
+        return None
+    if per.get("src_sha") != src_digest(KERNEL_FILES[kernel]):
         return None
     return per["fetch_bytes"] + per["write_bytes"]
 
