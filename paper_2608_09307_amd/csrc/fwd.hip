@@ -184,6 +184,137 @@ __global__ __launch_bounds__(256) void k_state_scan(FwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Prefill: the state after all n tokens of each (sequence, head), directly
+// (eq:Mstate, eq:astate summed over the whole prefix, Theorem 1).  One
+// workgroup per (sequence, head); wave wv owns features 32 wv .. 32 wv + 31 and
+// walks the chunks in order, keeping its rows of M and a in registers in the
+// running key frame R (log2): per chunk, the key log2-features (bf16 hi/lo
+// Omega, two MFMAs per k-step), the chunk maximum shared across the waves,
+// the frame update (M, a scaled by 2^(R - R')), then M += chi^T V on the
+// matrix cores.  The chunk's k rows and V^T are staged in LDS one chunk ahead.
+// Nothing but the final state is written (the chunked forward materialises
+// every chunk's contribution instead).  bf16 inputs, m <= 128.
+// ---------------------------------------------------------------------------
+template <int D, int DV, int M>
+__global__ __launch_bounds__(256) void k_prefill_state(FwdArgs a) {
+  using T = bf16;
+  using F = MF<T>;
+  constexpr int PAD = F::PAD, PT = M / 32;
+  static_assert(PT <= 4, "one feature tile per wave");
+  __shared__ __align__(16) T sK[2][32][D + PAD];
+  __shared__ __align__(16) T sVt[2][DV][32 + PAD];
+  __shared__ float snk[4][32];
+  __shared__ float smx[4];
+  const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
+  const int bh = blockIdx.x, hh = bh % a.H, n = a.n, nch = a.nch;
+  const bool owner = wv < PT;
+  const size_t seq = (size_t)bh * n;
+  const T* ks = (const T*)a.k + seq * D;
+  const T* vs = (const T*)a.v + seq * DV;
+  const T* omk_h = (const T*)a.omk + (size_t)hh * 2 * M * D;
+  // this wave's Omega tile (hi, lo): B operands, lanes <-> feature p
+  typename F::frag oh[D / F::KS], ol[D / F::KS];
+#pragma unroll
+  for (int s = 0; s < D / F::KS; ++s) {
+    const int k0 = s * F::KS + h * F::KPL;
+    const int pr = (owner ? wv : 0) * 32 + col;
+    oh[s] = F::ld(omk_h + (size_t)pr * D, k0);
+    ol[s] = F::ld(omk_h + (size_t)M * D + (size_t)pr * D, k0);
+  }
+  f32x16 Macc[DV / 32];
+#pragma unroll
+  for (int dt = 0; dt < DV / 32; ++dt) Macc[dt] = zero16();
+  float apart = 0.0f;                          // sum over this lane's tokens of chi_p, p = 32 wv + col
+  float R = kNegInf;
+  const float rs = rsqrtf((float)M);
+
+  StageRows<T, 32, D, 256> sk;
+  StageRowsT<T, 32, DV, 256> sv;
+  auto stage_store = [&](int b, int buf) {
+    sk.store(&sK[buf][0][0], D + PAD, b * 32, 0, n, tid);
+    sv.store(b * 32, 0, n, tid, [&](int jj, int d0, const typename StageRowsT<T, 32, DV, 256>::V4& x) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sVt[buf][d0 + e][F::sigma(jj)] = x[e];
+    });
+  };
+  sk.load(ks, D, 0, 0, n, tid);
+  sv.load(vs, DV, 0, 0, n, tid);
+  stage_store(0, 0);
+
+#pragma unroll 1
+  for (int b = 0; b < nch; ++b) {
+    const int cur = b & 1;
+    __syncthreads();                           // chunk b staged; the other buffer is free
+    if (b + 1 < nch) {
+      sk.load(ks, D, (b + 1) * 32, 0, n, tid);
+      sv.load(vs, DV, (b + 1) * 32, 0, n, tid);
+    }
+    // key log2-features of the tile: regs <-> token crow(v, h), lanes <-> p
+    f32x16 acc = zero16();
+    float mx = kNegInf;
+    if (owner) {
+      float nkp = 0.0f;
+      const T* krow = &sK[cur][col][0];
+#pragma unroll
+      for (int s = 0; s < D / F::KS; ++s) {
+        const typename F::frag kf = F::ld(krow, s * F::KS + h * F::KPL);
+#pragma unroll
+        for (int e = 0; e < F::KPL; ++e) { const float x = fel(kf, e); nkp += x * x; }
+        acc = F::mma(kf, oh[s], acc);
+        acc = F::mma(kf, ol[s], acc);
+      }
+      const float nk = half_swap_add(nkp);     // |k|^2 of token col
+      if (h == 0) snk[wv][col] = nk;
+      wave_lds_sync();
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int tk = crow(v, h);
+        const float x = (b * 32 + tk < n) ? acc[v] - 0.5f * kLog2e * snk[wv][tk] : kNegInf;
+        acc[v] = x;
+        mx = fmaxf(mx, x);
+      }
+      mx = wave_max(mx);
+    }
+    if (l == 0) smx[wv] = mx;
+    if (b + 1 < nch) stage_store(b + 1, cur ^ 1);
+    __syncthreads();
+    const float cm = fmaxf(fmaxf(smx[0], smx[1]), fmaxf(smx[2], smx[3]));
+    const float Rn = fmaxf(R, cm);
+    if (owner) {
+      const float sa = fast_exp2(R - Rn);      // 0 while the state is empty
+      if (sa != 1.0f) {
+#pragma unroll
+        for (int dt = 0; dt < DV / 32; ++dt) Macc[dt] *= sa;
+        apart *= sa;
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float c = fast_exp2(acc[v] - Rn) * rs;
+        acc[v] = c;
+        apart += c;
+      }
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt)
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp)
+          Macc[dt] = F::mma(F::cfrag(acc, sp), F::ldc(&sVt[cur][dt * 32 + col][0], 0, sp, h), Macc[dt]);
+    }
+    R = Rn;
+  }
+  // M rows p = 32 wv + crow(v, h) (lanes <-> d), a[p], the frame
+  if (owner) {
+    float* Mo = a.final_M + (size_t)bh * M * DV;
+#pragma unroll
+    for (int dt = 0; dt < DV / 32; ++dt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) Mo[(size_t)(wv * 32 + crow(v, h)) * DV + dt * 32 + col] = Macc[dt][v];
+    const float at = half_swap_add(apart);
+    if (h == 0) a.final_a[(size_t)bh * M + wv * 32 + col] = at;
+  }
+  if (tid == 0) a.final_rex[bh] = R;
+}
+
+// ---------------------------------------------------------------------------
 // K3: anchor-window readout for one chunk of 32 rows.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int DV, int M, int NW, int NA>
@@ -496,6 +627,18 @@ static int run_fwd(const Shape& s, FwdArgs a, hipStream_t st) {
     int tot = (int)s.H * M * D;
     ProfScope ps("prep_omega", st);
     k_prep_omega<T><<<(tot + 255) / 256, 256, 0, st>>>(a.omega, (T*)a.omq, (T*)a.omk, (int)s.H, M * D);
+  }
+  if constexpr (sizeof(T) == 2 && M <= 128) {
+    if (a.out == nullptr && a.final_M != nullptr) {   // prefill: the final state only
+      { ProfScope ps("prefill_state", st);
+      k_prefill_state<D, DV, M><<<BH, 256, 0, st>>>(a); }
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) {
+        set_error("prefill launch failed: %s", hipGetErrorString(e));
+        return -4;
+      }
+      return 0;
+    }
   }
   { ProfScope ps("chunk_state", st);
   k_chunk_state<T, D, DV, M><<<dim3((nch + 3) / 4, BH), 256, 0, st>>>(a); }
