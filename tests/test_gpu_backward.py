@@ -1,10 +1,14 @@
 """GPU parity of the backward pass against the float64 oracle (through the C ABI).
 
 Each gradient (dq, dk, dv, dr, du) is held to relative L2 <= 1e-4 for float32
-inputs and <= 2e-2 for bf16 inputs.  Shapes cover several segments of the
-query sweeps (segment edges use atomics), ragged tails, windows that are not
-multiples of 32, w = 1, both feature-block layouts (m = 256 splits features in
-two) and full-size sampled heads of the 16k layer and the 64k stress shape.
+inputs and <= 2e-2 for bf16 inputs.  A gradient that is exactly zero in the
+definition (n = 1: the output is v_0 (*) u_0 whatever q, k, r are; its
+reference norm is below 1e-6 of the largest of the five) has no relative
+scale; its error is measured against the largest reference gradient norm,
+the size of the terms that cancel in it.  Shapes cover several chunks, ragged tails,
+windows that are not multiples of 32, w = 1, single rows and single partial
+chunks, both feature-block layouts (m = 256 splits features in two) and
+full-size sampled heads of the 16k layer and the 64k stress shape.
 """
 
 import numpy as np
@@ -32,11 +36,14 @@ def _run(wl: Workload, pairs=None):
         pairs = [(b, h) for b in range(wl.B) for h in range(wl.H)]
     ref = oracle_backward(x, wl.w, pairs)
     errs = {}
+    exps = [np.stack([ref[p][gi] for p in pairs]) for gi in range(len(NAMES))]
+    big = max(np.linalg.norm(e) for e in exps)
     for gi, nm in enumerate(NAMES):
         got = np.stack([f64(grads[gi][b, h]) for b, h in pairs])
-        exp = np.stack([ref[p][gi] for p in pairs])
+        exp = exps[gi]
         assert np.all(np.isfinite(got)), nm
-        errs[nm] = rel_l2(got, exp)
+        den = np.linalg.norm(exp) if np.linalg.norm(exp) > 1e-6 * big else big
+        errs[nm] = float(np.linalg.norm(got - exp) / den)
     print("      " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()), flush=True)
     for nm, e in errs.items():
         assert e <= TOL[wl.dtype], (nm, e)
@@ -58,6 +65,17 @@ def test_backward_f32_structure(D, m, n, w, B, H):
 def test_backward_bf16_shapes(D, m, n, w):
     _run(Workload("bf16_bwd", 1, 2, n, D, D, m, w, "bf16", "fwdbwd", seed=32,
                   boost_frac=0.05 if m == 256 else 0.0, boost=4.0))
+
+
+@pytest.mark.parametrize("D,m,n,w,dt", [
+    (32, 32, 1, 64, "f32"),       # a single row
+    (128, 128, 1, 64, "bf16"),
+    (128, 128, 31, 64, "bf16"),   # one partial chunk
+    (64, 64, 33, 5, "bf16"),      # chunk boundary + 1, short window
+    (128, 256, 40, 64, "bf16"),   # two feature blocks, short sequence
+])
+def test_backward_edge_lengths(D, m, n, w, dt):
+    _run(Workload("edge_bwd", 1, 2, n, D, D, m, w, dt, "fwdbwd", seed=34))
 
 
 def test_backward_layer16k_sampled_heads():
