@@ -5,7 +5,8 @@ Workload: the 16k-context layer (B=2, H=16, n=16384, d=m=128, w=64; bf16
 inputs, float32 state), synthetic seeded inputs resident in HBM.  One step is
 the whole hot path: forward (key feature map, chunk states, chunk scan,
 anchor-window readout) and backward (query sweeps, state sweep, reverse scan,
-key side) on the same batch.
+key side) on the same batch; the backward reuses the boundary states the
+forward left in the shared workspace.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--head]
 
@@ -193,23 +194,24 @@ def main():
     wl = WORKLOADS[WORKLOAD]
     x = make_inputs(wl, device=dev, with_grad=True)
     d = L.dims_of(x["q"], x["v"], x["omega"], wl.w)
-    ws_f = L.alloc_workspace(d, False, dev)
     ws_b = L.alloc_workspace(d, True, dev)
     out = torch.empty_like(x["v"])
     stats = torch.empty(x["q"].shape[:3] + (2,), dtype=torch.float32, device=dev)
     grads = tuple(torch.empty_like(x[nm]) for nm in ("q", "k", "v", "r", "u"))
 
     def step():
+        # the forward writes its boundary states into the backward-sized
+        # workspace and the backward reuses them (LINSIMP_BWD_REUSE_STATES)
         L.fwd(x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w, out=out, stats=stats,
-              workspace=ws_f)
+              workspace=ws_b)
         L.bwd(x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w, out, stats, x["dO"],
-              grads=grads, workspace=ws_b)
+              grads=grads, workspace=ws_b, reuse_states=True)
 
     if args.head:
         import ctypes
         hp = make_head_params(wl, device=dev)
         hargs = (x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w, hp["tau"], hp["gate"])
-        del ws_f, ws_b
+        del ws_b
         hws = L._aligned_bytes(int(L.lib().linsimp_head_workspace_size(ctypes.byref(d), 1)), dev)
         y, saved = L.head_fwd(*hargs, workspace=hws)
 

@@ -101,6 +101,24 @@ int linsimp_bwd(const linsimp_dims* dims, const void* q, const void* k, const vo
                 const float* stats, const void* dout, void* dq, void* dk, void* dv, void* dr,
                 void* du, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Flags of linsimp_bwd_ex. */
+enum {
+  /* The workspace is the one the matching linsimp_fwd call used (sized for
+   * the backward, linsimp_workspace_size(dims, 1)), with the same dims and
+   * inputs, and nothing has written it since: its feature-bank copies and
+   * boundary states are reused instead of recomputed (the backward otherwise
+   * re-runs the forward's state pass).  Results are bitwise those of
+   * linsimp_bwd. */
+  LINSIMP_BWD_REUSE_STATES = 1
+};
+
+/* linsimp_bwd with flags (0 or LINSIMP_BWD_REUSE_STATES); otherwise the same
+ * contract. */
+int linsimp_bwd_ex(const linsimp_dims* dims, const void* q, const void* k, const void* v,
+                   const void* r, const void* u, const float* omega, const void* out,
+                   const float* stats, const void* dout, void* dq, void* dk, void* dv, void* dr,
+                   void* du, int32_t flags, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Prefill: build the decode state of Theorem 1 from a prefix of n tokens
  * (dims->n) per sequence; dims->B is the number of sequences S.
  *   k, r : [S, H, n, D] dtype;  v, u : [S, H, n, Dv] dtype; omega [H, m, D] f32

@@ -219,6 +219,18 @@ int linsimp_bwd(const linsimp_dims* dims, const void* q, const void* k, const vo
                 const void* r, const void* u, const float* omega, const void* out,
                 const float* stats, const void* dout, void* dq, void* dk, void* dv, void* dr,
                 void* du, void* workspace, size_t workspace_bytes_, void* stream) {
+  return linsimp_bwd_ex(dims, q, k, v, r, u, omega, out, stats, dout, dq, dk, dv, dr, du, 0, workspace,
+                        workspace_bytes_, stream);
+}
+
+int linsimp_bwd_ex(const linsimp_dims* dims, const void* q, const void* k, const void* v,
+                   const void* r, const void* u, const float* omega, const void* out,
+                   const float* stats, const void* dout, void* dq, void* dk, void* dv, void* dr,
+                   void* du, int32_t flags, void* workspace, size_t workspace_bytes_, void* stream) {
+  if (flags != 0 && flags != LINSIMP_BWD_REUSE_STATES) {
+    set_error("bwd flags %d: only 0 or LINSIMP_BWD_REUSE_STATES", flags);
+    return LINSIMP_E_INVALID_ARG;
+  }
   Shape s;
   int rc = check_dims(dims, &s, true);
   if (rc) return rc;
@@ -228,7 +240,7 @@ int linsimp_bwd(const linsimp_dims* dims, const void* q, const void* k, const vo
   Workspace ws;
   carve(s, workspace, true, &ws);
   return launch_backward(s, q, k, v, r, u, omega, out, stats, dout, dq, dk, dv, dr, du, ws,
-                         (hipStream_t)stream);
+                         (hipStream_t)stream, flags == LINSIMP_BWD_REUSE_STATES);
 }
 
 int linsimp_prefill(const linsimp_dims* dims, const void* k, const void* v, const void* r,
@@ -506,6 +518,6 @@ int linsimp_feature_bank(int32_t H, int32_t m, int32_t D, const float* gauss, co
 
 const char* linsimp_last_error(void) { return g_err; }
 
-int linsimp_version(void) { return 101; }
+int linsimp_version(void) { return 102; }
 
 }  // extern "C"

@@ -1358,10 +1358,13 @@ static int run_bwd(const Shape& s, BwdArgs a, hipStream_t st) {
 int launch_backward(const Shape& s, const void* q, const void* k, const void* v, const void* r,
                     const void* u, const float* omega, const void* out, const float* stats,
                     const void* dout, void* dq, void* dk, void* dv, void* dr, void* du,
-                    const Workspace& ws, hipStream_t st) {
-  // recompute the forward's prefix states (boundary states and frames)
-  int rc = launch_forward(s, q, k, v, r, u, omega, nullptr, nullptr, nullptr, nullptr, nullptr, ws, st);
-  if (rc) return rc;
+                    const Workspace& ws, hipStream_t st, bool reuse_states) {
+  // the forward's prefix states (boundary states and frames): recomputed,
+  // unless the caller's workspace still holds them from the forward
+  if (!reuse_states) {
+    int rc = launch_forward(s, q, k, v, r, u, omega, nullptr, nullptr, nullptr, nullptr, nullptr, ws, st);
+    if (rc) return rc;
+  }
   BwdArgs a;
   a.q = q; a.k = k; a.v = v; a.r = r; a.u = u; a.omega = omega; a.out = out; a.stats = stats;
   a.dout = dout; a.dq = dq; a.dk = dk; a.dv = dv; a.dr = dr; a.du = du;

@@ -63,7 +63,7 @@ int launch_ring_fill(const Shape& s, const void* r, const void* u, void* ring_r,
 int launch_backward(const Shape& s, const void* q, const void* k, const void* v, const void* r,
                     const void* u, const float* omega, const void* out, const float* stats,
                     const void* dout, void* dq, void* dk, void* dv, void* dr, void* du,
-                    const Workspace& ws, hipStream_t st);
+                    const Workspace& ws, hipStream_t st, bool reuse_states = false);
 
 int launch_decode(int64_t S, int H, int ntok, int D, int Dv, int m, int w, int dtype, float eps,
                   const void* q, const void* k, const void* v, const void* r, const void* u,

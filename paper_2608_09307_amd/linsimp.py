@@ -41,7 +41,9 @@ class HeadOpts(ctypes.Structure):
 GATE_HEAD, GATE_CHANNEL = 0, 1
 NORM_EPS, RMS_EPS = 1e-12, 1e-6
 
-EXPORTS = ("linsimp_workspace_size", "linsimp_fwd", "linsimp_bwd", "linsimp_prefill",
+BWD_REUSE_STATES = 1
+
+EXPORTS = ("linsimp_workspace_size", "linsimp_fwd", "linsimp_bwd", "linsimp_bwd_ex", "linsimp_prefill",
            "linsimp_decode_step", "linsimp_decode_chunk", "linsimp_timing_enable",
            "linsimp_timing_read", "linsimp_last_error", "linsimp_version")
 HEAD_EXPORTS = ("linsimp_head_saved_size", "linsimp_head_workspace_size", "linsimp_head_fwd",
@@ -69,6 +71,8 @@ def lib():
     L.linsimp_fwd.restype = ctypes.c_int
     L.linsimp_bwd.argtypes = [pd] + [vp] * 14 + [vp, sz, vp]
     L.linsimp_bwd.restype = ctypes.c_int
+    L.linsimp_bwd_ex.argtypes = [pd] + [vp] * 14 + [i32, vp, sz, vp]
+    L.linsimp_bwd_ex.restype = ctypes.c_int
     L.linsimp_prefill.argtypes = [pd] + [vp] * 11 + [vp, sz, vp]
     L.linsimp_prefill.restype = ctypes.c_int
     L.linsimp_decode_step.argtypes = [i64, i32, i32, i32, i32, i32, i32, f32] + [vp] * 13 + [vp]
@@ -165,19 +169,25 @@ def fwd(q, k, v, r, u, omega, w, eps=EPS, out=None, stats=None, workspace=None,
     return out, stats
 
 
-def bwd(q, k, v, r, u, omega, w, out, stats, dout, eps=EPS, grads=None, workspace=None):
-    """Backward pass; returns (dq, dk, dv, dr, du).  See linsimp_bwd."""
+def bwd(q, k, v, r, u, omega, w, out, stats, dout, eps=EPS, grads=None, workspace=None,
+        reuse_states=False):
+    """Backward pass; returns (dq, dk, dv, dr, du).  See linsimp_bwd; with
+    ``reuse_states`` (linsimp_bwd_ex, LINSIMP_BWD_REUSE_STATES) ``workspace``
+    must be the backward-sized workspace the matching fwd call used."""
     d = dims_of(q, v, omega, w, eps)
     if grads is None:
         grads = tuple(torch.empty_like(x) for x in (q, k, v, r, u))
     dq, dk, dv, dr, du = grads
     if workspace is None:
+        if reuse_states:
+            raise ValueError("reuse_states needs the workspace of the matching forward call")
         workspace = alloc_workspace(d, True, q.device)
-    _check(lib().linsimp_bwd(ctypes.byref(d), _ptr(q, "q"), _ptr(k, "k"), _ptr(v, "v"),
-                             _ptr(r, "r"), _ptr(u, "u"), _ptr(omega, "omega"), _ptr(out, "out"),
-                             _ptr(stats, "stats"), _ptr(dout, "dout"), _ptr(dq, "dq"),
-                             _ptr(dk, "dk"), _ptr(dv, "dv"), _ptr(dr, "dr"), _ptr(du, "du"),
-                             _ptr(workspace, "workspace"), workspace.numel(), _stream()))
+    _check(lib().linsimp_bwd_ex(ctypes.byref(d), _ptr(q, "q"), _ptr(k, "k"), _ptr(v, "v"),
+                                _ptr(r, "r"), _ptr(u, "u"), _ptr(omega, "omega"), _ptr(out, "out"),
+                                _ptr(stats, "stats"), _ptr(dout, "dout"), _ptr(dq, "dq"),
+                                _ptr(dk, "dk"), _ptr(dv, "dv"), _ptr(dr, "dr"), _ptr(du, "du"),
+                                BWD_REUSE_STATES if reuse_states else 0,
+                                _ptr(workspace, "workspace"), workspace.numel(), _stream()))
     return dq, dk, dv, dr, du
 
 

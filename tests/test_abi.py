@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
         assert set(names) == set(exports), header
         for name in names:
             assert hasattr(lib, name), name
-    assert lib.linsimp_version() == 101
+    assert lib.linsimp_version() == 102
 
 
 def test_head_sizes_and_argument_errors():

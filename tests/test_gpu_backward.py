@@ -97,3 +97,21 @@ def test_backward_bitwise_deterministic():
     torch.cuda.synchronize()
     for nm, a_, b_ in zip(NAMES, g1, g2):
         assert torch.equal(a_, b_), nm
+
+
+@pytest.mark.parametrize("D,m,n,w,dt", [(128, 128, 700, 64, "bf16"), (128, 256, 300, 64, "bf16"),
+                                        (32, 32, 100, 20, "f32")])
+def test_backward_reusing_forward_states_is_bitwise_equal(D, m, n, w, dt):
+    """linsimp_bwd_ex with LINSIMP_BWD_REUSE_STATES on the workspace the forward
+    used gives the bits of the recomputing backward."""
+    wl = Workload("reuse", 2, 2, n, D, D, m, w, dt, "fwdbwd", seed=35)
+    x = make_inputs(wl, device=DEV, with_grad=True)
+    d = L.dims_of(x["q"], x["v"], x["omega"], wl.w)
+    ws = L.alloc_workspace(d, True, DEV)
+    args = (x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w)
+    out, stats = L.fwd(*args, workspace=ws)
+    g_re = tuple(t.clone() for t in L.bwd(*args, out, stats, x["dO"], workspace=ws, reuse_states=True))
+    g_rc = L.bwd(*args, out, stats, x["dO"])
+    torch.cuda.synchronize()
+    for nm, a_, b_ in zip(NAMES, g_re, g_rc):
+        assert torch.equal(a_, b_), nm
