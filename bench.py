@@ -217,7 +217,7 @@ def main():
 
         def step():  # noqa: F811  (the full head instead of the core)
             L.head_fwd(*hargs, y=y, saved=saved, workspace=hws)
-            L.head_bwd(*hargs, saved, x["dO"], workspace=hws)
+            L.head_bwd(*hargs, saved, x["dO"], workspace=hws, reuse_states=True)
 
     for _ in range(args.warmup):
         step()

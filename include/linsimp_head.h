@@ -78,6 +78,18 @@ int linsimp_head_bwd(const linsimp_dims* dims, const linsimp_head_opts* opts, co
                      const void* dy, void* dq, void* dk, void* dv, void* dr, void* du, float* dtau,
                      void* dgate, void* workspace, size_t workspace_bytes, void* stream);
 
+/* linsimp_head_bwd with flags: 0, or LINSIMP_BWD_REUSE_STATES (linsimp.h) when
+ * `workspace` is the backward-sized head workspace (linsimp_head_workspace_size
+ * (dims, 1)) that the matching linsimp_head_fwd call used and nothing has
+ * written since: the core's boundary states are reused, results are bitwise
+ * those of linsimp_head_bwd. */
+int linsimp_head_bwd_ex(const linsimp_dims* dims, const linsimp_head_opts* opts, const void* q,
+                        const void* k, const void* v, const void* r, const void* u,
+                        const float* omega, const float* tau, const void* gate, const void* saved,
+                        const void* dy, void* dq, void* dk, void* dv, void* dr, void* du,
+                        float* dtau, void* dgate, int32_t flags, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

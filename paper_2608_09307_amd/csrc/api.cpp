@@ -458,6 +458,20 @@ int linsimp_head_bwd(const linsimp_dims* dims, const linsimp_head_opts* opts, co
                      const float* omega, const float* tau, const void* gate, const void* saved,
                      const void* dy, void* dq, void* dk, void* dv, void* dr, void* du, float* dtau,
                      void* dgate, void* workspace, size_t workspace_bytes_, void* stream) {
+  return linsimp_head_bwd_ex(dims, opts, q, k, v, r, u, omega, tau, gate, saved, dy, dq, dk, dv, dr, du,
+                             dtau, dgate, 0, workspace, workspace_bytes_, stream);
+}
+
+int linsimp_head_bwd_ex(const linsimp_dims* dims, const linsimp_head_opts* opts, const void* q,
+                        const void* k, const void* v, const void* r, const void* u,
+                        const float* omega, const float* tau, const void* gate, const void* saved,
+                        const void* dy, void* dq, void* dk, void* dv, void* dr, void* du,
+                        float* dtau, void* dgate, int32_t flags, void* workspace,
+                        size_t workspace_bytes_, void* stream) {
+  if (flags != 0 && flags != LINSIMP_BWD_REUSE_STATES) {
+    set_error("head bwd flags %d: only 0 or LINSIMP_BWD_REUSE_STATES", flags);
+    return LINSIMP_E_INVALID_ARG;
+  }
   Shape s;
   int rc = check_head(dims, opts, &s, true);
   if (rc) return rc;
@@ -483,7 +497,7 @@ int linsimp_head_bwd(const linsimp_dims* dims, const linsimp_head_opts* opts, co
   // core gradients with respect to q', k', r' land in dq, dk, dr and are
   // turned into gradients with respect to q, k, r in place
   if ((rc = launch_backward(s, hs.qn, hs.kn, v, hs.rn, u, omega, hs.ot, hs.stats, dot, dq, dk, dv, dr,
-                            du, ws, st)))
+                            du, ws, st, flags == LINSIMP_BWD_REUSE_STATES)))
     return rc;
   if ((rc = launch_head_prenorm_bwd(s, q, k, r, tau, dq, dk, dr, part_t, opts->norm_eps, st))) return rc;
   if ((rc = launch_head_reduce(s, part_t, dtau, st))) return rc;

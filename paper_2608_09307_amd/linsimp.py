@@ -47,7 +47,7 @@ EXPORTS = ("linsimp_workspace_size", "linsimp_fwd", "linsimp_bwd", "linsimp_bwd_
            "linsimp_decode_step", "linsimp_decode_chunk", "linsimp_timing_enable",
            "linsimp_timing_read", "linsimp_last_error", "linsimp_version")
 HEAD_EXPORTS = ("linsimp_head_saved_size", "linsimp_head_workspace_size", "linsimp_head_fwd",
-                "linsimp_head_bwd")
+                "linsimp_head_bwd", "linsimp_head_bwd_ex")
 BANK_EXPORTS = ("linsimp_feature_bank",)
 
 
@@ -97,6 +97,8 @@ def lib():
     L.linsimp_head_fwd.restype = ctypes.c_int
     L.linsimp_head_bwd.argtypes = [pd, po] + [vp] * 17 + [vp, sz, vp]
     L.linsimp_head_bwd.restype = ctypes.c_int
+    L.linsimp_head_bwd_ex.argtypes = [pd, po] + [vp] * 17 + [i32, vp, sz, vp]
+    L.linsimp_head_bwd_ex.restype = ctypes.c_int
     L.linsimp_feature_bank.argtypes = [i32, i32, i32, vp, vp, vp, i32, vp]
     L.linsimp_feature_bank.restype = ctypes.c_int
     _lib = L
@@ -317,9 +319,10 @@ def head_fwd(q, k, v, r, u, omega, w, tau, gate, eps=EPS, norm_eps=NORM_EPS, rms
 
 
 def head_bwd(q, k, v, r, u, omega, w, tau, gate, saved, dy, eps=EPS, norm_eps=NORM_EPS,
-             rms_eps=RMS_EPS, workspace=None):
+             rms_eps=RMS_EPS, workspace=None, reuse_states=False):
     """Backward of one full head; returns (dq, dk, dv, dr, du, dtau, dgate).
-    See linsimp_head_bwd."""
+    See linsimp_head_bwd; with ``reuse_states`` (linsimp_head_bwd_ex)
+    ``workspace`` must be the backward-sized one the matching head_fwd used."""
     d = dims_of(q, v, omega, w, eps)
     o = head_opts(_gate_kind(gate, v), norm_eps, rms_eps)
     L = lib()
@@ -327,16 +330,19 @@ def head_bwd(q, k, v, r, u, omega, w, tau, gate, saved, dy, eps=EPS, norm_eps=NO
     dtau = torch.empty_like(tau)
     dgate = torch.empty_like(gate)
     if workspace is None:
+        if reuse_states:
+            raise ValueError("reuse_states needs the workspace of the matching head_fwd call")
         nb = int(L.linsimp_head_workspace_size(ctypes.byref(d), 1))
         if nb == 0:
             _check(-2)
         workspace = _aligned_bytes(nb, q.device)
-    _check(L.linsimp_head_bwd(ctypes.byref(d), ctypes.byref(o), _ptr(q, "q"), _ptr(k, "k"),
-                              _ptr(v, "v"), _ptr(r, "r"), _ptr(u, "u"), _ptr(omega, "omega"),
-                              _ptr(tau, "tau"), _ptr(gate, "gate"), _ptr(saved, "saved"),
-                              _ptr(dy, "dy"), *[_ptr(g, "grad") for g in grads],
-                              _ptr(dtau, "dtau"), _ptr(dgate, "dgate"),
-                              _ptr(workspace, "workspace"), workspace.numel(), _stream()))
+    _check(L.linsimp_head_bwd_ex(ctypes.byref(d), ctypes.byref(o), _ptr(q, "q"), _ptr(k, "k"),
+                                 _ptr(v, "v"), _ptr(r, "r"), _ptr(u, "u"), _ptr(omega, "omega"),
+                                 _ptr(tau, "tau"), _ptr(gate, "gate"), _ptr(saved, "saved"),
+                                 _ptr(dy, "dy"), *[_ptr(g, "grad") for g in grads],
+                                 _ptr(dtau, "dtau"), _ptr(dgate, "dgate"),
+                                 BWD_REUSE_STATES if reuse_states else 0,
+                                 _ptr(workspace, "workspace"), workspace.numel(), _stream()))
     return (*grads, dtau, dgate)
 
 

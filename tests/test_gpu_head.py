@@ -138,3 +138,19 @@ def test_head_backward_is_bitwise_reproducible():
     torch.cuda.synchronize()
     for a, b in zip(g1, g2):
         assert torch.equal(a, b)
+
+
+def test_head_backward_reusing_forward_states_is_bitwise_equal():
+    import ctypes
+    wl = Workload("head_reuse", 1, 2, 300, 128, 128, 128, 64, "bf16", "fwdbwd", seed=65)
+    x = make_inputs(wl, device=DEV, with_grad=True)
+    p = make_head_params(wl, device=DEV, channel_gate=True)
+    args = (x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w, p["tau"], p["gate"])
+    d = L.dims_of(x["q"], x["v"], x["omega"], wl.w)
+    ws = L._aligned_bytes(int(L.lib().linsimp_head_workspace_size(ctypes.byref(d), 1)), DEV)
+    y, saved = L.head_fwd(*args, workspace=ws)
+    g_re = tuple(t.clone() for t in L.head_bwd(*args, saved, x["dO"], workspace=ws, reuse_states=True))
+    g_rc = L.head_bwd(*args, saved, x["dO"])
+    torch.cuda.synchronize()
+    for a_, b_ in zip(g_re, g_rc):
+        assert torch.equal(a_, b_)
