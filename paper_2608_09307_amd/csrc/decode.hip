@@ -99,6 +99,45 @@ LS_DEV void stage_omega(T* dst, const float* om, int tid) {
   }
 }
 
+// Log2 key features of one token, lambda_p = (omega_p . k - |k|^2 / 2) log2(e),
+// in float32 into lam[p] (LDS, p < M).  Feature p's dot product is split over
+// lanes l and l ^ 32 (the two halves of D), so the whole block takes part.
+// Returns max_p lambda_p; every thread calls it (it ends with a barrier).
+template <int D, int M>
+LS_DEV float key_log2_features(const float* sk, const float* om, float* lam, float* sred) {
+  const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = tid >> 6;
+  float nk = 0.0f;
+#pragma unroll
+  for (int e = l; e < D; e += 64) nk += sk[e] * sk[e];
+  nk = wave_sum(nk);
+  float mx = kNegInf;
+#pragma unroll
+  for (int p0 = 0; p0 < M; p0 += 128) {
+    const int p = p0 + wv * 32 + col;
+    float acc = 0.0f;
+    if (p < M) {
+      const float* orow = om + (size_t)p * D + h * (D / 2);
+      const float* kh = sk + h * (D / 2);
+#pragma unroll 8
+      for (int e = 0; e < D / 2; e += 4) {
+        const f32x4 o4 = *(const f32x4*)(orow + e);
+        const f32x4 k4 = *(const f32x4*)(kh + e);
+        acc += o4[0] * k4[0] + o4[1] * k4[1] + o4[2] * k4[2] + o4[3] * k4[3];
+      }
+    }
+    acc = half_swap_add(acc);
+    const float x = (acc - 0.5f * nk) * kLog2e;
+    if (p < M) {
+      mx = fmaxf(mx, x);
+      if (h == 0) lam[p] = x;
+    }
+  }
+  mx = wave_max(mx);
+  if (l == 0) sred[wv] = mx;
+  __syncthreads();
+  return fmaxf(fmaxf(sred[0], sred[1]), fmaxf(sred[2], sred[3]));
+}
+
 template <typename T, int D, int DV, int M, int NA>
 __global__ __launch_bounds__(256) void k_decode(DecArgs A) {
   using F = MF<T>;
@@ -137,6 +176,21 @@ __global__ __launch_bounds__(256) void k_decode(DecArgs A) {
   float* Ms = A.M + (size_t)sh * M * DV;
   float* as = A.a + (size_t)sh * M;
 
+  // The state rows this thread updates (feature tile pt = wv when each wave
+  // owns one tile) and its entry of a are fetched first: their latency then
+  // overlaps the staging, the key features and the logits.
+  constexpr bool PRE = PTW == 1;
+  float mreg[PRE ? DV / 32 : 1][16];
+  if constexpr (PRE) {
+    if (wv < PT) {
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt)
+#pragma unroll
+        for (int vv = 0; vv < 16; ++vv) mreg[dt][vv] = Ms[(size_t)(wv * 32 + crow(vv, h)) * DV + dt * 32 + col];
+    }
+  }
+  const float a_old = tid < M ? as[tid] : 0.0f;
+
   // ---- stage the token, the ring (slot t mod w replaced by the new token) and Omega ----
   for (int i = tid; i < D; i += 256) { sq[i] = tof(qt[i]); sk[i] = tof(kt[i]); }
   for (int i = tid; i < DV; i += 256) sv[i] = tof(vt[i]);
@@ -147,25 +201,14 @@ __global__ __launch_bounds__(256) void k_decode(DecArgs A) {
   __syncthreads();
 
   // ---- key features of k_t (float32 GEMV) and the frame update ----
-  float nk = 0.0f;
-  for (int e = 0; e < D; ++e) nk += sk[e] * sk[e];
-  float lam = kNegInf;
-  if (tid < M) {
-    const float* orow = om + (size_t)tid * D;
-    float acc = 0.0f;
-    for (int e = 0; e < D; ++e) acc += orow[e] * sk[e];
-    lam = (acc - 0.5f * nk) * kLog2e;
-  }
-  float mx = wave_max(lam);
-  if (l == 0) sred[wv] = mx;
-  __syncthreads();
-  const float rho_t = fmaxf(fmaxf(sred[0], sred[1]), fmaxf(sred[2], sred[3]));
+  const float rho_t = key_log2_features<D, M>(sk, om, schi, sred);
+  const float lam = tid < M ? schi[tid] : kNegInf;   // each thread rewrites only its own entry below
   const float Rn = fmaxf(Rold, rho_t);
   const float sa = fast_exp2(Rold - Rn);          // 0 for an empty state (R = -inf)
   if (tid < M) {
     float chi = fast_exp2(lam - Rn) * rsqrtf((float)M);
     schi[tid] = chi;
-    float an = sa * as[tid] + chi;
+    float an = sa * a_old + chi;
     san[tid] = an;
     as[tid] = an;
   }
@@ -245,7 +288,7 @@ __global__ __launch_bounds__(256) void k_decode(DecArgs A) {
         acc[pi][ct][v] = psi;
         zpart += psi * anp;
       }
-#pragma unroll 1
+#pragma unroll
     for (int dt = 0; dt < DV / 32; ++dt) {
       no_hoist();
       f32x16 accW = zero16();
@@ -263,7 +306,10 @@ __global__ __launch_bounds__(256) void k_decode(DecArgs A) {
       for (int vv = 0; vv < 16; ++vv) {
         const int p = pt * 32 + crow(vv, h);
         float* mp = Ms + (size_t)p * DV + d;
-        float mnew = sa * (*mp) + schi[p] * vd;
+        float mold;
+        if constexpr (PRE) mold = mreg[dt][vv];
+        else mold = *mp;
+        float mnew = sa * mold + schi[p] * vd;
         *mp = mnew;
         np += mnew * accW[vv];
       }
@@ -373,19 +419,8 @@ __global__ __launch_bounds__(256) void k_decode_chunk(DecArgs A, int NTOK) {
     __syncthreads();
 
     // key features of k_t and the frame update
-    float nk = 0.0f;
-    for (int e = 0; e < D; ++e) nk += sk[e] * sk[e];
-    float lam = kNegInf;
-    if (tid < M) {
-      const float* orow = om + (size_t)tid * D;
-      float acc = 0.0f;
-      for (int e = 0; e < D; ++e) acc += orow[e] * sk[e];
-      lam = (acc - 0.5f * nk) * kLog2e;
-    }
-    float mx = wave_max(lam);
-    if (l == 0) sred[wv] = mx;
-    __syncthreads();
-    const float rho_t = fmaxf(fmaxf(sred[0], sred[1]), fmaxf(sred[2], sred[3]));
+    const float rho_t = key_log2_features<D, M>(sk, om, schi, sred);
+    const float lam = tid < M ? schi[tid] : kNegInf;
     const float Rn = fmaxf(R, rho_t);
     const float sa = fast_exp2(R - Rn);
     if (tid < M) {
