@@ -189,19 +189,22 @@ __global__ __launch_bounds__(256) void k_state_scan(FwdArgs a) {
 // workgroup per (sequence, head); wave wv owns features 32 wv .. 32 wv + 31 and
 // walks the chunks in order, keeping its rows of M and a in registers in the
 // running key frame R (log2): per chunk, the key log2-features (bf16 hi/lo
-// Omega, two MFMAs per k-step), the chunk maximum shared across the waves,
+// Omega, two MFMAs per k-step: the hi half of the wave's tile in registers,
+// the lo half of all tiles in LDS, so that two workgroups fit on a CU with
+// two waves per SIMD), the chunk maximum shared across the waves,
 // the frame update (M, a scaled by 2^(R - R')), then M += chi^T V on the
 // matrix cores.  The chunk's k rows and V^T are staged in LDS one chunk ahead.
 // Nothing but the final state is written (the chunked forward materialises
 // every chunk's contribution instead).  bf16 inputs, m <= 128.
 // ---------------------------------------------------------------------------
 template <int D, int DV, int M>
-__global__ __launch_bounds__(256) void k_prefill_state(FwdArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_prefill_state(FwdArgs a) {
   using T = bf16;
   using F = MF<T>;
   constexpr int PAD = F::PAD, PT = M / 32;
   static_assert(PT <= 4, "one feature tile per wave");
   __shared__ __align__(16) T sK[2][32][D + PAD];
+  __shared__ __align__(16) T sOl[M][D + PAD];
   __shared__ __align__(16) T sVt[2][DV][32 + PAD];
   __shared__ float snk[4][32];
   __shared__ float smx[4];
@@ -212,15 +215,20 @@ __global__ __launch_bounds__(256) void k_prefill_state(FwdArgs a) {
   const T* ks = (const T*)a.k + seq * D;
   const T* vs = (const T*)a.v + seq * DV;
   const T* omk_h = (const T*)a.omk + (size_t)hh * 2 * M * D;
-  // this wave's Omega tile (hi, lo): B operands, lanes <-> feature p
-  typename F::frag oh[D / F::KS], ol[D / F::KS];
+  // hi half of this wave's Omega tile: B operands, lanes <-> feature p
+  typename F::frag oh[D / F::KS];
 #pragma unroll
   for (int s = 0; s < D / F::KS; ++s) {
     const int k0 = s * F::KS + h * F::KPL;
     const int pr = (owner ? wv : 0) * 32 + col;
     oh[s] = F::ld(omk_h + (size_t)pr * D, k0);
-    ol[s] = F::ld(omk_h + (size_t)M * D + (size_t)pr * D, k0);
   }
+  {
+    StageRows<T, M, D, 256> so;
+    so.load(omk_h + (size_t)M * D, D, 0, 0, M, tid);
+    so.store(&sOl[0][0], D + PAD, 0, 0, M, tid);
+  }
+  const T* olrow = &sOl[(owner ? wv : 0) * 32 + col][0];
   f32x16 Macc[DV / 32];
 #pragma unroll
   for (int dt = 0; dt < DV / 32; ++dt) Macc[dt] = zero16();
@@ -253,6 +261,10 @@ __global__ __launch_bounds__(256) void k_prefill_state(FwdArgs a) {
     f32x16 acc = zero16();
     float mx = kNegInf;
     if (owner) {
+      // two independent accumulation chains (hi, lo), summed at the end
+      f32x16 part[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) part[i] = zero16();
       float nkp = 0.0f;
       const T* krow = &sK[cur][col][0];
 #pragma unroll
@@ -260,9 +272,11 @@ __global__ __launch_bounds__(256) void k_prefill_state(FwdArgs a) {
         const typename F::frag kf = F::ld(krow, s * F::KS + h * F::KPL);
 #pragma unroll
         for (int e = 0; e < F::KPL; ++e) { const float x = fel(kf, e); nkp += x * x; }
-        acc = F::mma(kf, oh[s], acc);
-        acc = F::mma(kf, ol[s], acc);
+        part[0] = F::mma(kf, oh[s], part[0]);
+        part[1] = F::mma(kf, F::ld(olrow, s * F::KS + h * F::KPL), part[1]);
       }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[v] = part[0][v] + part[1][v];
       const float nk = half_swap_add(nkp);     // |k|^2 of token col
       if (h == 0) snk[wv][col] = nk;
       wave_lds_sync();
