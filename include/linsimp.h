@@ -23,6 +23,11 @@
  * shifts cancel in the ratio, and eps is added to Z after both shifts (so eps
  * only matters where the shifted Z underflows).  bf16 inputs are used as
  * matrix-core operands with float32 accumulation and float32 prefix states.
+ * For bf16 inputs the composite-query logits run on the f16 matrix cores:
+ * q, r (and u in the backward) are converted to f16 and z = q (*) r is
+ * formed in f16, so the entries of q, r, u and of q (*) r must stay below
+ * f16's largest value (65504) in magnitude; entries below 2^-14 keep fewer
+ * bits.  Normalised streams (Sec. 3.1) are far inside that range.
  *
  * Conventions for every entry point:
  *   - Tensor pointers are DEVICE pointers owned by the caller, 16-byte aligned,
