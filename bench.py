@@ -8,12 +8,17 @@ anchor-window readout) and backward (query sweeps, state sweep, reverse scan,
 key side) on the same batch; the backward reuses the boundary states the
 forward left in the shared workspace.
 
-    python bench.py [--steps K] [--warmup W] [--gpus 1] [--head]
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--head | --decode]
 
 With --head the step is the full head instead of the core: L2 normalisation
 and query temperature, core, gated RMSNorm (per-head gate), and the backward
 of all three; the line then also reports the streaming head kernels against
 the HBM peak (`head_streams`).
+
+With --decode the line is the autoregressive path instead (256 sequences x
+16 heads, d = m = 128, w = 64, after an 8192-token prefix): decode steps per
+second over all sequences, the decode kernel against the HBM peak, and the
+prefill and 16-token chunked decode times.
 
 Prints one JSON line.  `value` is tokens/s (B*n per step time).  `roofline`
 reports the dominant kernel (largest share of the timed region) against the
@@ -38,6 +43,7 @@ WORKLOAD = "layer16k_bf16"
 PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 matrix-core peak
 PEAK_HBM_GBS = 8000.0              # MI355X HBM3E peak
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_layer16k_bf16.json")
+DECODE_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_decode_s256_h16.json")
 
 
 def anchor_rows(n, w):
@@ -63,6 +69,85 @@ def kernel_flops(wl):
     }
 
 
+def decode_step_bytes(wl, es=2):
+    """Algorithmic HBM bytes of one decode step over all (sequence, head)
+    pairs: M and a read and written (float32) with the frame, both anchor
+    rings read and one slot of each written, the token's q, k, v, r, u in and
+    the output row out."""
+    D, Dv, m, w = wl.D, wl.Dv, wl.m, wl.w
+    per = (2 * 4 * m * Dv + 2 * 4 * m + 2 * 4 + w * (D + Dv) * es + (D + Dv) * es
+           + (3 * D + 2 * Dv) * es + Dv * es)
+    return wl.B * wl.H * per
+
+
+def run_decode(args, torch, L, dev):
+    """Decode-mode line: prefill once, then timed single decode steps and one
+    timed 16-token chunked call, all on the default stream."""
+    from paper_2608_09307_amd.workloads import WORKLOADS, make_decode_inputs
+    wl = WORKLOADS["decode_s256_h16"]
+    x = make_decode_inputs(wl, device=dev)
+    pre, tok = x["prefix"], x["token"]
+    st = L.prefill(pre["k"], pre["v"], pre["r"], pre["u"], x["omega"], wl.w)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+    ev[0].record(stream)
+    st = L.prefill(pre["k"], pre["v"], pre["r"], pre["u"], x["omega"], wl.w)
+    ev[1].record(stream)
+    for _ in range(args.warmup):
+        L.decode_step(st, tok["q"], tok["k"], tok["v"], tok["r"], tok["u"], x["omega"], wl.w)
+    torch.cuda.synchronize()
+    L.timing_enable(True)
+    L.timing_read()
+    ev[2].record(stream)
+    for _ in range(args.steps):
+        L.decode_step(st, tok["q"], tok["k"], tok["v"], tok["r"], tok["u"], x["omega"], wl.w)
+    ev[3].record(stream)
+    torch.cuda.synchronize()
+    kt = L.timing_read()
+    L.timing_enable(False)
+    T = 16
+    chunk = {nm: tok[nm][:, :, None, :].expand(wl.B, wl.H, T, tok[nm].shape[-1]).contiguous()
+             for nm in ("q", "k", "v", "r", "u")}
+    L.decode_chunk(st, *(chunk[nm] for nm in ("q", "k", "v", "r", "u")), x["omega"], wl.w)
+    torch.cuda.synchronize()
+    ev[4].record(stream)
+    L.decode_chunk(st, *(chunk[nm] for nm in ("q", "k", "v", "r", "u")), x["omega"], wl.w)
+    ev[5].record(stream)
+    torch.cuda.synchronize()
+    ms = ev[2].elapsed_time(ev[3]) / args.steps
+    chunk_ms = ev[4].elapsed_time(ev[5])
+    roofline = None
+    if "decode" in kt:
+        avg_ms = kt["decode"][0] / kt["decode"][1]
+        gbs = decode_step_bytes(wl) / (avg_ms * 1e-3) / 1e9
+        roofline = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic_for("decode", DECODE_TRAFFIC_FILE),
+                    "kernel": "decode",
+                    "avg_ms": round(avg_ms, 4), "bytes": decode_step_bytes(wl)}
+    line = {
+        "metric": "LinSimp decode tokens/s (256 sequences x 16 heads, 8192-token prefix)",
+        "value": round(wl.B / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1)*d^-1/4 prefix and tokens, N(0,1) feature bank)",
+        "config": {"workload": "decode_s256_h16", "S": wl.B, "H": wl.H, "prefix": wl.n_prefix,
+                   "d": wl.D, "m": wl.m, "w": wl.w},
+        "roofline": roofline,
+        "prefill_ms": round(ev[0].elapsed_time(ev[1]), 3),
+        "chunk16": {"ms_per_call": round(chunk_ms, 4), "us_per_token_step": round(chunk_ms * 1e3 / T, 2),
+                    "tokens_per_s": round(wl.B * T / (chunk_ms * 1e-3), 1)},
+    }
+    print(json.dumps(line), flush=True)
+
+
 def head_stream_bytes(wl, es=2):
     """Algorithmic HBM bytes per launch of the streaming head kernels (each
     row read and written once; per-row float32 scalars included)."""
@@ -79,7 +164,7 @@ def head_stream_bytes(wl, es=2):
 HEADERS = ["common.h", "keyfeat.h", "linsimp_internal.h", "prof.h"]
 KERNEL_FILES = {"fwd_readout": ["fwd.hip"] + HEADERS, "bwd_du": ["bwd.hip"] + HEADERS,
                 "bwd_dqdr": ["bwd.hip"] + HEADERS, "bwd_state": ["bwd.hip"] + HEADERS,
-                "bwd_keys": ["bwd.hip"] + HEADERS}
+                "bwd_keys": ["bwd.hip"] + HEADERS, "decode": ["decode.hip"] + HEADERS}
 
 
 def src_digest(files=None):
@@ -96,15 +181,15 @@ def src_digest(files=None):
 
 
 KERNEL_SYMBOLS = {"fwd_readout": "k_readout", "bwd_du": "k_bwd_du", "bwd_dqdr": "k_bwd_dqdr",
-                  "bwd_state": "k_bwd_state", "bwd_keys": "k_bwd_keys"}
+                  "bwd_state": "k_bwd_state", "bwd_keys": "k_bwd_keys", "decode": "k_decode"}
 
 
-def traffic_for(kernel):
+def traffic_for(kernel, path=TRAFFIC_FILE):
     """Calibrated HBM bytes (FETCH_SIZE + WRITE_SIZE) per launch of `kernel`
     from the committed counter runs, if they were taken on the kernel's
     current sources (its .hip file and the headers it includes); else None."""
     try:
-        with open(TRAFFIC_FILE) as fh:
+        with open(path) as fh:
             t = json.load(fh)
     except (OSError, ValueError):
         return None
@@ -176,6 +261,8 @@ def main():
                     help="only run a plain device copy of known size (for scaling HBM counters)")
     ap.add_argument("--head", action="store_true",
                     help="time the full head (normalisation, core, gated RMSNorm) instead of the core")
+    ap.add_argument("--decode", action="store_true",
+                    help="time prefill, decode steps and chunked decode (256 x 16 sequences)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
@@ -190,6 +277,9 @@ def main():
     torch.cuda.set_device(0)
     if args.copy_calibration:
         copy_calibration(torch, dev)
+        return
+    if args.decode:
+        run_decode(args, torch, L, dev)
         return
     wl = WORKLOADS[WORKLOAD]
     x = make_inputs(wl, device=dev, with_grad=True)
