@@ -136,7 +136,7 @@ using namespace linsimp;
 static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 // Validates dims; fills `s`.  Returns LINSIMP_OK or an error status.
-static int check_dims(const linsimp_dims* d, Shape* s, bool backward) {
+static int check_dims(const linsimp_dims* d, Shape* s, bool backward, bool bh_on_grid_y = true) {
   if (d == nullptr) { set_error("dims is NULL"); return LINSIMP_E_INVALID_ARG; }
   if (d->B < 1 || d->H < 1 || d->n < 1 || d->D < 1 || d->Dv < 1 || d->m < 1 || d->w < 1) {
     set_error("dims must be positive (B=%lld H=%lld n=%lld D=%d Dv=%d m=%d w=%d)",
@@ -148,8 +148,11 @@ static int check_dims(const linsimp_dims* d, Shape* s, bool backward) {
     return LINSIMP_E_INVALID_ARG;
   }
   if (!(d->eps >= 0.0f)) { set_error("eps must be >= 0"); return LINSIMP_E_INVALID_ARG; }
-  if (d->n > (int64_t)1 << 30 || d->B * d->H > (int64_t)1 << 30) {
-    set_error("sequence or batch too large");
+  // (batch, head) pairs index the grid's y dimension (not in decode); rows bound the 1-D grids
+  if (d->n > (int64_t)1 << 30 || (bh_on_grid_y && d->B * d->H > 65535) ||
+      d->B * d->H * d->n > (int64_t)1 << 31) {
+    set_error("sizes too large: B*H=%lld (at most 65535), B*H*n=%lld (at most 2^31)",
+              (long long)(d->B * d->H), (long long)(d->B * d->H * d->n));
     return LINSIMP_E_UNSUPPORTED;
   }
   s->B = d->B; s->H = d->H; s->n = d->n; s->D = d->D; s->Dv = d->Dv; s->m = d->m; s->w = d->w;
@@ -268,7 +271,7 @@ int linsimp_decode_step(int64_t S, int32_t H, int32_t D, int32_t Dv, int32_t m, 
   linsimp_dims d;
   d.B = S; d.H = H; d.n = 1; d.D = D; d.Dv = Dv; d.m = m; d.w = w; d.dtype = dtype; d.eps = eps;
   Shape s;
-  int rc = check_dims(&d, &s, false);
+  int rc = check_dims(&d, &s, false, false);
   if (rc) return rc;
   const void* ps[] = {q, k, v, r, u, omega, M, a, rho, ring_r, ring_u, pos, out};
   if ((rc = check_ptrs("q,k,v,r,u,omega,M,a,rho,ring_r,ring_u,pos,out", ps, 13))) return rc;
@@ -288,7 +291,7 @@ int linsimp_decode_chunk(int64_t S, int32_t H, int32_t T, int32_t D, int32_t Dv,
   linsimp_dims d;
   d.B = S; d.H = H; d.n = T; d.D = D; d.Dv = Dv; d.m = m; d.w = w; d.dtype = dtype; d.eps = eps;
   Shape s;
-  int rc = check_dims(&d, &s, false);
+  int rc = check_dims(&d, &s, false, false);
   if (rc) return rc;
   const void* ps[] = {q, k, v, r, u, omega, M, a, rho, ring_r, ring_u, pos, out};
   if ((rc = check_ptrs("q,k,v,r,u,omega,M,a,rho,ring_r,ring_u,pos,out", ps, 13))) return rc;

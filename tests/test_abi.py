@@ -61,7 +61,9 @@ def test_workspace_size_and_unsupported_shapes():
                 L.make_dims(1, 1, 256, 32, 32, 32, 65, L.BF16),     # w > 64
                 L.make_dims(1, 1, 256, 128, 128, 128, 64, L.F32),   # f32 only up to 64
                 L.make_dims(1, 1, 0, 32, 32, 32, 64, L.BF16),       # n = 0
-                L.make_dims(1, 1, 8, 32, 32, 32, 64, 7)):           # bad dtype
+                L.make_dims(1, 1, 8, 32, 32, 32, 64, 7),            # bad dtype
+                L.make_dims(256, 256, 64, 32, 32, 32, 64, L.BF16),  # B*H above the grid's y limit
+                L.make_dims(1, 3, 1 << 30, 32, 32, 32, 64, L.BF16)):  # B*H*n above 2^31
         assert L.workspace_size(bad, False) == 0
         assert L.lib().linsimp_last_error()
 
