@@ -564,6 +564,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       if (t + NW < 32) load_g(t + NW);
       const int i = s0 + t;
       if (i >= n || i < c0 || i - c0 > w + 30) continue;
+      __builtin_amdgcn_iglp_opt(0);             // interleave the matrix-core and LDS streams
       const float Li = uniform(a.stats[(seq + i) * 2]);
       const float inv = uniform(a.rowstat[(seq + i) * 2]);
       const float dZ = uniform(a.rowstat[(seq + i) * 2 + 1]);
