@@ -61,7 +61,7 @@ def test_backward_f32_structure(D, m, n, w, B, H):
 
 
 @pytest.mark.parametrize("D,m,n,w", [(128, 128, 700, 64), (64, 64, 513, 64), (128, 64, 300, 40),
-                                     (128, 256, 400, 64), (32, 32, 200, 64)])
+                                     (128, 256, 400, 64), (32, 32, 200, 64), (64, 128, 257, 48)])
 def test_backward_bf16_shapes(D, m, n, w):
     _run(Workload("bf16_bwd", 1, 2, n, D, D, m, w, "bf16", "fwdbwd", seed=32,
                   boost_frac=0.05 if m == 256 else 0.0, boost=4.0))

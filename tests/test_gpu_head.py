@@ -106,6 +106,7 @@ def _run(wl: Workload, channel: bool, zero_rows: bool = False, pairs=None):
     (128, 128, 300, 64, 1, 2, "bf16"),
     (64, 64, 257, 48, 2, 2, "bf16"),
     (32, 32, 130, 64, 1, 1, "bf16"),
+    (128, 256, 150, 64, 1, 2, "bf16"),   # two feature blocks
 ])
 def test_head_parity(D, m, n, w, B, H, dt, channel):
     _run(Workload("head", B, H, n, D, D, m, w, dt, "fwdbwd", seed=61), channel)
