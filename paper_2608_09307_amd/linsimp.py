@@ -132,6 +132,42 @@ def _stream():
     return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
+def _expect(pairs, device=None):
+    """Check (tensor, name, shape, dtype) tuples before their pointers go to
+    the C ABI, which sees bare pointers and trusts the sizes it is given: a
+    tensor of the wrong shape would be read or written out of bounds.  Shape
+    and dtype are checked first, then that every tensor is on the first one's
+    device and that this is the current device (the launch stream's)."""
+    for t, name, shape, dtype in pairs:
+        if t is None:
+            raise ValueError(f"{name} is required")
+        if tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+        if t.dtype != dtype:
+            raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    dev = device if device is not None else pairs[0][0].device
+    for t, name, _, _ in pairs:
+        if t.device != dev:
+            raise ValueError(f"{name} is on {t.device}, expected {dev}")
+    if dev.type == "cuda" and dev.index is not None and dev.index != torch.cuda.current_device():
+        raise ValueError(f"tensors are on {dev} but the current device is cuda:{torch.cuda.current_device()}")
+
+
+def _layer_shapes(q, v, omega):
+    if q.dim() != 4 or v.dim() != 4 or omega.dim() != 3:
+        raise ValueError("q, v must be [B, H, n, D|Dv] and omega [H, m, D]")
+    B, H, n, D = q.shape
+    return B, H, n, D, v.shape[-1], omega.shape[1]
+
+
+def _layer_inputs(q, k, v, r, u, omega):
+    B, H, n, D, Dv, m = _layer_shapes(q, v, omega)
+    dt = q.dtype
+    return [(q, "q", (B, H, n, D), dt), (k, "k", (B, H, n, D), dt), (v, "v", (B, H, n, Dv), dt),
+            (r, "r", (B, H, n, D), dt), (u, "u", (B, H, n, Dv), dt),
+            (omega, "omega", (H, m, D), torch.float32)]
+
+
 def make_dims(B, H, n, D, Dv, m, w, dtype, eps=EPS) -> Dims:
     return Dims(B, H, n, D, Dv, m, w, dtype, eps)
 
@@ -157,11 +193,16 @@ def alloc_workspace(d: Dims, backward: bool, device) -> torch.Tensor:
 def fwd(q, k, v, r, u, omega, w, eps=EPS, out=None, stats=None, workspace=None,
         want_stats=True):
     """Forward pass; returns (out, stats).  See linsimp_fwd."""
+    chk = _layer_inputs(q, k, v, r, u, omega)
     d = dims_of(q, v, omega, w, eps)
     if out is None:
         out = torch.empty(q.shape[:3] + (v.shape[-1],), dtype=q.dtype, device=q.device)
     if stats is None and want_stats:
         stats = torch.empty(q.shape[:3] + (2,), dtype=torch.float32, device=q.device)
+    chk.append((out, "out", q.shape[:3] + (v.shape[-1],), q.dtype))
+    if stats is not None:
+        chk.append((stats, "stats", q.shape[:3] + (2,), torch.float32))
+    _expect(chk)
     if workspace is None:
         workspace = alloc_workspace(d, False, q.device)
     _check(lib().linsimp_fwd(ctypes.byref(d), _ptr(q, "q"), _ptr(k, "k"), _ptr(v, "v"),
@@ -176,10 +217,16 @@ def bwd(q, k, v, r, u, omega, w, out, stats, dout, eps=EPS, grads=None, workspac
     """Backward pass; returns (dq, dk, dv, dr, du).  See linsimp_bwd; with
     ``reuse_states`` (linsimp_bwd_ex, LINSIMP_BWD_REUSE_STATES) ``workspace``
     must be the backward-sized workspace the matching fwd call used."""
+    chk = _layer_inputs(q, k, v, r, u, omega)
     d = dims_of(q, v, omega, w, eps)
     if grads is None:
         grads = tuple(torch.empty_like(x) for x in (q, k, v, r, u))
     dq, dk, dv, dr, du = grads
+    ov = q.shape[:3] + (v.shape[-1],)
+    chk += [(out, "out", ov, q.dtype), (stats, "stats", q.shape[:3] + (2,), torch.float32),
+            (dout, "dout", ov, q.dtype)]
+    chk += [(g, "d" + nm, x.shape, x.dtype) for g, nm, x in zip(grads, "qkvru", (q, k, v, r, u))]
+    _expect(chk)
     if workspace is None:
         if reuse_states:
             raise ValueError("reuse_states needs the workspace of the matching forward call")
@@ -213,9 +260,10 @@ def timing_read(max_kernels: int = 64):
 def prefill(k, v, r, u, omega, w, eps=EPS, workspace=None):
     """Decode state after a prefix (k, v, r, u: [S, H, n, *]).  Returns a dict
     with M [S,H,m,Dv], a [S,H,m], rho [S,H] (log2 frame), ring_r, ring_u, pos."""
-    S, H, n, D = k.shape
-    Dv = v.shape[-1]
-    m = omega.shape[1]
+    S, H, n, D, Dv, m = _layer_shapes(k, v, omega)
+    _expect([(k, "k", (S, H, n, D), k.dtype), (v, "v", (S, H, n, Dv), k.dtype),
+             (r, "r", (S, H, n, D), k.dtype), (u, "u", (S, H, n, Dv), k.dtype),
+             (omega, "omega", (H, m, D), torch.float32)])
     d = make_dims(S, H, n, D, Dv, m, w, _dtype_code(k), eps)
     dev = k.device
     st = {"M": torch.empty(S, H, m, Dv, dtype=torch.float32, device=dev),
@@ -235,14 +283,28 @@ def prefill(k, v, r, u, omega, w, eps=EPS, workspace=None):
     return st
 
 
+def _decode_checks(state, q, k, v, r, u, omega, w, out, tok):
+    """Shapes of a decode call: tok is () for one token, (T,) for a chunk."""
+    if q.dim() != 3 + len(tok) or omega.dim() != 3:
+        raise ValueError("q must be [S, H, *tok, D] and omega [H, m, D]")
+    S, H, D = q.shape[0], q.shape[1], q.shape[-1]
+    Dv, m, dt = v.shape[-1], omega.shape[1], q.dtype
+    f32 = torch.float32
+    _expect([(q, "q", (S, H, *tok, D), dt), (k, "k", (S, H, *tok, D), dt), (v, "v", (S, H, *tok, Dv), dt),
+             (r, "r", (S, H, *tok, D), dt), (u, "u", (S, H, *tok, Dv), dt),
+             (omega, "omega", (H, m, D), f32), (state["M"], "M", (S, H, m, Dv), f32),
+             (state["a"], "a", (S, H, m), f32), (state["rho"], "rho", (S, H), f32),
+             (state["ring_r"], "ring_r", (S, H, w, D), dt), (state["ring_u"], "ring_u", (S, H, w, Dv), dt),
+             (state["pos"], "pos", (S,), torch.int64), (out, "out", (S, H, *tok, Dv), dt)])
+    return S, H, D, Dv, m
+
+
 def decode_step(state, q, k, v, r, u, omega, w, eps=EPS, out=None):
     """One decode step for S sequences (q, k, v, r, u: [S, H, *]); updates
     ``state`` in place and returns out [S, H, Dv]."""
-    S, H, D = q.shape
-    Dv = v.shape[-1]
-    m = omega.shape[1]
     if out is None:
-        out = torch.empty(S, H, Dv, dtype=q.dtype, device=q.device)
+        out = torch.empty(q.shape[:2] + (v.shape[-1],), dtype=q.dtype, device=q.device)
+    S, H, D, Dv, m = _decode_checks(state, q, k, v, r, u, omega, w, out, ())
     _check(lib().linsimp_decode_step(S, H, D, Dv, m, w, _dtype_code(q), eps, _ptr(q, "q"),
                                      _ptr(k, "k"), _ptr(v, "v"), _ptr(r, "r"), _ptr(u, "u"),
                                      _ptr(omega, "omega"), _ptr(state["M"], "M"),
@@ -253,15 +315,13 @@ def decode_step(state, q, k, v, r, u, omega, w, eps=EPS, out=None):
     return out
 
 
-
 def decode_chunk(state, q, k, v, r, u, omega, w, eps=EPS, out=None):
     """T consecutive decode steps for S sequences (q, k, v, r, u: [S, H, T, *]);
     updates ``state`` in place and returns out [S, H, T, Dv]."""
-    S, H, T, D = q.shape
-    Dv = v.shape[-1]
-    m = omega.shape[1]
     if out is None:
-        out = torch.empty(S, H, T, Dv, dtype=q.dtype, device=q.device)
+        out = torch.empty(q.shape[:3] + (v.shape[-1],), dtype=q.dtype, device=q.device)
+    T = q.shape[2]
+    S, H, D, Dv, m = _decode_checks(state, q, k, v, r, u, omega, w, out, (T,))
     _check(lib().linsimp_decode_chunk(S, H, T, D, Dv, m, w, _dtype_code(q), eps, _ptr(q, "q"),
                                       _ptr(k, "k"), _ptr(v, "v"), _ptr(r, "r"), _ptr(u, "u"),
                                       _ptr(omega, "omega"), _ptr(state["M"], "M"),
@@ -290,6 +350,12 @@ def _gate_kind(gate: torch.Tensor, v: torch.Tensor) -> int:
     return GATE_CHANNEL if gate.dim() == 4 else GATE_HEAD
 
 
+def _head_params(q, v, tau, gate):
+    H = q.shape[1]
+    gshape, gdt = ((q.shape[:3] + (v.shape[-1],), q.dtype) if gate.dim() == 4 else ((H,), torch.float32))
+    return [(tau, "tau", (H,), torch.float32), (gate, "gate", gshape, gdt)]
+
+
 def head_fwd(q, k, v, r, u, omega, w, tau, gate, eps=EPS, norm_eps=NORM_EPS, rms_eps=RMS_EPS,
              y=None, saved=None, workspace=None):
     """Forward of one full head; returns (y, saved).  ``gate`` is gamma [H]
@@ -300,6 +366,8 @@ def head_fwd(q, k, v, r, u, omega, w, tau, gate, eps=EPS, norm_eps=NORM_EPS, rms
     L = lib()
     if y is None:
         y = torch.empty(q.shape[:3] + (v.shape[-1],), dtype=q.dtype, device=q.device)
+    _expect(_layer_inputs(q, k, v, r, u, omega) + _head_params(q, v, tau, gate)
+            + [(y, "y", q.shape[:3] + (v.shape[-1],), q.dtype)])
     if saved is None:
         nb = int(L.linsimp_head_saved_size(ctypes.byref(d)))
         if nb == 0:
@@ -326,6 +394,8 @@ def head_bwd(q, k, v, r, u, omega, w, tau, gate, saved, dy, eps=EPS, norm_eps=NO
     d = dims_of(q, v, omega, w, eps)
     o = head_opts(_gate_kind(gate, v), norm_eps, rms_eps)
     L = lib()
+    _expect(_layer_inputs(q, k, v, r, u, omega) + _head_params(q, v, tau, gate)
+            + [(dy, "dy", q.shape[:3] + (v.shape[-1],), q.dtype)])
     grads = [torch.empty_like(x) for x in (q, k, v, r, u)]
     dtau = torch.empty_like(tau)
     dgate = torch.empty_like(gate)

@@ -114,3 +114,29 @@ def test_feature_bank_argument_errors():
     assert lib.linsimp_feature_bank(1, 64, 64, *ok, 2, vp(0)) == -1
     assert lib.linsimp_feature_bank(1, 64, 64, vp(0), ok[1], ok[2], 1, vp(0)) == -1
     assert lib.linsimp_feature_bank(70000, 64, 64, *ok, 1, vp(0)) == -2
+
+
+def test_binding_checks_shapes_and_dtypes_before_the_call():
+    """The C ABI takes bare pointers; the binding refuses tensors whose shape
+    or dtype disagrees with the others before any pointer is passed."""
+    import torch
+    B, H, n, D = 1, 2, 8, 32
+    x = {nm: torch.zeros(B, H, n, D) for nm in ("q", "k", "v", "r", "u")}
+    om = torch.zeros(H, 32, D)
+    bad_k = torch.zeros(B, H, n - 1, D)
+    with pytest.raises(ValueError, match="k has shape"):
+        L.fwd(x["q"], bad_k, x["v"], x["r"], x["u"], om, 8)
+    with pytest.raises(TypeError, match="omega has dtype"):
+        L.fwd(x["q"], x["k"], x["v"], x["r"], x["u"], om.double(), 8)
+    with pytest.raises(ValueError, match="dout has shape"):
+        L.bwd(*(x[nm] for nm in ("q", "k", "v", "r", "u")), om, 8, x["v"], torch.zeros(B, H, n, 2),
+              torch.zeros(B, H, n, D + 1))
+    st = {"M": torch.zeros(B, H, 32, D), "a": torch.zeros(B, H, 32), "rho": torch.zeros(B, H),
+          "ring_r": torch.zeros(B, H, 8, D), "ring_u": torch.zeros(B, H, 7, D),
+          "pos": torch.zeros(B, dtype=torch.int64)}
+    tok = {nm: torch.zeros(B, H, D) for nm in ("q", "k", "v", "r", "u")}
+    with pytest.raises(ValueError, match="ring_u has shape"):
+        L.decode_step(st, *(tok[nm] for nm in ("q", "k", "v", "r", "u")), om, 8)
+    with pytest.raises(ValueError, match="gate has shape"):
+        L.head_fwd(*(x[nm] for nm in ("q", "k", "v", "r", "u")), om, 8, torch.zeros(H),
+                   torch.zeros(H + 1))
