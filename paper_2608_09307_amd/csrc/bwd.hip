@@ -82,20 +82,26 @@ template <typename T, int N> constexpr int tr_pad() {
 // ---------------------------------------------------------------------------
 // prep: row scalars and zeroed float32 accumulators
 // ---------------------------------------------------------------------------
+// One row per LPR lanes, each lane one 16-byte piece of dO and of out.
 template <typename T, int DV>
 __global__ __launch_bounds__(256) void k_bwd_rowprep(BwdArgs a) {
+  constexpr int VE = 16 / sizeof(T);
+  constexpr int LPR = DV / VE;                 // lanes per row (a power of two, <= 32)
+  typedef T V __attribute__((ext_vector_type(VE)));
   const size_t rows = (size_t)a.BH * a.n;
-  const size_t row = (size_t)blockIdx.x * 8 + (threadIdx.x >> 5);
-  const int lane = threadIdx.x & 31;
-  if (row >= rows) return;
-  const T* g = (const T*)a.dout + row * DV;
-  const T* o = (const T*)a.out + row * DV;
+  const size_t row = (size_t)blockIdx.x * (256 / LPR) + threadIdx.x / LPR;
+  const int lane = threadIdx.x % LPR;
+  const bool act = row < rows;
+  const size_t rr = act ? row : rows - 1;
+  const V g = *(const V*)((const T*)a.dout + rr * DV + lane * VE);
+  const V o = *(const V*)((const T*)a.out + rr * DV + lane * VE);
   float s = 0.0f;
-  for (int d = lane; d < DV; d += 32) s += tof(g[d]) * tof(o[d]);
 #pragma unroll
-  for (int off = 16; off >= 1; off >>= 1) s += __shfl_xor(s, off, 32);
-  const float inv = 1.0f / (a.stats[row * 2 + 1] + a.eps);
-  if (lane == 0) {
+  for (int e = 0; e < VE; ++e) s += tof(g[e]) * tof(o[e]);
+#pragma unroll
+  for (int off = LPR / 2; off >= 1; off >>= 1) s += __shfl_xor(s, off, LPR);
+  if (act && lane == 0) {
+    const float inv = 1.0f / (a.stats[row * 2 + 1] + a.eps);
     a.rowstat[row * 2 + 0] = inv;
     a.rowstat[row * 2 + 1] = -s * inv;
   }
@@ -147,12 +153,11 @@ __global__ __launch_bounds__(256) void k_bwd_keyfeat(BwdArgs a) {
   for (int pt = 0; pt < M / 32; ++pt)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      T x4[4];
+      typedef T V4 __attribute__((ext_vector_type(4)));
+      V4 x4;
 #pragma unroll
       for (int e = 0; e < 4; ++e) x4[e] = (T)(fast_exp2(acc[pt][4 * g + e] - R) * rsm);
-      T* dst = row + F::sigma(pt * 32 + 8 * g + 4 * h);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) dst[e] = x4[e];
+      *(V4*)(row + F::sigma(pt * 32 + 8 * g + 4 * h)) = x4;   // sigma keeps 4-groups contiguous
     }
 }
 
@@ -721,19 +726,24 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
 template <typename T>
 __global__ __launch_bounds__(256) void k_bwd_final_dq(const float* __restrict__ src, T* __restrict__ dst,
                                                       int BH, int n, int D, int nfb, int NS, int w) {
+  // four consecutive elements of one row per thread (D is a multiple of 4)
   const size_t count = (size_t)BH * n * D;
-  const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const size_t idx = ((size_t)blockIdx.x * 256 + threadIdx.x) * 4;
   if (idx >= count) return;
   const int i = (int)((idx / D) % n);
   const int bi = i >> 5;
-  float acc = 0.0f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   for (int fb = 0; fb < nfb; ++fb)
     for (int s = 0; s < NS; ++s) {
       const int k = bi - s;
       if (k < 0 || i - 32 * k > w + 30) continue;
-      acc += src[((size_t)fb * NS + s) * count + idx];
+      acc += *(const f32x4*)(src + ((size_t)fb * NS + s) * count + idx);
     }
-  dst[idx] = (T)acc;
+  typedef T V4 __attribute__((ext_vector_type(4)));
+  V4 y;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) y[e] = (T)acc[e];
+  *(V4*)(dst + idx) = y;
 }
 
 // ---------------------------------------------------------------------------
@@ -1311,7 +1321,8 @@ static int run_bwd(const Shape& s, BwdArgs a, hipStream_t st) {
   const size_t rows = (size_t)BH * s.n;
   {
     ProfScope ps("bwd_prep", st);
-    k_bwd_rowprep<T, DV><<<(unsigned)((rows + 7) / 8), 256, 0, st>>>(a);
+    constexpr int RPB = 256 / (DV / (16 / (int)sizeof(T)));     // rows per block of k_bwd_rowprep
+    k_bwd_rowprep<T, DV><<<(unsigned)((rows + RPB - 1) / RPB), 256, 0, st>>>(a);
     k_bwd_keyfeat<T, D, M><<<dim3((nch + 3) / 4, BH), 256, 0, st>>>(a);
   }
   if (int rc = launch_err("prep")) return rc;
@@ -1340,7 +1351,8 @@ static int run_bwd(const Shape& s, BwdArgs a, hipStream_t st) {
     k_bwd_final<T><<<(unsigned)((rows * DV + 255) / 256), 256, 0, st>>>(a.du32, (T*)a.du, rows * DV, NFB);
     k_bwd_final<T><<<(unsigned)((rows * D + 255) / 256), 256, 0, st>>>(a.dr32, (T*)a.dr, rows * D, NFB);
   }
-  k_bwd_final_dq<T><<<(unsigned)((rows * D + 255) / 256), 256, 0, st>>>(a.dq32, (T*)a.dq, BH, (int)s.n, D, NFB, NS, s.w);
+  k_bwd_final_dq<T><<<(unsigned)((rows * D / 4 + 255) / 256), 256, 0, st>>>(a.dq32, (T*)a.dq, BH, (int)s.n, D, NFB, NS,
+                                                                            s.w);
   return launch_err("final");
 }
 
