@@ -13,6 +13,7 @@
 #include "linsimp_internal.h"
 #include "prof.h"
 
+#include <atomic>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -86,9 +87,10 @@ void carve(const Shape& s, void* base, bool backward, Workspace* ws) {
 struct TimedLaunch {
   std::string name;
   hipEvent_t ev0, ev1;
+  bool open;        // begin recorded, end not yet
 };
 static std::mutex g_tmu;
-static bool g_timing = false;
+static std::atomic<bool> g_timing{false};
 static std::vector<TimedLaunch> g_launches;
 static std::vector<hipEvent_t> g_free;
 
@@ -112,13 +114,20 @@ void timing_mark(const char* name, hipStream_t st, bool begin) {
     t.name = name;
     t.ev0 = take_event();
     t.ev1 = take_event();
-    if (t.ev0 == nullptr || t.ev1 == nullptr) return;
+    if (t.ev0 == nullptr || t.ev1 == nullptr) {     // not timed; keep what was obtained
+      if (t.ev0 != nullptr) g_free.push_back(t.ev0);
+      if (t.ev1 != nullptr) g_free.push_back(t.ev1);
+      return;
+    }
+    t.open = true;
     hipEventRecord(t.ev0, st);
     g_launches.push_back(t);
   } else {
+    // the most recent open launch of this name (scopes of one name never nest)
     for (auto it = g_launches.rbegin(); it != g_launches.rend(); ++it)
-      if (it->name == name) {
+      if (it->open && it->name == name) {
         hipEventRecord(it->ev1, st);
+        it->open = false;
         break;
       }
   }
@@ -316,6 +325,7 @@ int linsimp_timing_read(char* names, int names_len, float* total_ms, int* counts
   std::vector<int> cnt;
   int rc = LINSIMP_OK;
   for (auto& t : g_launches) {
+    if (t.open) continue;                             // its end was never marked
     if (hipEventSynchronize(t.ev1) != hipSuccess) { rc = LINSIMP_E_HIP; continue; }
     float ms = 0.0f;
     if (hipEventElapsedTime(&ms, t.ev0, t.ev1) != hipSuccess) { rc = LINSIMP_E_HIP; continue; }
@@ -329,7 +339,9 @@ int linsimp_timing_read(char* names, int names_len, float* total_ms, int* counts
   g_launches.clear();
   std::string all;
   int nk = 0;
+  // only whole names that fit the caller's buffer (with its terminating NUL)
   for (size_t k = 0; k < keys.size() && nk < max_kernels; ++k, ++nk) {
+    if (all.size() + keys[k].size() + 1 >= (size_t)names_len) break;
     all += keys[k];
     all += '\n';
     total_ms[nk] = (float)tot[k];
