@@ -140,3 +140,23 @@ def test_binding_checks_shapes_and_dtypes_before_the_call():
     with pytest.raises(ValueError, match="gate has shape"):
         L.head_fwd(*(x[nm] for nm in ("q", "k", "v", "r", "u")), om, 8, torch.zeros(H),
                    torch.zeros(H + 1))
+
+
+def test_plain_c_client_links_and_runs(tmp_path):
+    """The headers and the library are usable from C with no Python or torch:
+    a C client is compiled with gcc against include/, linked with
+    liblinsimp.so and run (calls that need no GPU)."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not available")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    libdir = os.path.dirname(L.lib_path())
+    exe = str(tmp_path / "abi_smoke")
+    subprocess.run([gcc, "-std=c99", "-Wall", "-Werror", "-I", os.path.join(root, "include"),
+                    os.path.join(root, "tests", "c", "abi_smoke.c"), "-L", libdir, "-llinsimp",
+                    "-Wl,-rpath," + libdir, "-o", exe], check=True)
+    res = subprocess.run([exe], capture_output=True, text=True, timeout=60)
+    assert res.returncode == 0, res.stdout + res.stderr
+    assert "0 failure(s)" in res.stdout
