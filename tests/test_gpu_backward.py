@@ -115,3 +115,10 @@ def test_backward_reusing_forward_states_is_bitwise_equal(D, m, n, w, dt):
     torch.cuda.synchronize()
     for nm, a_, b_ in zip(NAMES, g_re, g_rc):
         assert torch.equal(a_, b_), nm
+
+
+@pytest.mark.parametrize("w,n", [(1, 70), (33, 97)])
+def test_backward_two_feature_blocks_short_windows(w, n):
+    """m = 256 (float32 du/dr partials per feature block, then summed) with
+    one anchor tile per row (w <= 32), w = 1 included."""
+    _run(Workload("m256_short_w", 1, 2, n, 128, 128, 256, w, "bf16", "fwdbwd", seed=36))

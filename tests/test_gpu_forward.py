@@ -111,3 +111,10 @@ def test_first_key_underflow_is_handled():
     ref = O.forward_logspace(f64(x["q"][0, 0]), f64(x["k"][0, 0]), f64(x["v"][0, 0]),
                              f64(x["r"][0, 0]), f64(x["u"][0, 0]), f64(x["omega"][0]), wl.w)[0]
     assert rel_l2(f64(out[0, 0]), ref) < 2e-2
+
+
+@pytest.mark.parametrize("w,n", [(1, 70), (33, 97)])
+def test_forward_two_feature_blocks_short_windows(w, n):
+    """m = 256 (feature-block partials merged by the online maximum) with one
+    anchor tile per row, w = 1 included."""
+    _run_and_compare(Workload("m256_short_w_fwd", 1, 2, n, 128, 128, 256, w, "bf16", "fwd", seed=37))
