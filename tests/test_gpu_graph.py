@@ -1,4 +1,4 @@
-"""HIP graph capture of the library's calls.
+"""HIP graph capture of the library's calls, and calls on concurrent streams.
 
 Every entry point only enqueues kernels on the caller's stream (no
 allocation, copy, memset or synchronisation), so a forward + backward step
@@ -84,3 +84,31 @@ def test_decode_step_graph_replays_match_eager():
         assert torch.equal(out_g, out_e), rep
         for k in st_g:
             assert torch.equal(st_g[k], st_e[k]), (rep, k)
+
+
+def test_calls_on_two_streams_match_sequential_calls():
+    """The library keeps no device state between calls: two forward +
+    backward steps with their own workspaces, enqueued on two streams at
+    once, give the bits of the same steps run one after the other."""
+    wls = [Workload("streams", 1, 2, 257, 128, 128, 128, 64, "bf16", "fwdbwd", seed=73 + s) for s in range(2)]
+    xs = [make_inputs(wl, device=DEV, with_grad=True) for wl in wls]
+
+    def step(x, wl, ws):
+        args = (x["q"], x["k"], x["v"], x["r"], x["u"], x["omega"], wl.w)
+        out, stats = L.fwd(*args, workspace=ws)
+        return (out, stats) + tuple(L.bwd(*args, out, stats, x["dO"], workspace=ws, reuse_states=True))
+
+    wss = [L.alloc_workspace(L.dims_of(x["q"], x["v"], x["omega"], wl.w), True, DEV) for x, wl in zip(xs, wls)]
+    ref = [tuple(t.clone() for t in step(x, wl, ws)) for x, wl, ws in zip(xs, wls, wss)]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in range(2)]
+    got = [None, None]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    for k in range(2):
+        with torch.cuda.stream(streams[k]):
+            got[k] = step(xs[k], wls[k], wss[k])
+    torch.cuda.synchronize()
+    for k in range(2):
+        for i, (a, b) in enumerate(zip(got[k], ref[k])):
+            assert torch.equal(a, b), (k, i)
