@@ -8,12 +8,16 @@ anchor-window readout) and backward (query sweeps, state sweep, reverse scan,
 key side) on the same batch; the backward reuses the boundary states the
 forward left in the shared workspace.
 
-    python bench.py [--steps K] [--warmup W] [--gpus 1] [--head | --decode]
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--head | --decode] [--workload NAME]
 
 With --head the step is the full head instead of the core: L2 normalisation
 and query temperature, core, gated RMSNorm (per-head gate), and the backward
 of all three; the line then also reports the streaming head kernels against
 the HBM peak (`head_streams`).
+
+--workload runs the same step on another forward + backward workload of
+paper_2608_09307_amd/workloads.py (the 64k stress shape, or the 2k-token layer
+the paper times); the default line is the 16k layer.
 
 With --decode the line is the autoregressive path instead (256 sequences x
 16 heads, d = m = 128, w = 64, after an 8192-token prefix): decode steps per
@@ -263,6 +267,9 @@ def main():
                     help="time the full head (normalisation, core, gated RMSNorm) instead of the core")
     ap.add_argument("--decode", action="store_true",
                     help="time prefill, decode steps and chunked decode (256 x 16 sequences)")
+    ap.add_argument("--workload", default=WORKLOAD,
+                    help="forward + backward workload of the step (default: the 16k layer); "
+                         "e.g. stress64k_m256 or layer2k_h6_d64_m128")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported "
@@ -281,7 +288,10 @@ def main():
     if args.decode:
         run_decode(args, torch, L, dev)
         return
-    wl = WORKLOADS[WORKLOAD]
+    if args.workload not in WORKLOADS or WORKLOADS[args.workload].mode != "fwdbwd":
+        print(f"--workload must be a forward + backward workload, not {args.workload}", file=sys.stderr)
+        sys.exit(2)
+    wl = WORKLOADS[args.workload]
     x = make_inputs(wl, device=dev, with_grad=True)
     d = L.dims_of(x["q"], x["v"], x["omega"], wl.w)
     ws_b = L.alloc_workspace(d, True, dev)
@@ -342,7 +352,8 @@ def main():
             achieved = kf[dominant] / avg_s / 1e12
             roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
                         "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                        "traffic": traffic_for(dominant), "kernel": dominant,
+                        "traffic": traffic_for(dominant) if args.workload == WORKLOAD else None,
+                        "kernel": dominant,
                         "avg_ms": round(tot / cnt, 4)}
     head_streams = None
     if args.head:
@@ -356,7 +367,8 @@ def main():
                                    "bytes": b, "avg_ms": round(kt[k][0] / kt[k][1], 4)}
     line = {
         "metric": ("LinSimp head fwd+bwd tokens/s at n=16k" if args.head else
-                   "LinSimp fwd+bwd tokens/s at n=16k; % of MI355X bf16 MFMA peak"),
+                   "LinSimp fwd+bwd tokens/s at n=16k; % of MI355X bf16 MFMA peak" if args.workload == WORKLOAD else
+                   f"LinSimp fwd+bwd tokens/s ({args.workload})"),
         "value": round(tokens / (ms * 1e-3), 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -368,7 +380,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1)*d^-1/4 streams, N(0,1) feature bank and dO)",
-        "config": {"workload": WORKLOAD + ("_head" if args.head else ""), "B": wl.B, "H": wl.H,
+        "config": {"workload": args.workload + ("_head" if args.head else ""), "B": wl.B, "H": wl.H,
                    "n": wl.n, "d": wl.D, "m": wl.m, "w": wl.w},
         "mfma_frac_step": round(step_tflops / PEAK_BF16_TFLOPS, 4),
         "algorithmic_tflops_step": round(step_tflops, 2),

@@ -63,6 +63,8 @@ WORKLOADS = {
                                 "decode", n_prefix=8192),
     "stress64k_m256": Workload("stress64k_m256", 1, 32, 65536, 128, 128, 256, 64, "bf16",
                                "fwdbwd", boost_frac=0.05, boost=4.0),
+    # the layer the paper times (8 sequences x 6 heads of 2048 tokens, d = 64, m = 128)
+    "layer2k_h6_d64_m128": Workload("layer2k_h6_d64_m128", 8, 6, 2048, 64, 64, 128, 64, "bf16", "fwdbwd"),
 }
 
 
