@@ -172,15 +172,19 @@ KERNEL_FILES = {"fwd_readout": ["fwd.hip"] + HEADERS, "bwd_du": ["bwd.hip"] + HE
 
 
 def src_digest(files=None):
-    """sha256 prefix of the named kernel sources (all of csrc/ by default)."""
+    """sha256 prefix of the named kernel sources (all of csrc/ by default) and
+    of the build script that holds their compiler flags."""
     h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2608_09307_amd", "csrc")
+    pkg = os.path.join(ROOT, "paper_2608_09307_amd")
+    csrc = os.path.join(pkg, "csrc")
     names = sorted(files) if files else sorted(os.listdir(csrc))
     for name in names:
         if name.endswith((".hip", ".h", ".cpp")):
             with open(os.path.join(csrc, name), "rb") as fh:
                 h.update(name.encode())
                 h.update(fh.read())
+    with open(os.path.join(pkg, "build.py"), "rb") as fh:
+        h.update(fh.read())
     return h.hexdigest()[:16]
 
 
