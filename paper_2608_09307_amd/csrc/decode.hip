@@ -26,14 +26,14 @@ struct DecArgs {
   int H; int w; float eps;
 };
 
-template <typename T, int D, int DV, int M, int NA>
+template <typename T, int D, int DV, int M, int NA, bool OM_LDS = true>
 struct DCfg {
   static constexpr int PAD = MF<T>::PAD;
   static constexpr int W = 32 * NA;
   static constexpr int ES = sizeof(T);
   static constexpr int a16(int x) { return (x + 15) & ~15; }
-  static constexpr int oOm = 0;
-  static constexpr int oRr = oOm + a16(M * (D + PAD) * ES);
+  static constexpr int oOm = 0;                         // Omega * log2 e (when staged in LDS)
+  static constexpr int oRr = oOm + (OM_LDS ? a16(M * (D + PAD) * ES) : 0);
   static constexpr int oUt = oRr + a16(W * (D + PAD) * ES);
   static constexpr int oQ = oUt + a16(DV * (W + PAD) * ES);
   static constexpr int oK = oQ + a16(D * 4);
@@ -101,10 +101,16 @@ LS_DEV void stage_omega(T* dst, const float* om, int tid) {
 
 // Log2 key features of one token, lambda_p = (omega_p . k - |k|^2 / 2) log2(e),
 // in float32 into lam[p] (LDS, p < M).  Feature p's dot product is split over
-// lanes l and l ^ 32 (the two halves of D), so the whole block takes part.
-// Returns max_p lambda_p; every thread calls it (it ends with a barrier).
-template <int D, int M>
-LS_DEV float key_log2_features(const float* sk, const float* om, float* lam, float* sred) {
+// lanes l and l ^ 32, which take the alternate KPL-wide pieces of D that make
+// up an MFMA operand fragment of row p; with FRAGS (M <= 128) the fragments
+// of Omega * log2(e) in the operand type are kept in omf[D / KS] for the
+// query logits, so the bank is read once.  Returns max_p lambda_p; every
+// thread calls it (it ends with a barrier).
+template <typename T, int D, int M, bool FRAGS>
+LS_DEV float key_log2_features(const float* sk, const float* om, float* lam, float* sred,
+                               typename MF<T>::frag* omf) {
+  using F = MF<T>;
+  static_assert(!FRAGS || M <= 128, "fragments for one feature tile per wave");
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = tid >> 6;
   float nk = 0.0f;
 #pragma unroll
@@ -114,20 +120,38 @@ LS_DEV float key_log2_features(const float* sk, const float* om, float* lam, flo
 #pragma unroll
   for (int p0 = 0; p0 < M; p0 += 128) {
     const int p = p0 + wv * 32 + col;
+    const bool act = p < M;
+    const float* orow = om + (size_t)(act ? p : 0) * D;
     float acc = 0.0f;
-    if (p < M) {
-      const float* orow = om + (size_t)p * D + h * (D / 2);
-      const float* kh = sk + h * (D / 2);
-#pragma unroll 8
-      for (int e = 0; e < D / 2; e += 4) {
-        const f32x4 o4 = *(const f32x4*)(orow + e);
-        const f32x4 k4 = *(const f32x4*)(kh + e);
-        acc += o4[0] * k4[0] + o4[1] * k4[1] + o4[2] * k4[2] + o4[3] * k4[3];
+#pragma unroll
+    for (int ks = 0; ks < D / F::KS; ++ks) {
+      const int k0 = ks * F::KS + h * F::KPL;
+      float o[F::KPL];
+      if constexpr (F::KPL % 4 == 0) {
+#pragma unroll
+        for (int e4 = 0; e4 < F::KPL; e4 += 4) {
+          const f32x4 x = *(const f32x4*)(orow + k0 + e4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[e4 + e] = x[e];
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < F::KPL; ++e) o[e] = orow[k0 + e];
+      }
+#pragma unroll
+      for (int e = 0; e < F::KPL; ++e) acc += o[e] * sk[k0 + e];
+      if constexpr (FRAGS) {
+        if constexpr (sizeof(T) == 2) {
+#pragma unroll
+          for (int e = 0; e < F::KPL; ++e) omf[ks][e] = (T)(o[e] * kLog2e);
+        } else {
+          omf[ks] = o[0] * kLog2e;
+        }
       }
     }
     acc = half_swap_add(acc);
     const float x = (acc - 0.5f * nk) * kLog2e;
-    if (p < M) {
+    if (act) {
       mx = fmaxf(mx, x);
       if (h == 0) lam[p] = x;
     }
@@ -139,12 +163,12 @@ LS_DEV float key_log2_features(const float* sk, const float* om, float* lam, flo
 }
 
 template <typename T, int D, int DV, int M, int NA>
-__global__ __launch_bounds__(256) void k_decode(DecArgs A) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_decode(DecArgs A) {
   using F = MF<T>;
-  using C = DCfg<T, D, DV, M, NA>;
-  constexpr int PAD = C::PAD, W = C::W;
   constexpr int PT = M / 32;                  // feature tiles
   constexpr int PTW = (PT + 3) / 4;           // feature tiles per wave
+  using C = DCfg<T, D, DV, M, NA, PTW != 1>;
+  constexpr int PAD = C::PAD, W = C::W;
   static_assert(C::BYTES <= 160 * 1024, "decode LDS budget");
   __shared__ __align__(16) char smem[C::BYTES];
   T* sOm = (T*)(smem + C::oOm);
@@ -196,12 +220,15 @@ __global__ __launch_bounds__(256) void k_decode(DecArgs A) {
   for (int i = tid; i < DV; i += 256) sv[i] = tof(vt[i]);
   stage_ring<T, W, D, false>(sRr, D + PAD, rr, rt, slot, w, tid);
   stage_ring<T, W, DV, true>(sUt, W + PAD, ru, ut, slot, w, tid);
-  stage_omega<T, D, M>(sOm, om, tid);
+  if constexpr (!PRE) stage_omega<T, D, M>(sOm, om, tid);
   const float Rold = A.rho[sh];
   __syncthreads();
 
-  // ---- key features of k_t (float32 GEMV) and the frame update ----
-  const float rho_t = key_log2_features<D, M>(sk, om, schi, sred);
+  // ---- key features of k_t (float32 GEMV) and the frame update; with one
+  // feature tile per wave the GEMV's loads of the wave's Omega rows also
+  // give the logits' operand fragments (no LDS copy of the bank) ----
+  typename F::frag omf[PRE ? D / F::KS : 1];
+  const float rho_t = key_log2_features<T, D, M, PRE>(sk, om, schi, sred, omf);
   const float lam = tid < M ? schi[tid] : kNegInf;   // each thread rewrites only its own entry below
   const float Rn = fmaxf(Rold, rho_t);
   const float sa = fast_exp2(Rold - Rn);          // 0 for an empty state (R = -inf)
@@ -225,7 +252,7 @@ __global__ __launch_bounds__(256) void k_decode(DecArgs A) {
   for (int ct = 0; ct < NA; ++ct) {
     const int c = ct * 32 + col;
     const bool valid = c < nvalid;
-#pragma unroll 2
+#pragma unroll
     for (int ks = 0; ks < D / F::KS; ++ks) {
       const int k0 = ks * F::KS + h * F::KPL;
       typename F::frag rf = F::ld(sRr + c * (D + PAD), k0), zf;
@@ -241,11 +268,15 @@ __global__ __launch_bounds__(256) void k_decode(DecArgs A) {
         nz[ct] += p * p;
         zf = p;
       }
+      if constexpr (PRE) {
+        if (wv < PT) acc[0][ct] = F::mma(zf, omf[ks], acc[0][ct]);
+      } else {
 #pragma unroll
-      for (int pi = 0; pi < PTW; ++pi) {
-        const int pt = wv + 4 * pi;
-        if (pt < PT)
-          acc[pi][ct] = F::mma(zf, F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), acc[pi][ct]);
+        for (int pi = 0; pi < PTW; ++pi) {
+          const int pt = wv + 4 * pi;
+          if (pt < PT)
+            acc[pi][ct] = F::mma(zf, F::ld(sOm + (pt * 32 + col) * (D + PAD), k0), acc[pi][ct]);
+        }
       }
     }
     nz[ct] = half_swap_add(nz[ct]);
@@ -419,7 +450,7 @@ __global__ __launch_bounds__(256) void k_decode_chunk(DecArgs A, int NTOK) {
     __syncthreads();
 
     // key features of k_t and the frame update
-    const float rho_t = key_log2_features<D, M>(sk, om, schi, sred);
+    const float rho_t = key_log2_features<T, D, M, false>(sk, om, schi, sred, nullptr);
     const float lam = tid < M ? schi[tid] : kNegInf;
     const float Rn = fmaxf(R, rho_t);
     const float sa = fast_exp2(R - Rn);
