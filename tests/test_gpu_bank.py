@@ -53,3 +53,38 @@ def test_feature_bank_structure_at_layer_size():
     eye = torch.eye(D, dtype=torch.float64, device=DEV)
     gram = dirs @ dirs.transpose(-1, -2)
     assert float((gram - eye).abs().max()) < 2e-6
+
+
+def test_sampler_diagnostic_trend_on_device_banks():
+    """App. B.1's diagnostic on banks drawn by the device sampler (D = 32,
+    m = 1024 .. 262,144, the paper's range): with the sign fix the relative
+    error of the kernel estimate phi(x)^T phi(y) against exp(x^T y) falls like
+    m^{-1/2}; without it the error stops falling at a bias floor.  The
+    estimate is evaluated in float64 on the host (oracle.montecarlo); the
+    paper's absolute values (its metric and D are not stated) are not used."""
+    from oracle import montecarlo
+    D = 32
+    prng = np.random.default_rng(71)
+    pairs = []
+    for _ in range(16):
+        x, y = prng.standard_normal(D), prng.standard_normal(D)
+        pairs.append((0.5 * x / np.linalg.norm(x), 0.5 * y / np.linalg.norm(y)))
+    ms = [1024, 16384, 262144]
+
+    def err(m, fix):
+        out = []
+        for s in range(3):
+            gauss, radii = make_bank_draws(1, m, D, seed=300 + 7 * s + m % 97, device=DEV)
+            om = L.feature_bank(gauss, radii, m, fix)[0].double().cpu().numpy()
+            e = [montecarlo.kernel_estimate(x, y, om) / montecarlo.exact_kernel(x, y) - 1.0 for x, y in pairs]
+            out.append(float(np.sqrt(np.mean(np.square(e)))))
+        return float(np.mean(out))
+
+    fixed = [err(m, True) for m in ms]
+    raw = [err(m, False) for m in ms]
+    print(f"[bank diag] fixed={fixed} raw={raw}", flush=True)
+    slope = np.polyfit(np.log(ms), np.log(fixed), 1)[0]
+    assert -0.65 < slope < -0.35, (slope, fixed)
+    last_raw = np.log(raw[1] / raw[2]) / np.log(ms[2] / ms[1])    # 0 on a floor, 0.5 for m^{-1/2}
+    assert last_raw < 0.2, raw
+    assert raw[-1] > 3 * fixed[-1], (raw, fixed)
