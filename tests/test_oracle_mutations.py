@@ -150,3 +150,54 @@ def test_backward_slips_are_caught_by_finite_differences():
     assert _fd_failures(swapped)
     halved_du = lambda *a: (lambda g: (*g[:4], 0.5 * g[4]))(O.backward(*a))          # noqa: E731
     assert _fd_failures(halved_du)
+
+
+# ---- the full head (oracle.layer) ----
+
+def _head_reference_failures(head_forward):
+    """Compare a head forward against torch's library normalisations around an
+    independent pair-form core (the pin of tests/test_oracle_layer.py)."""
+    import torch
+    from test_oracle_layer import _inputs as head_inputs, _torch_head
+    from oracle import layer as LY
+    n, D, Dv, m, w = 9, 4, 3, 6, 4
+    q, k, v, r, u, Om = head_inputs(42, n, D, Dv, m, scale=2.0)
+    tau, gamma = 2.0, -2.0
+    ref = _torch_head(*(torch.tensor(x) for x in (q, k, v, r, u)), torch.tensor(Om), w,
+                      torch.tensor(tau, dtype=torch.float64), torch.tensor(gamma, dtype=torch.float64),
+                      LY.RMS_EPS).numpy()
+    y, _ = head_forward(q, k, v, r, u, Om, w, tau, gamma)
+    return not np.allclose(y, ref, rtol=1e-10, atol=1e-12)
+
+
+HEAD_MUTANTS = {
+    "temperature on the key instead of the query": "tau_on_k",
+    "RMSNorm over mean |x| instead of mean x^2": "rms_abs",
+    "gate sigmoid(-gamma)": "gate_sign",
+    "r left unnormalised": "no_r_norm",
+}
+
+
+def _mutant_head(kind):
+    from oracle import layer as LY
+
+    def head_forward(q, k, v, r, u, Omega, w, tau, gate, **kw):
+        qh, _ = LY.l2_normalize(q)
+        kh, _ = LY.l2_normalize(k)
+        rh = np.asarray(r, float) if kind == "no_r_norm" else LY.l2_normalize(r)[0]
+        qs, ks = (qh, tau * kh) if kind == "tau_on_k" else (tau * qh, kh)
+        ot = O.forward_recurrent(qs, ks, v, rh, u, Omega, w)
+        if kind == "rms_abs":
+            oh = ot / np.sqrt(np.mean(np.abs(ot), axis=-1, keepdims=True) + LY.RMS_EPS)
+        else:
+            oh, _ = LY.rmsnorm(ot)
+        g = LY.gate_values(-gate if kind == "gate_sign" else gate, *ot.shape)
+        return g * oh, ot
+    return head_forward
+
+
+def test_head_reference_accepts_the_oracle_and_catches_planted_slips():
+    from oracle import layer as LY
+    assert not _head_reference_failures(LY.head_forward)
+    for name, kind in HEAD_MUTANTS.items():
+        assert _head_reference_failures(_mutant_head(kind)), name
