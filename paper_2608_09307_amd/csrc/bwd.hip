@@ -937,22 +937,42 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
   for (int dt = 0; dt < DV / 32; ++dt) Fm[dt] = zero16();
   float fpart = 0.0f;                          // f[p = col], partial over this half's anchors
 
+  // the rows' q, dout, v and statistics are fetched one row ahead
+  constexpr int QE = (D + 63) / 64;
+  T qn[QE], gn[DV / 32], vn[DV / 32];
+  float invn, dZn;
+  auto fetch = [&](int t) {
+    const size_t i = (size_t)(s0 + t);
+#pragma unroll
+    for (int e = 0; e < QE; ++e) qn[e] = (e * 64 + l < D) ? qs[i * D + e * 64 + l] : (T)0.0f;
+#pragma unroll
+    for (int dt = 0; dt < DV / 32; ++dt) {
+      gn[dt] = gs[i * DV + dt * 32 + col];
+      vn[dt] = vs[i * DV + dt * 32 + col];
+    }
+    invn = a.rowstat[(seq + i) * 2];
+    dZn = a.rowstat[(seq + i) * 2 + 1];
+  };
+  fetch(tlast);
 #pragma unroll 1
   for (int t = tlast; t >= 0; --t) {
-    const int i = s0 + t;
-    const float inv = uniform(a.rowstat[(seq + i) * 2]);
-    const float dZ = uniform(a.rowstat[(seq + i) * 2 + 1]);
+    const float inv = uniform(invn);
+    const float dZ = uniform(dZn);
     const float fr = uniform(t < tlast ? fast_exp2(sRj[t] - sRj[t + 1]) : 1.0f);
-    for (int e = l; e < D; e += 64) {
-      if constexpr (sizeof(T) == 2) ((f16*)sQ)[e] = (f16)(float)qs[(size_t)i * D + e];
-      else sQ[e] = qs[(size_t)i * D + e];
-    }
+#pragma unroll
+    for (int e = 0; e < QE; ++e)
+      if (e * 64 + l < D) {
+        if constexpr (sizeof(T) == 2) ((f16*)sQ)[e * 64 + l] = (f16)(float)qn[e];
+        else sQ[e * 64 + l] = qn[e];
+      }
     float dN[DV / 32], vv[DV / 32];
 #pragma unroll
     for (int dt = 0; dt < DV / 32; ++dt) {
-      dN[dt] = tof(gs[(size_t)i * DV + dt * 32 + col]) * inv;
-      vv[dt] = tof(vs[(size_t)i * DV + dt * 32 + col]);
+      dN[dt] = tof(gn[dt]) * inv;
+      vv[dt] = tof(vn[dt]);
     }
+    if (t > 0) fetch(t - 1);
+    const int i = s0 + t;
     wave_lds_sync();
     // logits L[c, p] of the row's anchor tiles (regs <-> anchor c = i - 32an - crow)
     f32x16 acc[NA];
