@@ -111,10 +111,10 @@ int linsimp_bwd(const linsimp_dims* dims, const void* q, const void* k, const vo
 enum {
   /* The workspace is the one the matching linsimp_fwd call used (sized for
    * the backward, linsimp_workspace_size(dims, 1)), with the same dims and
-   * inputs, and nothing has written it since: its feature-bank copies and
-   * boundary states are reused instead of recomputed (the backward otherwise
-   * re-runs the forward's state pass).  Results are bitwise those of
-   * linsimp_bwd. */
+   * inputs, and nothing has written it since: its feature-bank copies,
+   * boundary states and key features are reused instead of recomputed (the
+   * backward otherwise re-runs the forward's state and key-feature passes).
+   * Results are bitwise those of linsimp_bwd. */
   LINSIMP_BWD_REUSE_STATES = 1
 };
 

@@ -40,6 +40,8 @@ size_t workspace_bytes(const Shape& s, bool backward) {
   t += al(BH * nch * S * 4);                   // states
   t += al(BH * nch * 4);                       // rho
   t += al(BH * (nch + 1) * 4);                 // rex
+  t += al(BH * (size_t)s.n * s.m * s.esize()); // chi
+  t += al(BH * (size_t)s.n * 4);               // rj
   if (s.m > 128) t += al((size_t)(s.m / 128) * BH * s.n * (s.Dv + 2) * 4);   // part
   if (backward) {
     const size_t n = (size_t)s.n, nfb = (size_t)bwd_nfb(s.m), ns = (size_t)bwd_slots(s.w);
@@ -50,8 +52,6 @@ size_t workspace_bytes(const Shape& s, bool backward) {
     t += al(nfp * BH * n * s.Dv * 4);          // du32
     t += al(nfp * BH * n * s.D * 4);           // dr32
     t += al(nfb * ns * BH * n * s.D * 4);      // dq32
-    t += al(BH * n * s.m * s.esize());         // chi
-    t += al(BH * n * 4);                       // rj
     t += al(BH * n * 2 * 4);                   // rowstat
   }
   return t;
@@ -67,6 +67,8 @@ void carve(const Shape& s, void* base, bool backward, Workspace* ws) {
   ws->states = (float*)p; p += al(BH * nch * S * 4);
   ws->rho = (float*)p; p += al(BH * nch * 4);
   ws->rex = (float*)p; p += al(BH * (nch + 1) * 4);
+  ws->chi = p; p += al(BH * (size_t)s.n * s.m * s.esize());
+  ws->rj = (float*)p; p += al(BH * (size_t)s.n * 4);
   if (s.m > 128) { ws->part = (float*)p; p += al((size_t)(s.m / 128) * BH * s.n * (s.Dv + 2) * 4); }
   if (backward) {
     const size_t n = (size_t)s.n, nfb = (size_t)bwd_nfb(s.m), ns = (size_t)bwd_slots(s.w);
@@ -77,8 +79,6 @@ void carve(const Shape& s, void* base, bool backward, Workspace* ws) {
     ws->du32 = nfp ? (float*)p : nullptr; p += al(nfp * BH * n * s.Dv * 4);
     ws->dr32 = nfp ? (float*)p : nullptr; p += al(nfp * BH * n * s.D * 4);
     ws->dq32 = (float*)p; p += al(nfb * ns * BH * n * s.D * 4);
-    ws->chi = p; p += al(BH * n * s.m * s.esize());
-    ws->rj = (float*)p; p += al(BH * n * 4);
     ws->rowstat = (float*)p; p += al(BH * n * 2 * 4);
   }
 }

@@ -19,7 +19,6 @@
 //
 // Kernels:
 //   k_bwd_rowprep  row scalars 1/(Z+eps) and dZ
-//   k_bwd_keyfeat  key features chi_j and frames R_j of every token
 //   k_bwd_du       anchor sweep 1: du
 //   k_bwd_dqdr     anchor sweep 2: dr (anchor side) and per-tile partials of dq
 //   k_bwd_state    state sweep: GB_b, gb_b and the intra-chunk dchi, dv
@@ -32,7 +31,6 @@
 #include <type_traits>
 
 #include "common.h"
-#include "keyfeat.h"
 #include "linsimp_internal.h"
 #include "prof.h"
 
@@ -107,59 +105,6 @@ __global__ __launch_bounds__(256) void k_bwd_rowprep(BwdArgs a) {
   }
 }
 
-
-// ---------------------------------------------------------------------------
-// Key features of every token in the running frame (one wave per chunk):
-//   R_j = max(Rex_b, max_{s0 <= j' <= j} max_p lambda_j'p),  chi_j = 2^(lambda_j - R_j)/sqrt(m)
-// stored with p permuted inside 16-blocks (the LDS layout of the sweeps).
-// ---------------------------------------------------------------------------
-template <typename T, int D, int M>
-__global__ __launch_bounds__(256) void k_bwd_keyfeat(BwdArgs a) {
-  using F = MF<T>;
-  const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
-  const int bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch;
-  const int cb = blockIdx.x * 4 + wv;
-  if (cb >= nch) return;
-  const int s0 = cb * 32;
-  const size_t seq = (size_t)bh * n;
-  const T* ks = (const T*)a.k + seq * D;
-  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
-  f32x16 acc[M / 32];
-  float nk;
-  key_logits<T, D, M, true>(acc, nk, ks, s0, n, omk_h);
-  const bool vt = s0 + col < n;
-  float mx = kNegInf;
-#pragma unroll
-  for (int pt = 0; pt < M / 32; ++pt)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      float x = vt ? acc[pt][v] - 0.5f * kLog2e * nk : kNegInf;
-      acc[pt][v] = x;
-      mx = fmaxf(mx, x);
-    }
-  mx = half_swap_max(mx);
-  float R = mx;
-#pragma unroll
-  for (int o = 1; o < 32; o <<= 1) {
-    float t = __shfl_up(R, o, 32);
-    if (col >= o) R = fmaxf(R, t);
-  }
-  R = fmaxf(R, a.rex[(size_t)bh * (nch + 1) + cb]);
-  if (!vt) return;
-  if (h == 0) a.rj[seq + s0 + col] = R;
-  const float rsm = rsqrtf((float)M);
-  T* row = (T*)a.chi + (seq + s0 + col) * M;
-#pragma unroll
-  for (int pt = 0; pt < M / 32; ++pt)
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      typedef T V4 __attribute__((ext_vector_type(4)));
-      V4 x4;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) x4[e] = (T)(fast_exp2(acc[pt][4 * g + e] - R) * rsm);
-      *(V4*)(row + F::sigma(pt * 32 + 8 * g + 4 * h)) = x4;   // sigma keeps 4-groups contiguous
-    }
-}
 
 // ---------------------------------------------------------------------------
 // Anchor-stationary sweeps.  A workgroup owns the 32 anchors [c0, c0 + 32) of
@@ -841,13 +786,11 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
   const int tlast = min(31, n - 1 - s0);
   const size_t seq = (size_t)bh * n;
   const T* qs = (const T*)a.q + seq * D;
-  const T* ks = (const T*)a.k + seq * D;
   const T* vs = (const T*)a.v + seq * DV;
   const T* rs_ = (const T*)a.r + seq * D;
   const T* us = (const T*)a.u + seq * DV;
   const T* gs = (const T*)a.dout + seq * DV;
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
-  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
   const float Rexb = a.rex[(size_t)bh * (nch + 1) + cb];
   const int w = a.w;
   const int pw = fb * FB + wv * 32;            // first feature of this wave's tile
@@ -856,20 +799,25 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
     // every global load of the window first, then the LDS stores
     StageRows<T, 32 * C::NT32, D, NT> sr;
     StageRows<T, WIN, DV, NT> su;
+    StageRows<T, 32, FB, NT> sc;
     sr.load(rs_, D, wb, 0, n, tid);
     su.load(us, DV, wb, 0, n, tid);
+    sc.load((const T*)a.chi + seq * M + fb * FB, M, s0, 0, n, tid);   // key features of the chunk
     const float lv = (tid < 32) ? a.stats[(seq + min(s0 + tid, n - 1)) * 2] : 0.0f;
+    const float rjv = (tid < 32) ? a.rj[seq + min(s0 + tid, n - 1)] : 0.0f;
     if constexpr (sizeof(T) == 2) sr.store((f16*)sR, D + PAD, wb, 0, n, tid);
     else sr.store(sR, D + PAD, wb, 0, n, tid);
     su.store(sU, DV + C::TP, wb, 0, n, tid);
-    if (tid < 32) sL[tid] = (s0 + tid < n) ? lv : 0.0f;
+    sc.store(sChi, FB + PAD, s0, 0, n, tid);
+    if (tid < 32) {
+      sL[tid] = (s0 + tid < n) ? lv : 0.0f;
+      sRj[tid] = (s0 + tid < n) ? rjv : 0.0f;
+    }
   }
   __syncthreads();
-  // wave 0: chunk key features and frames; the others: the |z|^2 table
-  if (wv == 0)
-    chunk_key_features<T, D, M>(ks, s0, n, omk_h, Rexb, sChi, FB + PAD, sRj, fb * FB, fb * FB + FB);
-  if (NW == 1 || wv > 0) {
-    for (int kt = (NW == 1 ? 0 : wv - 1); kt < C::NT32; kt += (NW == 1 ? 1 : NW - 1)) {
+  // the |z|^2 table
+  {
+    for (int kt = wv; kt < C::NT32; kt += NW) {
       // C[t][wi] = sum_D q_{s0+t}[D]^2 r_{wb+wi}[D]^2   (regs <-> t, lanes <-> window row)
       f32x16 acc = zero16();
       const bool vi = s0 + col < n;
@@ -1343,7 +1291,6 @@ static int run_bwd(const Shape& s, BwdArgs a, hipStream_t st) {
     ProfScope ps("bwd_prep", st);
     constexpr int RPB = 256 / (DV / (16 / (int)sizeof(T)));     // rows per block of k_bwd_rowprep
     k_bwd_rowprep<T, DV><<<(unsigned)((rows + RPB - 1) / RPB), 256, 0, st>>>(a);
-    k_bwd_keyfeat<T, D, M><<<dim3((nch + 3) / 4, BH), 256, 0, st>>>(a);
   }
   if (int rc = launch_err("prep")) return rc;
   { ProfScope ps("bwd_du", st);

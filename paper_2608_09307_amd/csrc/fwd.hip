@@ -32,6 +32,8 @@ struct FwdArgs {
   float* states; float* rho; float* rex;
   float* final_M; float* final_a; float* final_rex;   // optional state after the last token
   float* part;                                        // [NFB][BH][n][Dv+2] when m > 128
+  void* chi;          // [BH][n][m] key features 2^(lambda_j - R_j)/sqrt(m), p permuted in 16-blocks
+  float* rj;          // [BH][n]    running key frame R_j (log2)
   int H; int n; int w; int nch; int BH; float eps;
 };
 
@@ -181,6 +183,62 @@ __global__ __launch_bounds__(256) void k_state_scan(FwdArgs a) {
     rx[nch] = R;
     if (a.final_rex != nullptr) a.final_rex[bh] = R;
   }
+}
+
+// ---------------------------------------------------------------------------
+// Key features of every token in the causal running frame (one wave per chunk,
+// after the scan has fixed each chunk's entry frame Rex_b):
+//   R_j = max(Rex_b, max_{s0 <= j' <= j} max_p lambda_j'p),  chi_j = 2^(lambda_j - R_j)/sqrt(m)
+// stored with p permuted inside 16-blocks (the LDS operand layout), for the
+// readout's intra-chunk correction and, through the shared workspace, the
+// backward sweeps.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int M>
+__global__ __launch_bounds__(256) void k_keyfeat(FwdArgs a) {
+  using F = MF<T>;
+  const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
+  const int bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch;
+  const int cb = blockIdx.x * 4 + wv;
+  if (cb >= nch) return;
+  const int s0 = cb * 32;
+  const size_t seq = (size_t)bh * n;
+  const T* ks = (const T*)a.k + seq * D;
+  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
+  f32x16 acc[M / 32];
+  float nk;
+  key_logits<T, D, M, true>(acc, nk, ks, s0, n, omk_h);
+  const bool vt = s0 + col < n;
+  float mx = kNegInf;
+#pragma unroll
+  for (int pt = 0; pt < M / 32; ++pt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      float x = vt ? acc[pt][v] - 0.5f * kLog2e * nk : kNegInf;
+      acc[pt][v] = x;
+      mx = fmaxf(mx, x);
+    }
+  mx = half_swap_max(mx);
+  float R = mx;
+#pragma unroll
+  for (int o = 1; o < 32; o <<= 1) {
+    float t = __shfl_up(R, o, 32);
+    if (col >= o) R = fmaxf(R, t);
+  }
+  R = fmaxf(R, a.rex[(size_t)bh * (nch + 1) + cb]);
+  if (!vt) return;
+  if (h == 0) a.rj[seq + s0 + col] = R;
+  const float rsm = rsqrtf((float)M);
+  T* row = (T*)a.chi + (seq + s0 + col) * M;
+#pragma unroll
+  for (int pt = 0; pt < M / 32; ++pt)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      typedef T V4 __attribute__((ext_vector_type(4)));
+      V4 x4;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x4[e] = (T)(fast_exp2(acc[pt][4 * g + e] - R) * rsm);
+      *(V4*)(row + F::sigma(pt * 32 + 8 * g + 4 * h)) = x4;   // sigma keeps 4-groups contiguous
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -346,7 +404,7 @@ struct RCfg {
   static constexpr int oMt = oOm + a16(FB * (D + PAD) * ES);
   static constexpr int oA = oMt + a16(DV * (FB + PAD) * ES);
   static constexpr int oChi = oA + a16(M * 4);
-  static constexpr int oVt = oChi + a16(BC * (M + PAD) * ES);
+  static constexpr int oVt = oChi + a16(BC * (FB + PAD) * ES);
   static constexpr int oR = oVt + a16(DV * (BC + PAD) * ES);
   static constexpr int oUt = oR + a16(WIN * (D + PAD) * ES);
   static constexpr int oQ = oUt + a16(DV * UST * ES);
@@ -379,19 +437,15 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
   constexpr int S = M * DV + M;
   const size_t seq = (size_t)bh * n;
   const T* qs = (const T*)a.q + seq * D;
-  const T* ks = (const T*)a.k + seq * D;
   const T* vs = (const T*)a.v + seq * DV;
   const T* rs_ = (const T*)a.r + seq * D;
   const T* us = (const T*)a.u + seq * DV;
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
-  const T* omk_h = (const T*)a.omk + (size_t)hh * (sizeof(T) == 2 ? 2 : 1) * M * D;
   const float* bst = a.states + ((size_t)bh * nch + cb) * S;
   const float Rexb = a.rex[(size_t)bh * (nch + 1) + cb];
   const bool has_bnd = cb > 0;
 
-  // ---- prologue: key features of the chunk (wave 0) ----
-  if (wv == 0) chunk_key_features<T, D, M>(ks, s0, n, omk_h, Rexb, sChi, M + PAD, sRj);
-  // ---- prologue: everything else (all waves) ----
+  // ---- prologue ----
   const int fbk = blockIdx.z;
   {
     // every global load of the prologue first, then the LDS stores; the
@@ -404,6 +458,7 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     StageRows<T, WIN, D, NT> sr;
     StageRowsT<T, WIN, DV, NT> su;
     StageRows<T, 32, D, NT> sq;
+    StageRows<T, 32, FB, NT> sc;
     if constexpr (sizeof(T) == 2) so.load(a.omega + ((size_t)hh * M + (size_t)fbk * FB) * D, D, 0, 0, FB, tid);
     else so.load(omq_h + (size_t)fbk * FB * D, D, 0, 0, FB, tid);
     if (has_bnd) sm.load(bst + (size_t)fbk * FB * DV, tid);
@@ -411,6 +466,8 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     sr.load(rs_, D, wb, 0, n, tid);
     su.load(us, DV, wb, 0, n, tid);
     sq.load(qs, D, s0, 0, n, tid);
+    sc.load((const T*)a.chi + seq * M + fbk * FB, M, s0, 0, n, tid);   // this block's features
+    const float rjv = (tid < 32) ? a.rj[seq + min(s0 + tid, n - 1)] : 0.0f;
     float av[(M + NT - 1) / NT];
 #pragma unroll
     for (int k = 0; k < (M + NT - 1) / NT; ++k) {
@@ -438,6 +495,8 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     });
     if constexpr (sizeof(T) == 2) sq.store((f16*)sQ, D + PAD, s0, 0, n, tid);
     else sq.store(sQ, D + PAD, s0, 0, n, tid);
+    sc.store(sChi, FB + PAD, s0, 0, n, tid);
+    if (tid < 32) sRj[tid] = (s0 + tid < n) ? rjv : 0.0f;
   }
   __syncthreads();
 
@@ -530,12 +589,12 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
       // intra-chunk causal correction: P^T[j, anchor] = chi_j . psi_anchor, scaled
       // by the frame ratio 2^(R_j - R_i) and masked to j <= i
       f32x16 accP = zero16();
-      const T* chirow = sChi + col * (M + PAD);
+      const T* chirow = sChi + col * (FB + PAD);
 #pragma unroll
       for (int pt = 0; pt < FB / 32; ++pt)
 #pragma unroll
         for (int sp = 0; sp < F::CSTEPS; ++sp)
-          accP = F::mma(F::ldc(chirow, fb * FB + pt * 32, sp, h), pf[pt][sp], accP);
+          accP = F::mma(F::ldc(chirow, pt * 32, sp, h), pf[pt][sp], accP);
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         accP[v] *= sj[v];
@@ -661,6 +720,10 @@ static int run_fwd(const Shape& s, FwdArgs a, hipStream_t st) {
     ProfScope ps("state_scan", st);
     k_state_scan<M, DV><<<dim3((S / 4 + 255) / 256, BH), 256, 0, st>>>(a);
   }
+  if (a.out != nullptr || a.final_M == nullptr) {      // not for a prefill
+    ProfScope ps("keyfeat", st);
+    k_keyfeat<T, D, M><<<dim3((nch + 3) / 4, BH), 256, 0, st>>>(a);
+  }
   if (a.out != nullptr) {
     constexpr int NFB = RCfg<T, D, DV, M, NW, NA>::NFB;
     { ProfScope ps("fwd_readout", st);
@@ -748,6 +811,7 @@ int launch_forward(const Shape& s, const void* q, const void* k, const void* v, 
   a.final_M = final_M; a.final_a = final_a; a.final_rex = final_rex;
   a.H = (int)s.H; a.n = (int)s.n; a.w = s.w; a.nch = (int)s.nch(); a.BH = (int)s.BH(); a.eps = s.eps;
   a.part = ws.part;
+  a.chi = ws.chi; a.rj = ws.rj;
   const int NA = (s.w + 31) / 32;
 #define X(T, D_, DV_, M_)                                                          \
   if (s.dtype == (sizeof(T) == 2 ? 1 : 0) && s.D == D_ && s.Dv == DV_ && s.m == M_) { \

@@ -29,6 +29,8 @@ struct Workspace {
   float* states;    // [BH][nch][m*Dv + m]  chunk contributions, then boundary states
   float* rho;       // [BH][nch]            chunk max of key log2-features
   float* rex;       // [BH][nch + 1]        frame (log2) of each boundary state; [nch] = final
+  void* chi;        // [BH][n][m] operand type: key features 2^(lambda_j - R_j)/sqrt(m), p permuted in 16-blocks
+  float* rj;        // [BH][n]              running key frame R_j (log2)
   float* part;      // [m/128][BH][n][Dv+2] per-feature-block readout partials (m > 128)
   // backward-only regions (null in forward)
   float* gstates;   // [BH][nch][m*Dv + m]  per-chunk state gradients, then reverse-scanned
@@ -37,8 +39,6 @@ struct Workspace {
   float* du32;      // [nfb][BH][n][Dv]     du per feature block (m > 128 only)
   float* dr32;      // [nfb][BH][n][D]      dr per feature block (m > 128 only)
   float* dq32;      // [nfb][ns][BH][n][D]  dq partial of each anchor tile (slot = row chunk - anchor tile)
-  void* chi;        // [BH][n][m] operand type: key features 2^(lambda_j - R_j)/sqrt(m), p permuted in 16-blocks
-  float* rj;        // [BH][n]              running key frame R_j (log2)
   float* rowstat;   // [BH][n][2]           per-row 1/(Z+eps) and dZ
 };
 
