@@ -37,6 +37,7 @@ size_t workspace_bytes(const Shape& s, bool backward) {
   size_t t = 0;
   t += al(H * md * s.esize());                 // omq
   t += al(H * md * 4);                         // omk (bf16 hi+lo, or f32)
+  t += al(H * md * 2);                         // omh
   t += al(BH * nch * S * 4);                   // states
   t += al(BH * nch * 4);                       // rho
   t += al(BH * (nch + 1) * 4);                 // rex
@@ -64,6 +65,7 @@ void carve(const Shape& s, void* base, bool backward, Workspace* ws) {
   memset(ws, 0, sizeof(*ws));
   ws->omq = p; p += al(H * md * s.esize());
   ws->omk = p; p += al(H * md * 4);
+  ws->omh = p; p += al(H * md * 2);
   ws->states = (float*)p; p += al(BH * nch * S * 4);
   ws->rho = (float*)p; p += al(BH * nch * 4);
   ws->rex = (float*)p; p += al(BH * (nch + 1) * 4);

@@ -45,6 +45,7 @@ struct BwdArgs {
   void *dq, *dk, *dv, *dr, *du;
   const void* omq;
   const void* omk;
+  const void* omh;
   const float* states;
   const float* rex;
   float* gst;       // [BH][nch][M*DV + M]  GB_b, then Ghat_b
@@ -272,11 +273,11 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
 
   if constexpr (sizeof(T) == 2) {
-    StageRows<float, FB, D, NT> so;
+    StageRows<f16, FB, D, NT> so;
     StageRows<T, 32, D, NT> sr;
-    so.load(a.omega + ((size_t)hh * M + (size_t)fb * FB) * D, D, 0, 0, FB, tid);
+    so.load((const f16*)a.omh + ((size_t)hh * M + (size_t)fb * FB) * D, D, 0, 0, FB, tid);
     sr.load(rs_, D, c0, 0, n, tid);
-    so.store((f16*)sOm, D + PAD, 0, 0, FB, tid, kLog2e);
+    so.store((f16*)sOm, D + PAD, 0, 0, FB, tid);
     sr.store((f16*)sR, D + PAD, c0, 0, n, tid);
   } else {
     StageRows<T, FB, D, NT> so;
@@ -867,13 +868,7 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
   for (int s = 0; s < D / F::KS; ++s) {
     const int k0 = s * F::KS + h * F::KPL;
     if constexpr (sizeof(T) == 2) {
-      const float* orow = a.omega + ((size_t)hh * M + pw + col) * D + k0;
-      const f32x4 o0 = *(const f32x4*)orow, o1 = *(const f32x4*)(orow + 4);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        omf[s][e] = (f16)(o0[e] * kLog2e);
-        omf[s][4 + e] = (f16)(o1[e] * kLog2e);
-      }
+      omf[s] = *(const f16x8*)((const f16*)a.omh + ((size_t)hh * M + pw + col) * D + k0);
     } else {
       omf[s] = F::ld(omq_h + (size_t)(pw + col) * D, k0);
     }
@@ -1348,7 +1343,7 @@ int launch_backward(const Shape& s, const void* q, const void* k, const void* v,
   BwdArgs a;
   a.q = q; a.k = k; a.v = v; a.r = r; a.u = u; a.omega = omega; a.out = out; a.stats = stats;
   a.dout = dout; a.dq = dq; a.dk = dk; a.dv = dv; a.dr = dr; a.du = du;
-  a.omq = ws.omq; a.omk = ws.omk; a.states = ws.states; a.rex = ws.rex;
+  a.omq = ws.omq; a.omk = ws.omk; a.omh = ws.omh; a.states = ws.states; a.rex = ws.rex;
   a.gst = ws.gstates; a.dchi = ws.dchi; a.dvin = ws.dvin; a.du32 = ws.du32; a.dr32 = ws.dr32;
   a.dq32 = ws.dq32; a.rowstat = ws.rowstat; a.chi = ws.chi; a.rj = ws.rj;
   a.H = (int)s.H; a.n = (int)s.n; a.w = s.w; a.nch = (int)s.nch(); a.BH = (int)s.BH();

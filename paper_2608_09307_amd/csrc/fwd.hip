@@ -28,7 +28,7 @@ struct FwdArgs {
   const void* q; const void* k; const void* v; const void* r; const void* u;
   const float* omega;
   void* out; float* stats;
-  void* omq; void* omk;
+  void* omq; void* omk; void* omh;
   float* states; float* rho; float* rex;
   float* final_M; float* final_a; float* final_rex;   // optional state after the last token
   float* part;                                        // [NFB][BH][n][Dv+2] when m > 128
@@ -40,15 +40,17 @@ struct FwdArgs {
 // ---------------------------------------------------------------------------
 // K0: Omega * log2(e) in the operand type; key side keeps a hi/lo bf16 split so
 // that key log features are accurate to ~2^-16 relative (bf16 keys are exact).
+// bf16 inputs also get an f16 copy for the query-side logits (f16 matrix cores).
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void k_prep_omega(const float* __restrict__ omega, T* __restrict__ omq,
-                                                    T* __restrict__ omk, int H, int MD) {
+                                                    T* __restrict__ omk, f16* __restrict__ omh, int H, int MD) {
   int idx = blockIdx.x * 256 + threadIdx.x;
   if (idx >= H * MD) return;
   float x = omega[idx] * kLog2e;
   omq[idx] = (T)x;
   if constexpr (sizeof(T) == 2) {
+    omh[idx] = (f16)x;
     int hh = idx / MD, e = idx % MD;
     bf16 hi = (bf16)x;
     omk[(size_t)hh * 2 * MD + e] = hi;
@@ -451,7 +453,7 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     // every global load of the prologue first, then the LDS stores; the
     // transposed copies take the row index fastest across lanes, so the
     // 2-byte LDS writes of one instruction fall in one row
-    using OmT = typename std::conditional<sizeof(T) == 2, float, T>::type;
+    using OmT = typename std::conditional<sizeof(T) == 2, f16, T>::type;
     StageRows<OmT, FB, D, NT> so;
     StageState<FB, DV, NT, true> sm;
     StageRowsT<T, 32, DV, NT> sv;
@@ -459,7 +461,7 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     StageRowsT<T, WIN, DV, NT> su;
     StageRows<T, 32, D, NT> sq;
     StageRows<T, 32, FB, NT> sc;
-    if constexpr (sizeof(T) == 2) so.load(a.omega + ((size_t)hh * M + (size_t)fbk * FB) * D, D, 0, 0, FB, tid);
+    if constexpr (sizeof(T) == 2) so.load((const f16*)a.omh + ((size_t)hh * M + (size_t)fbk * FB) * D, D, 0, 0, FB, tid);
     else so.load(omq_h + (size_t)fbk * FB * D, D, 0, 0, FB, tid);
     if (has_bnd) sm.load(bst + (size_t)fbk * FB * DV, tid);
     sv.load(vs, DV, s0, 0, n, tid);
@@ -474,7 +476,7 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
       const int p = tid + NT * k;
       av[k] = (has_bnd && p < M) ? bst[(size_t)M * DV + p] : 0.0f;
     }
-    if constexpr (sizeof(T) == 2) so.store((f16*)sOm, D + PAD, 0, 0, FB, tid, kLog2e);
+    if constexpr (sizeof(T) == 2) so.store((f16*)sOm, D + PAD, 0, 0, FB, tid);
     else so.store(sOm, D + PAD, 0, 0, FB, tid);
     sm.store(tid, [&](int p, int d0, const f32x4& x) {
 #pragma unroll
@@ -699,7 +701,7 @@ static int run_fwd(const Shape& s, FwdArgs a, hipStream_t st) {
   {
     int tot = (int)s.H * M * D;
     ProfScope ps("prep_omega", st);
-    k_prep_omega<T><<<(tot + 255) / 256, 256, 0, st>>>(a.omega, (T*)a.omq, (T*)a.omk, (int)s.H, M * D);
+    k_prep_omega<T><<<(tot + 255) / 256, 256, 0, st>>>(a.omega, (T*)a.omq, (T*)a.omk, (f16*)a.omh, (int)s.H, M * D);
   }
   if constexpr (sizeof(T) == 2 && M <= 128) {
     if (a.out == nullptr && a.final_M != nullptr) {   // prefill: the final state only
@@ -807,7 +809,7 @@ int launch_forward(const Shape& s, const void* q, const void* k, const void* v, 
   FwdArgs a;
   a.q = q; a.k = k; a.v = v; a.r = r; a.u = u; a.omega = omega;
   a.out = out; a.stats = stats;
-  a.omq = ws.omq; a.omk = ws.omk; a.states = ws.states; a.rho = ws.rho; a.rex = ws.rex;
+  a.omq = ws.omq; a.omk = ws.omk; a.omh = ws.omh; a.states = ws.states; a.rho = ws.rho; a.rex = ws.rex;
   a.final_M = final_M; a.final_a = final_a; a.final_rex = final_rex;
   a.H = (int)s.H; a.n = (int)s.n; a.w = s.w; a.nch = (int)s.nch(); a.BH = (int)s.BH(); a.eps = s.eps;
   a.part = ws.part;

@@ -26,6 +26,7 @@ struct Shape {
 struct Workspace {
   void* omq;        // [H][m][D] operand type: query-side Omega * log2(e)
   void* omk;        // bf16: [H][2][m][D] hi/lo split of Omega*log2(e); f32: [H][m][D]
+  void* omh;        // [H][m][D] f16 Omega*log2(e): the query-side logits of bf16 inputs
   float* states;    // [BH][nch][m*Dv + m]  chunk contributions, then boundary states
   float* rho;       // [BH][nch]            chunk max of key log2-features
   float* rex;       // [BH][nch + 1]        frame (log2) of each boundary state; [nch] = final
