@@ -474,14 +474,15 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       auto put = [&](int p0) {
         return [&, p0](int p, int d0, const f32x4& x) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) sMp[(p0 + p) * (DV + PAD) + d0 + e] = (T)x[e];
+          for (int e = 0; e < 4; ++e) sMp[(p0 + p) * (DV + PAD) + d0 + e] = has_bnd ? (T)x[e] : (T)0.0f;
         };
       };
-      if (has_bnd) {
-        sm.store(tid, put(0));
-        if (tid < FB) sA[tid] = av;
-        sm.load(bst + (size_t)(fb * FB + FH) * DV, tid);
-      }
+      // the first chunk stages a zero boundary state, so that the boundary
+      // product below needs no branch (its accumulator chain then starts
+      // from an inline zero and the sweep keeps more registers)
+      sm.store(tid, put(0));
+      if (tid < FB) sA[tid] = av;
+      if (has_bnd) sm.load(bst + (size_t)(fb * FB + FH) * DV, tid);
       StageRows<T, 32, FB, NT> sc;
       StageRows<T, 32, DV, NT> sv;
       StageRows<T, 32, D, NT> sq;
@@ -489,7 +490,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       sv.load(vs, DV, s0, 0, n, tid);
       sq.load(qs, D, s0, 0, n, tid);
       const float rjv = (tid < 32) ? a.rj[seq + min(s0 + tid, n - 1)] : 0.0f;
-      if (has_bnd) sm.store(tid, put(FH));
+      sm.store(tid, put(FH));
       sc.store(sChi, C::CST, s0, 0, n, tid);
       sv.store(sV, C::VST, s0, 0, n, tid);
       if constexpr (sizeof(T) == 2) sq.store((f16*)sQ, D + PAD, s0, 0, n, tid);
@@ -572,18 +573,17 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
 #pragma unroll
       for (int pt = 0; pt < FB / 32; ++pt) {
         no_hoist();
+        // boundary part sb_i (M_b dA_c + dZ_i a_b), zero in the first chunk
         f32x16 dps = zero16();
-        if (has_bnd) {
 #pragma unroll
-          for (int s = 0; s < DV / F::KS; ++s)
-            dps = F::mma(F::ld(sMp + (pt * 32 + col) * (DV + PAD), s * F::KS + h * F::KPL), daf[s], dps);
-          const float* sAh = sA + pt * 32 + 4 * h;
+        for (int s = 0; s < DV / F::KS; ++s)
+          dps = F::mma(F::ld(sMp + (pt * 32 + col) * (DV + PAD), s * F::KS + h * F::KPL), daf[s], dps);
+        const float* sAh = sA + pt * 32 + 4 * h;
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const f32x4 av = *(const f32x4*)(sAh + 8 * g);
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 av = *(const f32x4*)(sAh + 8 * g);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) dps[4 * g + e] = (dps[4 * g + e] + dZ * av[e]) * sb;
-          }
+          for (int e = 0; e < 4; ++e) dps[4 * g + e] = (dps[4 * g + e] + dZ * av[e]) * sb;
         }
         // chi^T rows p, k = token j in crow order (chi stored [j][sigma(p)])
 #pragma unroll
