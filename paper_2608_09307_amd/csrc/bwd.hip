@@ -352,24 +352,36 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
       typename F::frag ppf[F::CSTEPS];
 #pragma unroll
       for (int sp = 0; sp < F::CSTEPS; ++sp) ppf[sp] = F::cfrag(accP, sp);
+      // two 32-wide d slices per step: two independent matrix-core chains
+      constexpr int G = DV / 32 >= 2 ? 2 : 1;
 #pragma unroll
-      for (int dt = 0; dt < DV / 32; ++dt) {
+      for (int d0 = 0; d0 < DV / 32; d0 += G) {
         no_hoist();
-        f32x16 accA = zero16();
+        f32x16 accA[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) accA[g] = zero16();
         if (has_bnd) {
-          const T* mrow = sMt + (dt * 32 + col) * (FB + PAD);
 #pragma unroll
           for (int pt = 0; pt < FB / 32; ++pt)
 #pragma unroll
             for (int sp = 0; sp < F::CSTEPS; ++sp)
-              accA = F::mma(pf[pt][sp], F::ldc(mrow, pt * 32, sp, h), accA);
-          if (sb != 1.0f) accA *= sb;
+#pragma unroll
+              for (int g = 0; g < G; ++g)
+                accA[g] = F::mma(pf[pt][sp], F::ldc(sMt + ((d0 + g) * 32 + col) * (FB + PAD), pt * 32, sp, h), accA[g]);
+          if (sb != 1.0f) {
+#pragma unroll
+            for (int g = 0; g < G; ++g) accA[g] *= sb;
+          }
         }
 #pragma unroll
         for (int sp = 0; sp < F::CSTEPS; ++sp)
-          accA = F::mma(ppf[sp], F::tld_crow(sV, C::VST, 0, sp, dt * 32), accA);
 #pragma unroll
-        for (int v = 0; v < 16; ++v) du[dt][v] += accA[v] * dN[dt];
+          for (int g = 0; g < G; ++g)
+            accA[g] = F::mma(ppf[sp], F::tld_crow(sV, C::VST, 0, sp, (d0 + g) * 32), accA[g]);
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) du[d0 + g][v] += accA[g][v] * dN[d0 + g];
       }
     }
   }
