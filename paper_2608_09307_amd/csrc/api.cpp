@@ -39,6 +39,7 @@ size_t workspace_bytes(const Shape& s, bool backward) {
   t += al(H * md * 4);                         // omk (bf16 hi+lo, or f32)
   t += al(H * md * 2);                         // omh
   t += al(BH * nch * S * 4);                   // states
+  if (s.esize() == 2) t += al(BH * nch * (size_t)s.m * s.Dv * 2);   // states16
   t += al(BH * nch * 4);                       // rho
   t += al(BH * (nch + 1) * 4);                 // rex
   t += al(BH * (size_t)s.n * s.m * s.esize()); // chi
@@ -67,6 +68,7 @@ void carve(const Shape& s, void* base, bool backward, Workspace* ws) {
   ws->omk = p; p += al(H * md * 4);
   ws->omh = p; p += al(H * md * 2);
   ws->states = (float*)p; p += al(BH * nch * S * 4);
+  if (s.esize() == 2) { ws->states16 = p; p += al(BH * nch * (size_t)s.m * s.Dv * 2); }
   ws->rho = (float*)p; p += al(BH * nch * 4);
   ws->rex = (float*)p; p += al(BH * (nch + 1) * 4);
   ws->chi = p; p += al(BH * (size_t)s.n * s.m * s.esize());

@@ -47,6 +47,7 @@ struct BwdArgs {
   const void* omk;
   const void* omh;
   const float* states;
+  const void* states16;
   const float* rex;
   float* gst;       // [BH][nch][M*DV + M]  GB_b, then Ghat_b
   float* dchi;      // [BH][n][M]           intra-chunk key-feature gradient
@@ -300,20 +301,33 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
     {
       // every global load of the chunk first, then the LDS stores
       StageState<FB, DV, NT, true> sm;
+      StageRowsT<T, FB, DV, NT> sm16;
       StageRows<T, 32, FB, NT> sc;
       StageRows<T, 32, DV, NT> sv;
       StageRows<T, 32, D, NT> sq;
-      if (has_bnd) sm.load(a.states + ((size_t)bh * nch + ch) * S + (size_t)fb * FB * DV, tid);
+      if constexpr (sizeof(T) == 2) {
+        if (has_bnd) sm16.load((const T*)a.states16 + (((size_t)bh * nch + ch) * M + (size_t)fb * FB) * DV, DV, 0, 0, FB, tid);
+      } else {
+        if (has_bnd) sm.load(a.states + ((size_t)bh * nch + ch) * S + (size_t)fb * FB * DV, tid);
+      }
       sc.load(chis, M, s0, 0, n, tid);
       sv.load(vs, DV, s0, 0, n, tid);
       sq.load(qs, D, s0, 0, n, tid);
       const float rjv = (tid < 32) ? a.rj[seq + min(s0 + tid, n - 1)] : 0.0f;
       __syncthreads();
-      if (has_bnd)
-        sm.store(tid, [&](int p, int d0, const f32x4& x) {
+      if (has_bnd) {
+        if constexpr (sizeof(T) == 2) {
+          sm16.store(0, 0, FB, tid, [&](int p, int d0, const typename StageRowsT<T, FB, DV, NT>::V4& x) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = (T)x[e];
-        });
+            for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = x[e];
+          });
+        } else {
+          sm.store(tid, [&](int p, int d0, const f32x4& x) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = (T)x[e];
+          });
+        }
+      }
       sc.store(sChi, C::CST, s0, 0, n, tid);
       sv.store(sV, C::VST, s0, 0, n, tid);
       if constexpr (sizeof(T) == 2) sq.store((f16*)sQ, D + PAD, s0, 0, n, tid);
@@ -472,14 +486,17 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
     const bool has_bnd = ch > 0;
     const float Rexb = a.rex[(size_t)bh * (nch + 1) + ch];
     {
-      // the chunk's global loads in two batches (the second half of the state
-      // with the chunk rows), each issued in full before its LDS stores
+      // the chunk's global loads, each batch issued in full before its LDS
+      // stores (float32 inputs: the state in two halves, the second with
+      // the chunk rows; bf16 inputs: the bf16 state at once)
       constexpr int FH = FB / 2;
       StageState<FH, DV, NT, false> sm;
+      StageRows<T, FB, DV, NT> sm16;
       const float* bst = a.states + ((size_t)bh * nch + ch) * S;
       float av = 0.0f;
       if (has_bnd) {
-        sm.load(bst + (size_t)fb * FB * DV, tid);
+        if constexpr (sizeof(T) == 2) sm16.load((const T*)a.states16 + (((size_t)bh * nch + ch) * M + (size_t)fb * FB) * DV, DV, 0, 0, FB, tid);
+        else sm.load(bst + (size_t)fb * FB * DV, tid);
         if (tid < FB) av = bst[(size_t)M * DV + fb * FB + tid];
       }
       __syncthreads();
@@ -492,9 +509,13 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       // the first chunk stages a zero boundary state, so that the boundary
       // product below needs no branch (its accumulator chain then starts
       // from an inline zero and the sweep keeps more registers)
-      sm.store(tid, put(0));
+      if constexpr (sizeof(T) == 2) {
+        sm16.store(sMp, DV + PAD, has_bnd ? 0 : FB, 0, FB, tid);   // rows outside [0, FB): zero
+      } else {
+        sm.store(tid, put(0));
+        if (has_bnd) sm.load(bst + (size_t)(fb * FB + FH) * DV, tid);
+      }
       if (tid < FB) sA[tid] = av;
-      if (has_bnd) sm.load(bst + (size_t)(fb * FB + FH) * DV, tid);
       StageRows<T, 32, FB, NT> sc;
       StageRows<T, 32, DV, NT> sv;
       StageRows<T, 32, D, NT> sq;
@@ -502,7 +523,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       sv.load(vs, DV, s0, 0, n, tid);
       sq.load(qs, D, s0, 0, n, tid);
       const float rjv = (tid < 32) ? a.rj[seq + min(s0 + tid, n - 1)] : 0.0f;
-      sm.store(tid, put(FH));
+      if constexpr (sizeof(T) != 2) sm.store(tid, put(FH));
       sc.store(sChi, C::CST, s0, 0, n, tid);
       sv.store(sV, C::VST, s0, 0, n, tid);
       if constexpr (sizeof(T) == 2) sq.store((f16*)sQ, D + PAD, s0, 0, n, tid);
@@ -1355,7 +1376,7 @@ int launch_backward(const Shape& s, const void* q, const void* k, const void* v,
   BwdArgs a;
   a.q = q; a.k = k; a.v = v; a.r = r; a.u = u; a.omega = omega; a.out = out; a.stats = stats;
   a.dout = dout; a.dq = dq; a.dk = dk; a.dv = dv; a.dr = dr; a.du = du;
-  a.omq = ws.omq; a.omk = ws.omk; a.omh = ws.omh; a.states = ws.states; a.rex = ws.rex;
+  a.omq = ws.omq; a.omk = ws.omk; a.omh = ws.omh; a.states = ws.states; a.states16 = ws.states16; a.rex = ws.rex;
   a.gst = ws.gstates; a.dchi = ws.dchi; a.dvin = ws.dvin; a.du32 = ws.du32; a.dr32 = ws.dr32;
   a.dq32 = ws.dq32; a.rowstat = ws.rowstat; a.chi = ws.chi; a.rj = ws.rj;
   a.H = (int)s.H; a.n = (int)s.n; a.w = s.w; a.nch = (int)s.nch(); a.BH = (int)s.BH();

@@ -30,6 +30,7 @@ struct FwdArgs {
   void* out; float* stats;
   void* omq; void* omk; void* omh;
   float* states; float* rho; float* rex;
+  void* states16;     // [BH][nch][m][Dv] bf16 inputs: the boundary states' M in bf16; null for float32
   float* final_M; float* final_a; float* final_rex;   // optional state after the last token
   float* part;                                        // [NFB][BH][n][Dv+2] when m > 128
   void* chi;          // [BH][n][m] key features 2^(lambda_j - R_j)/sqrt(m), p permuted in 16-blocks
@@ -138,8 +139,11 @@ __global__ __launch_bounds__(256) void k_chunk_state(FwdArgs a) {
 // K2b: exclusive scan over chunks with the log-scale monoid
 //   (M1, R1) + (M2, r2) = (e^{R1-R} M1 + e^{r2-R} M2, R = max(R1, r2))
 // in place: chunk b's contribution is replaced by the state of every token
-// before chunk b, in frame rex[b] (-inf for the empty state).  Element-parallel,
-// sequential over chunks, loads issued PF chunks ahead.
+// before chunk b, in frame rex[b] (-inf for the empty state).  With bf16
+// inputs the M part of that state goes to states16 in bf16 instead (the
+// operand type of every kernel that reads it, rounded once here; half the
+// bytes for the scan and its readers) and only a stays in place.
+// Element-parallel, sequential over chunks, loads issued PF chunks ahead.
 // [App. C "Host preparation": exclusive cumulative sum -> boundary states]
 // ---------------------------------------------------------------------------
 template <int M, int DV>
@@ -151,6 +155,7 @@ __global__ __launch_bounds__(256) void k_state_scan(FwdArgs a) {
   const bool act = i4 < S;
   const int nch = a.nch;
   float* st = a.states + (size_t)bh * nch * S;
+  bf16* s16 = a.states16 != nullptr ? (bf16*)a.states16 + (size_t)bh * nch * M * DV : nullptr;
   const float* rh = a.rho + (size_t)bh * nch;
   float* rx = a.rex + (size_t)bh * (nch + 1);
   const bool writer = (blockIdx.x == 0 && threadIdx.x == 0);
@@ -171,7 +176,16 @@ __global__ __launch_bounds__(256) void k_state_scan(FwdArgs a) {
       float Rn = fmaxf(R, rb);
       float sa = fast_exp2(R - Rn);      // 0 when R = -inf
       float sb = fast_exp2(rb - Rn);
-      if (act) *(f32x4*)(st + (size_t)b * S + i4) = run;
+      if (s16 != nullptr && i4 < M * DV) {
+        if (act) {
+          bf16x4 y;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) y[e] = (bf16)run[e];
+          *(bf16x4*)(s16 + (size_t)b * M * DV + i4) = y;
+        }
+      } else if (act) {
+        *(f32x4*)(st + (size_t)b * S + i4) = run;
+      }
       if (writer) rx[b] = R;
       run = run * sa + x[e] * sb;
       R = Rn;
@@ -456,6 +470,7 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     using OmT = typename std::conditional<sizeof(T) == 2, f16, T>::type;
     StageRows<OmT, FB, D, NT> so;
     StageState<FB, DV, NT, true> sm;
+    StageRowsT<T, FB, DV, NT> sm16;
     StageRowsT<T, 32, DV, NT> sv;
     StageRows<T, WIN, D, NT> sr;
     StageRowsT<T, WIN, DV, NT> su;
@@ -463,7 +478,11 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     StageRows<T, 32, FB, NT> sc;
     if constexpr (sizeof(T) == 2) so.load((const f16*)a.omh + ((size_t)hh * M + (size_t)fbk * FB) * D, D, 0, 0, FB, tid);
     else so.load(omq_h + (size_t)fbk * FB * D, D, 0, 0, FB, tid);
-    if (has_bnd) sm.load(bst + (size_t)fbk * FB * DV, tid);
+    if constexpr (sizeof(T) == 2) {
+      if (has_bnd) sm16.load((const T*)a.states16 + (((size_t)bh * nch + cb) * M + (size_t)fbk * FB) * DV, DV, 0, 0, FB, tid);
+    } else {
+      if (has_bnd) sm.load(bst + (size_t)fbk * FB * DV, tid);
+    }
     sv.load(vs, DV, s0, 0, n, tid);
     sr.load(rs_, D, wb, 0, n, tid);
     su.load(us, DV, wb, 0, n, tid);
@@ -478,10 +497,17 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     }
     if constexpr (sizeof(T) == 2) so.store((f16*)sOm, D + PAD, 0, 0, FB, tid);
     else so.store(sOm, D + PAD, 0, 0, FB, tid);
-    sm.store(tid, [&](int p, int d0, const f32x4& x) {
+    if constexpr (sizeof(T) == 2) {
+      sm16.store(0, 0, FB, tid, [&](int p, int d0, const typename StageRowsT<T, FB, DV, NT>::V4& x) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = has_bnd ? (T)x[e] : (T)0.0f;
-    });
+        for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = has_bnd ? x[e] : (T)0.0f;
+      });
+    } else {
+      sm.store(tid, [&](int p, int d0, const f32x4& x) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = has_bnd ? (T)x[e] : (T)0.0f;
+      });
+    }
 #pragma unroll
     for (int k = 0; k < (M + NT - 1) / NT; ++k)
       if (tid + NT * k < M) sA[tid + NT * k] = av[k];
@@ -809,7 +835,7 @@ int launch_forward(const Shape& s, const void* q, const void* k, const void* v, 
   FwdArgs a;
   a.q = q; a.k = k; a.v = v; a.r = r; a.u = u; a.omega = omega;
   a.out = out; a.stats = stats;
-  a.omq = ws.omq; a.omk = ws.omk; a.omh = ws.omh; a.states = ws.states; a.rho = ws.rho; a.rex = ws.rex;
+  a.omq = ws.omq; a.omk = ws.omk; a.omh = ws.omh; a.states = ws.states; a.states16 = ws.states16; a.rho = ws.rho; a.rex = ws.rex;
   a.final_M = final_M; a.final_a = final_a; a.final_rex = final_rex;
   a.H = (int)s.H; a.n = (int)s.n; a.w = s.w; a.nch = (int)s.nch(); a.BH = (int)s.BH(); a.eps = s.eps;
   a.part = ws.part;
