@@ -36,6 +36,7 @@
 
 namespace linsimp {
 
+
 struct BwdArgs {
   const void *q, *k, *v, *r, *u;
   const float* omega;
@@ -111,13 +112,14 @@ __global__ __launch_bounds__(256) void k_bwd_rowprep(BwdArgs a) {
 // ---------------------------------------------------------------------------
 // Anchor-stationary sweeps.  A workgroup owns the 32 anchors [c0, c0 + 32) of
 // one sequence and one feature block, and walks the row chunks that can see
-// them (rows c0 .. c0 + 31 + w - 1); each wave takes every eighth row of a
-// chunk.  Per (row, anchor tile) the query features psi[p, c] are formed with
+// them (rows c0 .. c0 + 31 + w - 1); in the dq/dr sweep each wave takes
+// every eighth row of a chunk (du, below, stages the three chunks at once and
+// pairs rows).  Per (row, anchor tile) the query features psi[p, c] are formed with
 // lanes <-> anchor (registers <-> feature), exactly as in the forward readout,
 // and the anchor-side sums stay in registers; the waves' sums are added once
 // at the end.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int DV, int M, int NA, bool DQ>
+template <typename T, int D, int DV, int M, int NA>
 struct AsCfg {
   static constexpr int PAD = MF<T>::PAD;
   static constexpr int FB = M < 128 ? M : 128;
@@ -128,11 +130,11 @@ struct AsCfg {
   static constexpr int mx(int x, int y) { return x > y ? x : y; }
   static constexpr int oOm = 0;                                             // Omega block [p][D]
   static constexpr int oM = oOm + a16(FB * (D + PAD) * ES);                 // boundary M ([d][sigma(p)] or [p][d])
-  static constexpr int TPF = tr_pad<T, FB>(), TPV = tr_pad<T, DV>(), TPD = tr_pad<T, D>();
-  // row pitches: chi and r are read transposed by the dq/dr sweep, V by the du sweep
-  static constexpr int CST = DQ ? FB + TPF : FB + PAD;
-  static constexpr int VST = DQ ? DV + PAD : DV + TPV;
-  static constexpr int RST = DQ ? D + TPD : D + PAD;
+  static constexpr int TPF = tr_pad<T, FB>(), TPD = tr_pad<T, D>();
+  // row pitches: chi and r are read transposed
+  static constexpr int CST = FB + TPF;
+  static constexpr int VST = DV + PAD;
+  static constexpr int RST = D + TPD;
   static constexpr int oChi = oM + a16(mx(DV * (FB + PAD), FB * (DV + PAD)) * ES);   // chi [j][sigma(p)]
   static constexpr int oV = oChi + a16(32 * CST * ES);                      // V [j][d]
   static constexpr int oQ = oV + a16(32 * VST * ES);                        // q rows of the chunk
@@ -142,7 +144,7 @@ struct AsCfg {
   static constexpr int oA = oRj + a16(32 * 4);                              // boundary a
   static constexpr int oW = oA + a16(FB * 4);                               // per wave: dN (DV), s_c (32)
   static constexpr int oOb = oW + a16(NW * (DV + 32) * 4);                 // Omega*log2 e, operand type (dz)
-  static constexpr int BYTES0 = DQ ? oOb + a16(FB * (D + TPD) * ES) : oOb;
+  static constexpr int BYTES0 = oOb + a16(FB * (D + TPD) * ES);
   static constexpr int RED = (NW / 2) * 32 * mx(DV, D) * 4;                 // end-of-sweep reduction
   static constexpr int BYTES = mx(BYTES0, RED);
 };
@@ -243,13 +245,43 @@ LS_DEV void frame_ratios(float (&sj)[16], const float* sRj, int t, float Ri) {
 
 // ---------------------------------------------------------------------------
 // k_bwd_du: du_c = sum_i dN_i (*) A_ic,  A_ic = psi_ic^T M^(i)  (regs <-> anchor,
-// lanes <-> d).  M^(i) = sb_i M_b + sum_{j <= i in the chunk} 2^(R_j - R_i) chi_j v_j^T.
+// lanes <-> d).  A workgroup stages once the boundary state M_b of its own
+// chunk kt and the key features, values and queries of chunks kt .. kt+2; the
+// state of any row i that sees the tile is then the boundary part plus a tail
+// of at most three chunks,
+//   M^(i) = 2^(Rex_kt - R_i) M_b + sum_{c0 <= j <= i} 2^(R_j - R_i) chi_j v_j^T.
+// Row t of chunk kt sees anchors c <= t of the tile and row t of chunk kt+2
+// anchors c > t (w <= 64): the two run as one pair, each lane c taking the row
+// that sees anchor c, so the logits, features and boundary product are formed
+// once for both.  Rows of chunk kt+1 run one at a time.
 // ---------------------------------------------------------------------------
+template <typename T, int D, int DV, int M>
+struct DuCfg {
+  static constexpr int PAD = MF<T>::PAD;
+  static constexpr int FB = M < 128 ? M : 128;
+  static constexpr int NW = 8;
+  static constexpr int ES = sizeof(T);
+  static constexpr int a16(int x) { return (x + 15) & ~15; }
+  static constexpr int mx(int x, int y) { return x > y ? x : y; }
+  static constexpr int CST = FB + PAD;                       // chi [j][sigma(p)]
+  static constexpr int VST = DV + tr_pad<T, DV>();           // V [j][d] (read transposed)
+  static constexpr int oOm = 0;                              // Omega block [p][D]
+  static constexpr int oM = oOm + a16(FB * (D + PAD) * ES);  // M_b^T [d][sigma(p)]
+  static constexpr int oChi = oM + a16(DV * (FB + PAD) * ES);
+  static constexpr int oV = oChi + a16(96 * CST * ES);
+  static constexpr int oQ = oV + a16(96 * VST * ES);
+  static constexpr int oR = oQ + a16(96 * (D + PAD) * ES);   // r of the anchor tile
+  static constexpr int oRj = oR + a16(32 * (D + PAD) * ES);  // R_j of the 96 rows
+  static constexpr int BYTES0 = oRj + a16(96 * 4);
+  static constexpr int RED = (NW / 2) * 32 * DV * 4;         // end-of-sweep reduction
+  static constexpr int BYTES = mx(BYTES0, RED);
+};
+
 template <typename T, int D, int DV, int M, int NA>
 __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
   using F = MF<T>;
-  using C = AsCfg<T, D, DV, M, NA, false>;
-  constexpr int PAD = C::PAD, FB = C::FB, NW = C::NW;
+  using C = DuCfg<T, D, DV, M>;
+  constexpr int PAD = C::PAD, FB = C::FB, NW = C::NW, CST = C::CST, VST = C::VST;
   constexpr int NT = 64 * NW;
   constexpr int S = M * DV + M;
   static_assert(C::BYTES <= 160 * 1024, "du LDS budget");
@@ -272,131 +304,149 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
   const T* gs = (const T*)a.dout + seq * DV;
   const T* chis = (const T*)a.chi + seq * M + fb * FB;
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
+  const bool has_bnd = kt > 0;
+  const float Rexb = a.rex[(size_t)bh * (nch + 1) + kt];
 
-  if constexpr (sizeof(T) == 2) {
-    StageRows<f16, FB, D, NT> so;
-    StageRows<T, 32, D, NT> sr;
-    so.load((const f16*)a.omh + ((size_t)hh * M + (size_t)fb * FB) * D, D, 0, 0, FB, tid);
-    sr.load(rs_, D, c0, 0, n, tid);
-    so.store((f16*)sOm, D + PAD, 0, 0, FB, tid);
-    sr.store((f16*)sR, D + PAD, c0, 0, n, tid);
-  } else {
-    StageRows<T, FB, D, NT> so;
-    StageRows<T, 32, D, NT> sr;
-    so.load(omq_h + (size_t)fb * FB * D, D, 0, 0, FB, tid);
-    sr.load(rs_, D, c0, 0, n, tid);
-    so.store(sOm, D + PAD, 0, 0, FB, tid);
-    sr.store(sR, D + PAD, c0, 0, n, tid);
+  // ---- staging, once per workgroup ----
+  {
+    // Omega block, r of the tile and the boundary state (zero for the first chunk)
+    StageState<FB, DV, NT, true> sm;
+    StageRowsT<T, FB, DV, NT> sm16;
+    if constexpr (sizeof(T) == 2) {
+      if (has_bnd) sm16.load((const T*)a.states16 + (((size_t)bh * nch + kt) * M + (size_t)fb * FB) * DV, DV, 0, 0, FB, tid);
+    } else {
+      if (has_bnd) sm.load(a.states + ((size_t)bh * nch + kt) * S + (size_t)fb * FB * DV, tid);
+    }
+    if constexpr (sizeof(T) == 2) {
+      StageRows<f16, FB, D, NT> so;
+      StageRows<T, 32, D, NT> sr;
+      so.load((const f16*)a.omh + ((size_t)hh * M + (size_t)fb * FB) * D, D, 0, 0, FB, tid);
+      sr.load(rs_, D, c0, 0, n, tid);
+      so.store((f16*)sOm, D + PAD, 0, 0, FB, tid);
+      sr.store((f16*)sR, D + PAD, c0, 0, n, tid);
+      sm16.store(0, 0, FB, tid, [&](int p, int d0, const typename StageRowsT<T, FB, DV, NT>::V4& x) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = has_bnd ? x[e] : (T)0.0f;
+      });
+    } else {
+      StageRows<T, FB, D, NT> so;
+      StageRows<T, 32, D, NT> sr;
+      so.load(omq_h + (size_t)fb * FB * D, D, 0, 0, FB, tid);
+      sr.load(rs_, D, c0, 0, n, tid);
+      so.store(sOm, D + PAD, 0, 0, FB, tid);
+      sr.store(sR, D + PAD, c0, 0, n, tid);
+      sm.store(tid, [&](int p, int d0, const f32x4& x) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = has_bnd ? (T)x[e] : (T)0.0f;
+      });
+    }
   }
+  {
+    // key features, values, queries and frames of rows c0 .. c0 + 95 (zero past n)
+    StageRows<T, 96, FB, NT> sc;
+    StageRows<T, 96, DV, NT> sv;
+    sc.load(chis, M, c0, 0, n, tid);
+    sv.load(vs, DV, c0, 0, n, tid);
+    sc.store(sChi, CST, c0, 0, n, tid);
+    sv.store(sV, VST, c0, 0, n, tid);
+    StageRows<T, 96, D, NT> sq;
+    sq.load(qs, D, c0, 0, n, tid);
+    if constexpr (sizeof(T) == 2) sq.store((f16*)sQ, D + PAD, c0, 0, n, tid);
+    else sq.store(sQ, D + PAD, c0, 0, n, tid);
+    for (int j = tid; j < 96; j += NT) sRj[j] = (c0 + j < n) ? a.rj[seq + c0 + j] : 0.0f;
+  }
+  __syncthreads();
+
   f32x16 du[DV / 32];
 #pragma unroll
   for (int dt = 0; dt < DV / 32; ++dt) du[dt] = zero16();
-  const int ch_end = min(nch - 1, (c0 + 30 + w) / 32);     // last chunk with a row that sees the tile
 
+  // items 0..31: pair t (rows c0 + t and c0 + 64 + t); 32..63: row c0 + 32 + t
 #pragma unroll 1
-  for (int ch = kt; ch <= ch_end; ++ch) {
-    const int s0 = ch * 32;
-    const bool has_bnd = ch > 0;
-    const float Rexb = a.rex[(size_t)bh * (nch + 1) + ch];
-    {
-      // every global load of the chunk first, then the LDS stores
-      StageState<FB, DV, NT, true> sm;
-      StageRowsT<T, FB, DV, NT> sm16;
-      StageRows<T, 32, FB, NT> sc;
-      StageRows<T, 32, DV, NT> sv;
-      StageRows<T, 32, D, NT> sq;
-      if constexpr (sizeof(T) == 2) {
-        if (has_bnd) sm16.load((const T*)a.states16 + (((size_t)bh * nch + ch) * M + (size_t)fb * FB) * DV, DV, 0, 0, FB, tid);
-      } else {
-        if (has_bnd) sm.load(a.states + ((size_t)bh * nch + ch) * S + (size_t)fb * FB * DV, tid);
-      }
-      sc.load(chis, M, s0, 0, n, tid);
-      sv.load(vs, DV, s0, 0, n, tid);
-      sq.load(qs, D, s0, 0, n, tid);
-      const float rjv = (tid < 32) ? a.rj[seq + min(s0 + tid, n - 1)] : 0.0f;
-      __syncthreads();
-      if (has_bnd) {
-        if constexpr (sizeof(T) == 2) {
-          sm16.store(0, 0, FB, tid, [&](int p, int d0, const typename StageRowsT<T, FB, DV, NT>::V4& x) {
+  for (int it = wv; it < 64; it += NW) {
+    const bool pair = it < 32;
+    const int t = it & 31;
+    const int iA = pair ? c0 + t : c0 + 32 + t;
+    const int iB = c0 + 64 + t;
+    const bool okA = iA < n && (pair || t + 1 < w);            // the row sees the tile
+    const bool okB = pair && iB < n && t + 33 < w;
+    if (!okA && !okB) continue;
+    const int rcA = pair ? 0 : 1;                              // chunk of row A relative to kt
+    // row scalars of the (at most two) rows
+    const int iAc = min(iA, n - 1), iBc = min(iB, n - 1);
+    const float LA = uniform(a.stats[(seq + iAc) * 2]), LB = uniform(a.stats[(seq + iBc) * 2]);
+    const float invA = uniform(a.rowstat[(seq + iAc) * 2]), invB = uniform(a.rowstat[(seq + iBc) * 2]);
+    const float RA = uniform(okA ? sRj[rcA * 32 + t] : -kNegInf), RB = uniform(okB ? sRj[64 + t] : -kNegInf);
+    const float sbA = uniform(has_bnd ? fast_exp2(Rexb - RA) : 0.0f);
+    const float sbB = uniform(has_bnd ? fast_exp2(Rexb - RB) : 0.0f);
+    float dNA[DV / 32], dNB[DV / 32];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = x[e];
-          });
-        } else {
-          sm.store(tid, [&](int p, int d0, const f32x4& x) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = (T)x[e];
-          });
-        }
-      }
-      sc.store(sChi, C::CST, s0, 0, n, tid);
-      sv.store(sV, C::VST, s0, 0, n, tid);
-      if constexpr (sizeof(T) == 2) sq.store((f16*)sQ, D + PAD, s0, 0, n, tid);
-      else sq.store(sQ, D + PAD, s0, 0, n, tid);
-      if (tid < 32) sRj[tid] = (s0 + tid < n) ? rjv : 0.0f;
+    for (int dt = 0; dt < DV / 32; ++dt) {
+      dNA[dt] = tof(gs[(size_t)iAc * DV + dt * 32 + col]) * invA;
+      dNB[dt] = tof(gs[(size_t)iBc * DV + dt * 32 + col]) * invB;
     }
-    __syncthreads();
-
-#pragma unroll 1
-    for (int t = wv; t < 32; t += NW) {
-      const int i = s0 + t;
-      if (i >= n || i < c0 || i - c0 > w + 30) continue;
-      const float Li = uniform(a.stats[(seq + i) * 2]);
-      const float inv = uniform(a.rowstat[(seq + i) * 2]);
-      const float Ri = uniform(sRj[t]);
-      const float sb = uniform(has_bnd ? fast_exp2(Rexb - Ri) : 0.0f);
-      float dN[DV / 32];
+    // this lane's row: the one that sees anchor c0 + col
+    const bool useB = pair && col > t;
+    const int i = useB ? iB : iA;
+    const int rc = useB ? 2 : rcA;
+    const float Ri = useB ? RB : RA;
+    const bool valid = (useB ? okB : okA) && (i - c0 - col >= 0) && (i - c0 - col < w);
+    typename F::frag pf[FB / 32][F::CSTEPS];
+    query_features<T, D, FB>(pf, sQ + (rc * 32 + t) * (D + PAD), sR + col * (D + PAD), sOm, valid, useB ? LB : LA);
+    // tails: P^T[j, c] = chi_j . psi_c of chunk kt + rj, framed, j <= row(c)
+    constexpr int NTL = 3;
+    typename F::frag ppf[NTL][F::CSTEPS];
+    const int ntl = okB ? 3 : rcA + 1;                          // tails any lane needs
 #pragma unroll
-      for (int dt = 0; dt < DV / 32; ++dt) dN[dt] = tof(gs[(size_t)i * DV + dt * 32 + col]) * inv;
-      const int c = c0 + col;
-      const bool valid = (i - c >= 0) && (i - c < w);
-      typename F::frag pf[FB / 32][F::CSTEPS];
-      query_features<T, D, FB>(pf, sQ + t * (D + PAD), sR + col * (D + PAD), sOm, valid, Li);
-      // intra-chunk part: P^T[j, c] = chi_j . psi_c, framed, j <= i
-      float sj[16];
-      frame_ratios(sj, sRj, t, Ri);
+    for (int rj = 0; rj < NTL; ++rj) {
+      if (rj >= ntl) {
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp) ppf[rj][sp] = F::zero();
+        continue;
+      }
       f32x16 accP = zero16();
-      const T* chirow = sChi + col * C::CST;
+      const T* chirow = sChi + (rj * 32 + col) * CST;
 #pragma unroll
       for (int pt = 0; pt < FB / 32; ++pt)
 #pragma unroll
         for (int sp = 0; sp < F::CSTEPS; ++sp)
           accP = F::mma(F::ldc(chirow, pt * 32, sp, h), pf[pt][sp], accP);
+      const int lim = rj < rc ? 31 : (rj == rc ? t : -1);      // last token of chunk rj this lane's row sees
+      const float* sRjh = sRj + rj * 32 + 4 * h;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) accP[v] *= sj[v];
-      typename F::frag ppf[F::CSTEPS];
+      for (int g = 0; g < 4; ++g) {
+        const f32x4 r4 = *(const f32x4*)(sRjh + 8 * g);
 #pragma unroll
-      for (int sp = 0; sp < F::CSTEPS; ++sp) ppf[sp] = F::cfrag(accP, sp);
-      // two 32-wide d slices per step: two independent matrix-core chains
-      constexpr int G = DV / 32 >= 2 ? 2 : 1;
-#pragma unroll
-      for (int d0 = 0; d0 < DV / 32; d0 += G) {
-        no_hoist();
-        f32x16 accA[G];
-#pragma unroll
-        for (int g = 0; g < G; ++g) accA[g] = zero16();
-        if (has_bnd) {
-#pragma unroll
-          for (int pt = 0; pt < FB / 32; ++pt)
-#pragma unroll
-            for (int sp = 0; sp < F::CSTEPS; ++sp)
-#pragma unroll
-              for (int g = 0; g < G; ++g)
-                accA[g] = F::mma(pf[pt][sp], F::ldc(sMt + ((d0 + g) * 32 + col) * (FB + PAD), pt * 32, sp, h), accA[g]);
-          if (sb != 1.0f) {
-#pragma unroll
-            for (int g = 0; g < G; ++g) accA[g] *= sb;
-          }
+        for (int e = 0; e < 4; ++e) {
+          const float x = fast_exp2(r4[e] - Ri);
+          accP[4 * g + e] *= (8 * g + 4 * h + e <= lim) ? x : 0.0f;
         }
+      }
+#pragma unroll
+      for (int sp = 0; sp < F::CSTEPS; ++sp) ppf[rj][sp] = F::cfrag(accP, sp);
+    }
+#pragma unroll
+    for (int dt = 0; dt < DV / 32; ++dt) {
+      no_hoist();
+      f32x16 accA = zero16();
+      const T* mrow = sMt + (dt * 32 + col) * (FB + PAD);
+#pragma unroll
+      for (int pt = 0; pt < FB / 32; ++pt)
 #pragma unroll
         for (int sp = 0; sp < F::CSTEPS; ++sp)
+          accA = F::mma(pf[pt][sp], F::ldc(mrow, pt * 32, sp, h), accA);
+      // registers <-> anchor crow(v, h): its row's boundary frame and dN
 #pragma unroll
-          for (int g = 0; g < G; ++g)
-            accA[g] = F::mma(ppf[sp], F::tld_crow(sV, C::VST, 0, sp, (d0 + g) * 32), accA[g]);
+      for (int v = 0; v < 16; ++v) accA[v] *= (pair && crow(v, h) > t) ? sbB : sbA;
 #pragma unroll
-        for (int g = 0; g < G; ++g)
+      for (int rj = 0; rj < NTL; ++rj) {
+        if (rj >= ntl) continue;
 #pragma unroll
-          for (int v = 0; v < 16; ++v) du[d0 + g][v] += accA[g][v] * dN[d0 + g];
+        for (int sp = 0; sp < F::CSTEPS; ++sp)
+          accA = F::mma(ppf[rj][sp], F::tld_crow(sV, VST, rj * 32, sp, dt * 32), accA);
       }
+#pragma unroll
+      for (int v = 0; v < 16; ++v) du[dt][v] += accA[v] * ((pair && crow(v, h) > t) ? dNB[dt] : dNA[dt]);
     }
   }
   reduce_waves<DV / 32>(du, (float*)smem, wv, NW);
@@ -407,7 +457,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
       for (int v = 0; v < 16; ++v) {
         const int c = c0 + crow(v, h);
         if (c >= n) continue;
-        if constexpr (C::NFB == 1) ((T*)a.du)[(seq + c) * DV + dt * 32 + col] = (T)du[dt][v];
+        if constexpr (M / FB == 1) ((T*)a.du)[(seq + c) * DV + dt * 32 + col] = (T)du[dt][v];
         else a.du32[(((size_t)fb * a.BH + bh) * n + c) * DV + dt * 32 + col] = du[dt][v];
       }
   }
@@ -424,7 +474,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
 template <typename T, int D, int DV, int M, int NA>
 __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
   using F = MF<T>;
-  using C = AsCfg<T, D, DV, M, NA, true>;
+  using C = AsCfg<T, D, DV, M, NA>;
   constexpr int PAD = C::PAD, FB = C::FB, NW = C::NW;
   constexpr int NT = 64 * NW;
   constexpr int S = M * DV + M;
@@ -1309,7 +1359,7 @@ static int launch_err(const char* what) {
 
 template <typename T, int D, int DV, int M, int NA>
 static int run_bwd(const Shape& s, BwdArgs a, hipStream_t st) {
-  using A = AsCfg<T, D, DV, M, NA, true>;
+  using A = AsCfg<T, D, DV, M, NA>;
   constexpr int NFB = A::NFB;
   constexpr int NS = NA + 1;
   const int BH = (int)s.BH();
