@@ -425,28 +425,39 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
 #pragma unroll
       for (int sp = 0; sp < F::CSTEPS; ++sp) ppf[rj][sp] = F::cfrag(accP, sp);
     }
+    // two 32-wide d slices per step (two independent matrix-core chains);
+    // registers <-> anchor crow(v, h), which takes its row's frame and dN
+    constexpr int G = DV / 32 >= 2 ? 2 : 1;
 #pragma unroll
-    for (int dt = 0; dt < DV / 32; ++dt) {
+    for (int d0 = 0; d0 < DV / 32; d0 += G) {
       no_hoist();
-      f32x16 accA = zero16();
-      const T* mrow = sMt + (dt * 32 + col) * (FB + PAD);
+      f32x16 accA[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) accA[g] = zero16();
 #pragma unroll
       for (int pt = 0; pt < FB / 32; ++pt)
 #pragma unroll
         for (int sp = 0; sp < F::CSTEPS; ++sp)
-          accA = F::mma(pf[pt][sp], F::ldc(mrow, pt * 32, sp, h), accA);
-      // registers <-> anchor crow(v, h): its row's boundary frame and dN
 #pragma unroll
-      for (int v = 0; v < 16; ++v) accA[v] *= (pair && crow(v, h) > t) ? sbB : sbA;
+          for (int g = 0; g < G; ++g)
+            accA[g] = F::mma(pf[pt][sp], F::ldc(sMt + ((d0 + g) * 32 + col) * (FB + PAD), pt * 32, sp, h), accA[g]);
+#pragma unroll
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) accA[g][v] *= (pair && crow(v, h) > t) ? sbB : sbA;
 #pragma unroll
       for (int rj = 0; rj < NTL; ++rj) {
         if (rj >= ntl) continue;
 #pragma unroll
         for (int sp = 0; sp < F::CSTEPS; ++sp)
-          accA = F::mma(ppf[rj][sp], F::tld_crow(sV, VST, rj * 32, sp, dt * 32), accA);
+#pragma unroll
+          for (int g = 0; g < G; ++g)
+            accA[g] = F::mma(ppf[rj][sp], F::tld_crow(sV, VST, rj * 32, sp, (d0 + g) * 32), accA[g]);
       }
 #pragma unroll
-      for (int v = 0; v < 16; ++v) du[dt][v] += accA[v] * ((pair && crow(v, h) > t) ? dNB[dt] : dNA[dt]);
+      for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) du[d0 + g][v] += accA[g][v] * ((pair && crow(v, h) > t) ? dNB[d0 + g] : dNA[d0 + g]);
     }
   }
   reduce_waves<DV / 32>(du, (float*)smem, wv, NW);
