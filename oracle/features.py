@@ -11,15 +11,10 @@ Each row is then marginally N(0, I_D), so Lemma 1 still holds.
 
 ``orthogonal_block`` / ``orthogonal_bank_from`` take the random draws (G and
 the chi_D radii) as inputs, so a device sampler can be compared with the same
-draws.  ``iid_bank`` is the plain Gaussian bank the synthetic workloads use.
+draws.
 """
 
 import numpy as np
-
-
-def iid_bank(rng, m, D):
-    """Omega with iid N(0, 1) entries, [m, D]."""
-    return rng.standard_normal((m, D))
 
 
 def orthogonal_block(G, radii, sign_correct=True):

@@ -136,38 +136,3 @@ def head_backward(q, k, v, r, u, Omega, w, tau, gate, dy, norm_eps=NORM_EPS, rms
     dk = _l2_backward(k, dkh, norm_eps)
     dr = _l2_backward(r, drh, norm_eps)
     return dq, dk, dv, dr, du, dtau, dgate
-
-
-def head_forward_bh(q, k, v, r, u, Omega, w, tau, gate, heads=None, **kw):
-    """head_forward over [B, H, n, *] inputs; tau [H]; gate [H] or [B, H, n, Dv].
-    Returns y [B, H, n, Dv] (only the listed (b, h) pairs when heads is given)."""
-    B, H = q.shape[:2]
-    y = np.zeros(v.shape, np.float64)
-    pairs = heads if heads is not None else [(b, h) for b in range(B) for h in range(H)]
-    gate = np.asarray(gate)
-    for b, h in pairs:
-        gt = gate[h] if gate.ndim == 1 else gate[b, h]
-        y[b, h], _ = head_forward(q[b, h], k[b, h], v[b, h], r[b, h], u[b, h], Omega[h], w, tau[h], gt, **kw)
-    return y
-
-
-def head_backward_bh(q, k, v, r, u, Omega, w, tau, gate, dy, heads=None, **kw):
-    """head_backward over [B, H, n, *]; returns dq, dk, dv, dr, du ([B, H, n, *]),
-    dtau [H] and dgate ([H] or [B, H, n, Dv]), summed over the processed pairs."""
-    B, H = q.shape[:2]
-    outs = [np.zeros(x.shape, np.float64) for x in (q, k, v, r, u)]
-    dtau = np.zeros(H)
-    gate = np.asarray(gate)
-    dgate = np.zeros(gate.shape, np.float64)
-    pairs = heads if heads is not None else [(b, h) for b in range(B) for h in range(H)]
-    for b, h in pairs:
-        gt = gate[h] if gate.ndim == 1 else gate[b, h]
-        res = head_backward(q[b, h], k[b, h], v[b, h], r[b, h], u[b, h], Omega[h], w, tau[h], gt, dy[b, h], **kw)
-        for o, x in zip(outs, res[:5]):
-            o[b, h] = x
-        dtau[h] += res[5]
-        if gate.ndim == 1:
-            dgate[h] += res[6]
-        else:
-            dgate[b, h] = res[6]
-    return (*outs, dtau, dgate)

@@ -182,55 +182,55 @@ def forward_logspace(q, k, v, r, u, Omega, w, eps=EPS):
 
 
 def forward_chunked(q, k, v, r, u, Omega, w, chunk=32, feature_block=128, eps=EPS):
-    """Chunked form of App. C (host preparation, state reconstruction,
-    Alg. 1).
+    """Chunked evaluation (App. C "Host preparation" and state reconstruction,
+    with the query-side shift of App. B.2 taken per feature block).
 
-    Host preparation: chi_j = phi(k_j); per-chunk sums of chi v^T and chi;
-    exclusive cumulative sum over chunks gives the boundary states (M_b, a_b)
-    of everything before chunk b.  Sequences are right-padded to a multiple
-    of the chunk with zero keys-features (padded rows are discarded).
-    Per row i of chunk b: M_i = M_b + sum_{j in b, j <= i} chi_j v_j^T (the
-    masked tail), then Alg. 1: feature blocks P with one running maximum
-    shared by anchors and features, rescaling N and Z when it grows.
+    States: the key features are grouped into chunks of ``chunk`` tokens
+    (right-padded with zero features); the state of row i is the exclusive
+    prefix over earlier chunks (eq:Mstate, eq:astate summed chunk by chunk)
+    plus the tokens j <= i of its own chunk.
+
+    Readout: the log features of all anchors and all features of a row are
+    formed at once.  The features are split into blocks of ``feature_block``;
+    each block b is shifted by its own maximum L_b, giving partial sums
+    (N_b, Z_b) of eq:Ni and eq:Zi scaled by e^{-L_b}.  The blocks are then
+    merged with the common shift L = max_b L_b: N = sum_b e^{L_b - L} N_b and
+    likewise Z.  The shift cancels in eq:linearized-output; eps is compared
+    with the unshifted Z, so it enters as eps e^{-L}.
     """
     q, k, v, r, u, Omega = _f64(q, k, v, r, u, Omega)
     n, Dv = v.shape
     m = Omega.shape[0]
-    nb = -(-n // chunk)
-    npad = nb * chunk
-    chi = np.zeros((npad, m))
-    chi[:n] = phi(k, Omega)
-    vp = np.zeros((npad, Dv))
-    vp[:n] = v
-    chi_b = chi.reshape(nb, chunk, m)
-    v_b = vp.reshape(nb, chunk, Dv)
-    Mc = np.einsum("bjp,bjd->bpd", chi_b, v_b)          # chunk contributions
-    ac = chi_b.sum(axis=1)
-    Mb = np.concatenate([np.zeros((1, m, Dv)), np.cumsum(Mc, axis=0)[:-1]])  # exclusive
-    ab = np.concatenate([np.zeros((1, m)), np.cumsum(ac, axis=0)[:-1]])
+    nchunks = -(-n // chunk)
+    feats = np.zeros((nchunks * chunk, m))
+    feats[:n] = phi(k, Omega)
+    vals = np.zeros((nchunks * chunk, Dv))
+    vals[:n] = v
+    feats = feats.reshape(nchunks, chunk, m)
+    vals = vals.reshape(nchunks, chunk, Dv)
+    # per-chunk totals, then the exclusive prefix over chunks
+    tot_M = np.matmul(feats.transpose(0, 2, 1), vals)                  # [nchunks, m, Dv]
+    tot_a = feats.sum(axis=1)                                          # [nchunks, m]
+    before_M = np.cumsum(tot_M, axis=0) - tot_M
+    before_a = np.cumsum(tot_a, axis=0) - tot_a
+    blocks = [np.arange(p0, min(m, p0 + feature_block)) for p0 in range(0, m, feature_block)]
     out = np.zeros((n, Dv))
     for i in range(n):
         b, t = divmod(i, chunk)
-        mask = (np.arange(chunk) <= t).astype(np.float64)[:, None]
-        Mi = Mb[b] + (chi_b[b] * mask).T @ v_b[b]       # masked tail, one matmul
-        ai = ab[b] + (chi_b[b] * mask).sum(axis=0)
+        M_i = before_M[b] + feats[b, : t + 1].T @ vals[b, : t + 1]
+        a_i = before_a[b] + feats[b, : t + 1].sum(axis=0)
         C = anchor_window(i, w)
-        zq = composite_query(q[i], r[C])
-        Lrun, N, Z = -np.inf, np.zeros(Dv), 0.0
-        for p0 in range(0, m, feature_block):
-            P = slice(p0, min(m, p0 + feature_block))
-            ell = zq @ Omega[P].T - 0.5 * np.sum(zq * zq, axis=1, keepdims=True)
-            Lnew = max(Lrun, ell.max())
-            if np.isfinite(Lrun):
-                N *= np.exp(Lrun - Lnew)
-                Z *= np.exp(Lrun - Lnew)
-            psi = np.exp(ell - Lnew) / np.sqrt(m)
-            N += np.sum((psi @ Mi[P]) * u[C], axis=0)
-            Z += np.sum(psi @ ai[P])
-            Lrun = Lnew
-        # N, Z above are the true ones times e^{-Lrun}; eps is compared with
-        # the true Z as in eq:linearized-output.
-        out[i] = N / (Z + eps * np.exp(-Lrun))
+        ell = log_features(composite_query(q[i], r[C]), Omega)       # [|C|, m]
+        L_b = np.array([ell[:, P].max() for P in blocks])
+        parts = []
+        for P, Lb in zip(blocks, L_b):
+            psi = np.exp(ell[:, P] - Lb) / np.sqrt(m)
+            parts.append((np.sum((psi @ M_i[P]) * u[C], axis=0), np.sum(psi @ a_i[P])))
+        L = L_b.max()
+        scale = np.exp(L_b - L)
+        N = sum(s * nb for s, (nb, _) in zip(scale, parts))
+        Z = sum(s * zb for s, (_, zb) in zip(scale, parts))
+        out[i] = N / (Z + eps * np.exp(-L))
     return out
 
 
@@ -250,14 +250,6 @@ def exact_window(q, k, v, r, u, w):
         kappa = np.exp(composite_query(q[i], r[C]) @ k[: i + 1].T)   # [|C|, i+1]
         out[i] = np.sum(u[C] * (kappa @ v[: i + 1]), axis=0) / kappa.sum()
     return out
-
-
-def exact_full(q, k, v, r, u):
-    """Exact 2-simplicial attention, Sec. 3.1 eq:exact-full: one softmax over
-    every causal pair (j, c), j <= i and c <= i.  O(n^3); tiny n only."""
-    q, k, v, r, u = _f64(q, k, v, r, u)
-    n = q.shape[0]
-    return exact_window(q, k, v, r, u, w=n)
 
 
 # ---------------------------------------------------------------------------
@@ -370,28 +362,3 @@ def decode_step(state, q_t, k_t, v_t, r_t, u_t, Omega, w, eps=EPS):
     Z = np.sum(F @ a)
     new = {"M": M, "a": a, "ring_r": ring_r, "ring_u": ring_u, "pos": t + 1}
     return N / (Z + eps), new
-
-
-# ---------------------------------------------------------------------------
-# Batched wrappers: [B, H, n, *] streams, Omega [H, m, D]
-# ---------------------------------------------------------------------------
-
-def forward_bh(q, k, v, r, u, Omega, w, eps=EPS, heads=None):
-    """Forward over [B, H, n, *] inputs, one Omega[h] per head.  ``heads`` is
-    an optional list of (b, h) pairs to evaluate (rows are independent across
-    (b, h), so a subset is exact for those pairs).  Returns a dict
-    {(b, h): out[n, Dv]}."""
-    B, H = q.shape[:2]
-    pairs = heads if heads is not None else [(b, h) for b in range(B) for h in range(H)]
-    return {(b, h): forward_recurrent(q[b, h], k[b, h], v[b, h], r[b, h], u[b, h],
-                                      Omega[h], w, eps)
-            for (b, h) in pairs}
-
-
-def backward_bh(q, k, v, r, u, Omega, w, dO, eps=EPS, heads=None):
-    """Backward over [B, H, n, *] inputs; returns {(b, h): (dq, dk, dv, dr, du)}."""
-    B, H = q.shape[:2]
-    pairs = heads if heads is not None else [(b, h) for b in range(B) for h in range(H)]
-    return {(b, h): backward(q[b, h], k[b, h], v[b, h], r[b, h], u[b, h],
-                             Omega[h], w, dO[b, h], eps)
-            for (b, h) in pairs}

@@ -375,6 +375,50 @@ def test_orthogonal_block_reconstructs_and_has_positive_diagonal():
     assert np.allclose(raw[0], -np.sign(G[0, 0]) * G[:, 0] / np.linalg.norm(G[:, 0]), atol=1e-13)
 
 
+def test_orthogonal_bank_from_stacks_blocks_in_order_and_truncates():
+    """orthogonal_bank_from (the reference of the device sampler): block b
+    comes from draw b and nothing else, blocks are stacked in draw order and
+    the last one is cut at m rows.  Pinned by properties of App. B.1's
+    construction, not by re-calling it: the rows of block b, divided by
+    radii[b], are orthonormal and Q_b^T G_b is upper triangular with a
+    positive diagonal (the sign-fixed R of G_b = Q_b R_b); a truncated block
+    keeps the leading rows, so those rows of Q^T G stay zero left of the
+    diagonal."""
+    rng = np.random.default_rng(72)
+    D, nb = 8, 3
+    G = rng.standard_normal((nb, D, D))
+    radii = np.sqrt(rng.chisquare(D, size=(nb, D)))
+    for m in (nb * D, nb * D - 3, D + 1, 5):
+        Om = features.orthogonal_bank_from(G, radii, m)
+        assert Om.shape == (m, D)
+        for b in range(-(-m // D)):
+            rows = Om[b * D: min(m, (b + 1) * D)]
+            k = rows.shape[0]
+            assert np.allclose(np.linalg.norm(rows, axis=1), radii[b, :k], rtol=1e-13)
+            Qt = rows / radii[b, :k, None]
+            assert np.allclose(Qt @ Qt.T, np.eye(k), atol=1e-13)
+            R = Qt @ G[b]                     # the leading k rows of R_b
+            assert np.allclose(np.tril(R, -1), 0, atol=1e-12)
+            assert np.all(np.diag(R[:, :k]) > 0)
+            if k >= 2:                        # draw b is the one that fits, not another's
+                other = Qt @ G[(b + 1) % nb]
+                assert not np.allclose(np.tril(other, -1), 0, atol=1e-6)
+    # the same draws replayed through the sampler give the same bank
+    m, D2 = 20, 6
+    r1 = np.random.default_rng(73)
+    Gs, Rs = [], []
+    for _ in range(-(-m // D2)):
+        Gs.append(r1.standard_normal((D2, D2)))
+        Rs.append(np.sqrt(r1.chisquare(D2, size=D2)))
+    assert np.array_equal(features.orthogonal_bank_from(np.stack(Gs), np.stack(Rs), m),
+                          features.orthogonal_bank(np.random.default_rng(73), m, D2))
+    # without the sign fix each block is Householder's factor of its own draw
+    raw = features.orthogonal_bank_from(G, np.ones((nb, D)), 2 * D, sign_correct=False)
+    for b in range(2):
+        g0 = G[b][:, 0]
+        assert np.allclose(raw[b * D], -np.sign(g0[0]) * g0 / np.linalg.norm(g0), atol=1e-13)
+
+
 def _kernel_error(rng, m, D, sign_correct, pairs):
     """RMS relative error of the kernel estimate of Lemma 1 over fixed pairs,
     one bank of m rows."""
