@@ -27,7 +27,10 @@
  * q, r (and u in the backward) are converted to f16 and z = q (*) r is
  * formed in f16, so the entries of q, r, u and of q (*) r must stay below
  * f16's largest value (65504) in magnitude; entries below 2^-14 keep fewer
- * bits.  Normalised streams (Sec. 3.1) are far inside that range.
+ * bits.  Normalised streams (Sec. 3.1) are far inside that range.  Outside
+ * it the rows whose queries or anchors overflow come out non-finite (inf or
+ * NaN); no status reports it, since the library never reads tensor data on
+ * the host.
  *
  * Conventions for every entry point:
  *   - Tensor pointers are DEVICE pointers owned by the caller, 16-byte aligned,
@@ -114,7 +117,14 @@ enum {
    * inputs, and nothing has written it since: its feature-bank copies,
    * boundary states and key features are reused instead of recomputed (the
    * backward otherwise re-runs the forward's state and key-feature passes).
-   * Results are bitwise those of linsimp_bwd. */
+   * Results are bitwise those of linsimp_bwd.  Those states depend on the
+   * dims, k, v and omega only: the library keeps a host-side record of the
+   * last call that left states in each workspace (linsimp_fwd, or
+   * linsimp_bwd_ex without the flag) and returns LINSIMP_E_INVALID_ARG when
+   * the record is missing (no such call, or a later linsimp_prefill or failed
+   * call on the same workspace) or names other dims or other k, v or omega
+   * pointers.  The contents behind those pointers must not have changed since
+   * (the library does not read data on the host). */
   LINSIMP_BWD_REUSE_STATES = 1
 };
 
@@ -147,7 +157,9 @@ int linsimp_prefill(const linsimp_dims* dims, const void* k, const void* v, cons
  *   q, k, r : [S, H, D] dtype;  v, u : [S, H, Dv] dtype;  omega [H, m, D] f32
  *   M, a, rho, ring_r, ring_u, pos : in/out, layouts as in linsimp_prefill
  *   out : [S, H, Dv] dtype
- * Uses no workspace.  Same shape support as the forward; S >= 1. */
+ * Uses no workspace.  Same shape support as the forward; 1 <= S and
+ * S*H <= 2^24 - 1 (one workgroup per (sequence, head); more returns
+ * LINSIMP_E_UNSUPPORTED).  pos advances only when the step was enqueued. */
 int linsimp_decode_step(int64_t S, int32_t H, int32_t D, int32_t Dv, int32_t m, int32_t w,
                         int32_t dtype, float eps, const void* q, const void* k, const void* v,
                         const void* r, const void* u, const float* omega, float* M, float* a,
@@ -162,7 +174,8 @@ int linsimp_decode_step(int64_t S, int32_t H, int32_t D, int32_t Dv, int32_t m, 
  *   q, k, r : [S, H, T, D] dtype;  v, u : [S, H, T, Dv] dtype; omega [H, m, D] f32
  *   M, a, rho, ring_r, ring_u, pos : in/out, layouts as in linsimp_prefill
  *   out : [S, H, T, Dv] dtype
- * 1 <= T <= 4096.  Uses no workspace.  Same shape support as the forward. */
+ * 1 <= T <= 4096.  Uses no workspace.  Same shape support and S*H bound as
+ * linsimp_decode_step. */
 int linsimp_decode_chunk(int64_t S, int32_t H, int32_t T, int32_t D, int32_t Dv, int32_t m,
                          int32_t w, int32_t dtype, float eps, const void* q, const void* k,
                          const void* v, const void* r, const void* u, const float* omega, float* M,

@@ -137,6 +137,59 @@ void timing_mark(const char* name, hipStream_t st, bool begin) {
   }
 }
 
+// ---- which forward's states a workspace holds ----
+// linsimp_bwd_ex with LINSIMP_BWD_REUSE_STATES reads the feature-bank copies,
+// boundary states, frames and key features a forward left in the workspace.
+// Those depend on the dims and on k, v and omega only, so every call that
+// writes them records (dims, k, v, omega) under the workspace pointer, calls
+// that overwrite them with something else drop the record, and a reusing
+// backward is refused unless the record matches its own arguments.
+struct StateRecord {
+  const void* ws;
+  int64_t B, H, n;
+  int D, Dv, m, w, dtype;
+  const void *k, *v, *omega;
+};
+static std::mutex g_recmu;
+static std::vector<StateRecord> g_records;       // most recent last
+static constexpr size_t kMaxRecords = 256;
+
+static void forget_states(const void* ws) {
+  std::lock_guard<std::mutex> lk(g_recmu);
+  for (size_t i = 0; i < g_records.size(); ++i)
+    if (g_records[i].ws == ws) { g_records.erase(g_records.begin() + i); break; }
+}
+
+void record_states(const void* ws, const Shape& s, const void* k, const void* v, const void* omega) {
+  forget_states(ws);
+  std::lock_guard<std::mutex> lk(g_recmu);
+  if (g_records.size() >= kMaxRecords) g_records.erase(g_records.begin());
+  g_records.push_back(StateRecord{ws, s.B, s.H, s.n, s.D, s.Dv, s.m, s.w, s.dtype, k, v, omega});
+}
+
+void drop_states(const void* ws) { forget_states(ws); }
+
+// LINSIMP_OK if `ws` holds the states of a forward with these dims, k, v and omega
+int check_states(const void* ws, const Shape& s, const void* k, const void* v, const void* omega) {
+  std::lock_guard<std::mutex> lk(g_recmu);
+  for (const StateRecord& r : g_records) {
+    if (r.ws != ws) continue;
+    if (r.B != s.B || r.H != s.H || r.n != s.n || r.D != s.D || r.Dv != s.Dv || r.m != s.m ||
+        r.w != s.w || r.dtype != s.dtype) {
+      set_error("LINSIMP_BWD_REUSE_STATES: the workspace holds the states of a forward with other dims");
+      return LINSIMP_E_INVALID_ARG;
+    }
+    if (r.k != k || r.v != v || r.omega != omega) {
+      set_error("LINSIMP_BWD_REUSE_STATES: the workspace holds the states of a forward with other k, v or omega");
+      return LINSIMP_E_INVALID_ARG;
+    }
+    return LINSIMP_OK;
+  }
+  set_error("LINSIMP_BWD_REUSE_STATES: no forward has left its states in this workspace "
+            "(or a later call overwrote them)");
+  return LINSIMP_E_INVALID_ARG;
+}
+
 bool shape_supported(const Shape& s, bool /*backward*/) {
   if (s.w < 1 || s.w > 64) return false;
   return fwd_combo_supported(s.dtype, s.D, s.Dv, s.m);
@@ -172,6 +225,17 @@ static int check_dims(const linsimp_dims* d, Shape* s, bool backward, bool bh_on
   s->dtype = d->dtype; s->eps = d->eps;
   if (!shape_supported(*s, backward)) {
     set_error("unsupported shape: dtype=%d D=%d Dv=%d m=%d w=%d", d->dtype, d->D, d->Dv, d->m, d->w);
+    return LINSIMP_E_UNSUPPORTED;
+  }
+  return LINSIMP_OK;
+}
+
+// the decode kernels run one 256-thread workgroup per (sequence, head) on a
+// one-dimensional grid, whose thread count must stay below 2^32
+static int check_decode_grid(int64_t S, int32_t H) {
+  if (S * (int64_t)H > kMaxDecodeGroups) {
+    set_error("decode: S*H = %lld (sequence, head) pairs, at most %lld per call",
+              (long long)(S * (int64_t)H), (long long)kMaxDecodeGroups);
     return LINSIMP_E_UNSUPPORTED;
   }
   return LINSIMP_OK;
@@ -227,8 +291,11 @@ int linsimp_fwd(const linsimp_dims* dims, const void* q, const void* k, const vo
   if ((rc = check_ws(s, false, workspace, workspace_bytes_))) return rc;
   Workspace ws;
   carve(s, workspace, false, &ws);
-  return launch_forward(s, q, k, v, r, u, omega, out, stats, nullptr, nullptr, nullptr, ws,
-                        (hipStream_t)stream);
+  rc = launch_forward(s, q, k, v, r, u, omega, out, stats, nullptr, nullptr, nullptr, ws,
+                      (hipStream_t)stream);
+  if (rc == LINSIMP_OK) record_states(workspace, s, k, v, omega);
+  else drop_states(workspace);
+  return rc;
 }
 
 int linsimp_bwd(const linsimp_dims* dims, const void* q, const void* k, const void* v,
@@ -253,10 +320,16 @@ int linsimp_bwd_ex(const linsimp_dims* dims, const void* q, const void* k, const
   const void* ps[] = {q, k, v, r, u, omega, out, stats, dout, dq, dk, dv, dr, du};
   if ((rc = check_ptrs("q,k,v,r,u,omega,out,stats,dout,dq,dk,dv,dr,du", ps, 14))) return rc;
   if ((rc = check_ws(s, true, workspace, workspace_bytes_))) return rc;
+  const bool reuse = flags == LINSIMP_BWD_REUSE_STATES;
+  if (reuse && (rc = check_states(workspace, s, k, v, omega))) return rc;
   Workspace ws;
   carve(s, workspace, true, &ws);
-  return launch_backward(s, q, k, v, r, u, omega, out, stats, dout, dq, dk, dv, dr, du, ws,
-                         (hipStream_t)stream, flags == LINSIMP_BWD_REUSE_STATES);
+  rc = launch_backward(s, q, k, v, r, u, omega, out, stats, dout, dq, dk, dv, dr, du, ws,
+                       (hipStream_t)stream, reuse);
+  // without reuse the backward re-ran the forward's state passes on its inputs
+  if (rc == LINSIMP_OK) { if (!reuse) record_states(workspace, s, k, v, omega); }
+  else drop_states(workspace);
+  return rc;
 }
 
 int linsimp_prefill(const linsimp_dims* dims, const void* k, const void* v, const void* r,
@@ -271,6 +344,7 @@ int linsimp_prefill(const linsimp_dims* dims, const void* k, const void* v, cons
   if ((rc = check_ws(s, false, workspace, workspace_bytes_))) return rc;
   Workspace ws;
   carve(s, workspace, false, &ws);
+  drop_states(workspace);          // the prefill leaves no reusable forward states
   rc = launch_forward(s, k, k, v, r, u, omega, nullptr, nullptr, M, a, rho, ws, (hipStream_t)stream);
   if (rc) return rc;
   return launch_ring_fill(s, r, u, ring_r, ring_u, pos, (hipStream_t)stream);
@@ -286,6 +360,7 @@ int linsimp_decode_step(int64_t S, int32_t H, int32_t D, int32_t Dv, int32_t m, 
   Shape s;
   int rc = check_dims(&d, &s, false, false);
   if (rc) return rc;
+  if ((rc = check_decode_grid(S, H))) return rc;
   const void* ps[] = {q, k, v, r, u, omega, M, a, rho, ring_r, ring_u, pos, out};
   if ((rc = check_ptrs("q,k,v,r,u,omega,M,a,rho,ring_r,ring_u,pos,out", ps, 13))) return rc;
   return launch_decode(S, H, 1, D, Dv, m, w, dtype, eps, q, k, v, r, u, omega, M, a, rho, ring_r,
@@ -306,6 +381,7 @@ int linsimp_decode_chunk(int64_t S, int32_t H, int32_t T, int32_t D, int32_t Dv,
   Shape s;
   int rc = check_dims(&d, &s, false, false);
   if (rc) return rc;
+  if ((rc = check_decode_grid(S, H))) return rc;
   const void* ps[] = {q, k, v, r, u, omega, M, a, rho, ring_r, ring_u, pos, out};
   if ((rc = check_ptrs("q,k,v,r,u,omega,M,a,rho,ring_r,ring_u,pos,out", ps, 13))) return rc;
   return launch_decode(S, H, T, D, Dv, m, w, dtype, eps, q, k, v, r, u, omega, M, a, rho, ring_r,
@@ -464,10 +540,13 @@ int linsimp_head_fwd(const linsimp_dims* dims, const linsimp_head_opts* opts, co
   head_saved_bytes(s, &hs, saved);
   Workspace ws;
   carve(s, workspace, false, &ws);
+  drop_states(workspace);
   if ((rc = launch_head_prenorm(s, q, k, r, tau, hs.qn, hs.kn, hs.rn, opts->norm_eps, st))) return rc;
   if ((rc = launch_forward(s, hs.qn, hs.kn, v, hs.rn, u, omega, hs.ot, hs.stats, nullptr, nullptr,
                            nullptr, ws, st)))
     return rc;
+  // the core's states are those of the normalised keys in `saved`
+  record_states(workspace, s, hs.kn, v, omega);
   return launch_head_gate(s, hs.ot, gate, opts->gate == LINSIMP_GATE_CHANNEL, y, hs.rho,
                           opts->rms_eps, st);
 }
@@ -503,8 +582,10 @@ int linsimp_head_bwd_ex(const linsimp_dims* dims, const linsimp_head_opts* opts,
   if ((rc = check_buf("workspace", workspace, workspace_bytes_, head_ws_bytes(s, true)))) return rc;
   hipStream_t st = (hipStream_t)stream;
   const bool channel = opts->gate == LINSIMP_GATE_CHANNEL;
+  const bool reuse = flags == LINSIMP_BWD_REUSE_STATES;
   HeadSaved hs;
   head_saved_bytes(s, &hs, (void*)saved);
+  if (reuse && (rc = check_states(workspace, s, hs.kn, v, omega))) return rc;
   Workspace ws;
   carve(s, workspace, true, &ws);
   const size_t rows = (size_t)s.BH() * s.n;
@@ -516,8 +597,11 @@ int linsimp_head_bwd_ex(const linsimp_dims* dims, const linsimp_head_opts* opts,
   // core gradients with respect to q', k', r' land in dq, dk, dr and are
   // turned into gradients with respect to q, k, r in place
   if ((rc = launch_backward(s, hs.qn, hs.kn, v, hs.rn, u, omega, hs.ot, hs.stats, dot, dq, dk, dv, dr,
-                            du, ws, st, flags == LINSIMP_BWD_REUSE_STATES)))
+                            du, ws, st, reuse))) {
+    drop_states(workspace);
     return rc;
+  }
+  if (!reuse) record_states(workspace, s, hs.kn, v, omega);
   if ((rc = launch_head_prenorm_bwd(s, q, k, r, tau, dq, dk, dr, part_t, opts->norm_eps, st))) return rc;
   if ((rc = launch_head_reduce(s, part_t, dtau, st))) return rc;
   if (!channel && (rc = launch_head_reduce(s, part_g, (float*)dgate, st))) return rc;
@@ -551,6 +635,6 @@ int linsimp_feature_bank(int32_t H, int32_t m, int32_t D, const float* gauss, co
 
 const char* linsimp_last_error(void) { return g_err; }
 
-int linsimp_version(void) { return 102; }
+int linsimp_version(void) { return 103; }
 
 }  // extern "C"

@@ -608,6 +608,8 @@ __global__ __launch_bounds__(256) void k_decode_advance(int64_t* pos, int64_t S,
 
 template <typename T, int D, int DV, int M, int NA>
 static int run_decode(int64_t S, DecArgs a, int ntok, hipStream_t st) {
+  // the caller bounds S*H by kMaxDecodeGroups (one workgroup each)
+  hipGetLastError();                                   // an earlier call's error is not this one's
   if (ntok == 1) {
     ProfScope ps("decode", st);
     k_decode<T, D, DV, M, NA><<<(unsigned)(S * a.H), 256, 0, st>>>(a);
@@ -615,10 +617,15 @@ static int run_decode(int64_t S, DecArgs a, int ntok, hipStream_t st) {
     ProfScope ps("decode_chunk", st);
     k_decode_chunk<T, D, DV, M, NA><<<(unsigned)(S * a.H), 256, 0, st>>>(a, ntok);
   }
-  k_decode_advance<<<(unsigned)((S + 255) / 256), 256, 0, st>>>(a.pos, S, ntok);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) {
+  if (e != hipSuccess) {                               // pos must not advance past a step not taken
     set_error("decode launch failed: %s", hipGetErrorString(e));
+    return -4;
+  }
+  k_decode_advance<<<(unsigned)((S + 255) / 256), 256, 0, st>>>(a.pos, S, ntok);
+  e = hipGetLastError();
+  if (e != hipSuccess) {
+    set_error("decode position update launch failed: %s", hipGetErrorString(e));
     return -4;
   }
   return 0;

@@ -90,6 +90,10 @@ int launch_head_reduce(const Shape& s, const float* part, float* out, hipStream_
 int launch_feature_bank(int H, int m, int D, const float* gauss, const float* radii, float* omega,
                         int sign_correct, hipStream_t st);
 
+// (sequence, head) pairs of one decode call: one 256-thread workgroup each on
+// a one-dimensional grid (fewer than 2^32 threads)
+constexpr int64_t kMaxDecodeGroups = ((int64_t)1 << 24) - 1;
+
 void set_error(const char* fmt, ...);
 bool shape_supported(const Shape& s, bool backward);
 

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
         assert set(names) == set(exports), header
         for name in names:
             assert hasattr(lib, name), name
-    assert lib.linsimp_version() == 102
+    assert lib.linsimp_version() == 103
 
 
 def test_head_sizes_and_argument_errors():
@@ -95,6 +95,39 @@ def test_argument_errors_are_reported_not_raised():
     rc = lib.linsimp_decode_step(4, 2, 32, 32, 32, 0, L.BF16, 1e-30,
                                  *[vp(4096 * (i + 1)) for i in range(13)], vp(0))
     assert rc == -1
+
+
+def test_reuse_flag_without_a_matching_forward_is_refused():
+    """LINSIMP_BWD_REUSE_STATES is accepted only for a workspace a forward with
+    the same dims, k, v and omega left its states in (a host-side record); a
+    workspace no forward has used is refused before anything is launched."""
+    lib = L.lib()
+    vp = ctypes.c_void_p
+    d = L.make_dims(1, 1, 64, 32, 32, 32, 8, L.F32)
+    need = L.workspace_size(d, True)
+    ptrs = [vp(4096 * (i + 1)) for i in range(14)]
+    rc = lib.linsimp_bwd_ex(ctypes.byref(d), *ptrs, L.BWD_REUSE_STATES, vp(1 << 24), need, vp(0))
+    assert rc == -1 and b"no forward" in lib.linsimp_last_error()
+    # the head entry point checks the same record
+    o = L.head_opts(L.GATE_HEAD)
+    hw = lib.linsimp_head_workspace_size(ctypes.byref(d), 1)
+    hp = [vp(4096 * (i + 1)) for i in range(17)]
+    hp[10] = vp(1 << 22)                         # saved: 256-byte aligned
+    rc = lib.linsimp_head_bwd_ex(ctypes.byref(d), ctypes.byref(o), *hp, L.BWD_REUSE_STATES,
+                                 vp(1 << 24), hw, vp(0))
+    assert rc == -1 and b"no forward" in lib.linsimp_last_error()
+
+
+def test_decode_grid_bound_is_an_error():
+    """One workgroup per (sequence, head): S*H above 2^24 - 1 is refused
+    (LINSIMP_E_UNSUPPORTED) before any launch."""
+    lib = L.lib()
+    vp = ctypes.c_void_p
+    ptrs = [vp(4096 * (i + 1)) for i in range(13)]
+    rc = lib.linsimp_decode_step(1 << 20, 16, 32, 32, 32, 8, L.BF16, 1e-30, *ptrs, vp(0))
+    assert rc == -2 and b"at most" in lib.linsimp_last_error()
+    rc = lib.linsimp_decode_chunk(1 << 20, 16, 2, 32, 32, 32, 8, L.BF16, 1e-30, *ptrs, vp(0))
+    assert rc == -2
 
 
 def test_binding_refuses_cpu_tensors():

@@ -1,7 +1,8 @@
 """GPU parity of the forward pass against the float64 oracle (through the C ABI).
 
 Bars: relative L2 <= 1e-4 for float32 inputs, <= 2e-2 for bf16 inputs with a
-float32 state, per output tensor; the per-row worst case is printed.
+float32 state, per output tensor; and per row (relative L2 of each output row)
+<= 1e-4 for float32 and <= 5e-2 for bf16 inputs.
 """
 
 import numpy as np
@@ -12,7 +13,7 @@ from oracle import linsimp as O
 from paper_2608_09307_amd import linsimp as L
 from paper_2608_09307_amd.workloads import WORKLOADS, Workload, make_inputs
 
-from helpers import f64, oracle_forward, rel_l2, row_max_rel
+from helpers import ROW_TOL, f64, oracle_forward, rel_l2, row_max_rel
 
 pytestmark = pytest.mark.gpu
 
@@ -31,9 +32,11 @@ def _run_and_compare(wl: Workload, pairs=None, tol=None):
     got = np.stack([f64(out[b, h]) for b, h in pairs])
     exp = np.stack([ref[p] for p in pairs])
     err = rel_l2(got, exp)
-    print(f"      rel_l2={err:.3e} row_max={row_max_rel(got, exp):.3e}", flush=True)
+    rmax = row_max_rel(got, exp)
+    print(f"      rel_l2={err:.3e} row_max={rmax:.3e}", flush=True)
     assert np.all(np.isfinite(got))
     assert err <= (tol if tol is not None else TOL[wl.dtype]), err
+    assert rmax <= ROW_TOL[wl.dtype], rmax
     return x, out, stats
 
 
@@ -68,7 +71,7 @@ def test_bf16_shapes_reduced_n(D, m, n, w):
 
 def test_layer16k_bf16_sampled_heads():
     wl = WORKLOADS["layer16k_bf16"]
-    _run_and_compare(wl, pairs=[(0, 3), (1, 14)])
+    _run_and_compare(wl, pairs=[(0, 3), (1, 14), (1, 0)])
 
 
 def test_stress64k_m256_sampled_head():

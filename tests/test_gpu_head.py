@@ -3,7 +3,8 @@ RMSNorm; per-head and channel-wise gates) against the float64 oracle of
 oracle.layer, through the C ABI (include/linsimp_head.h).
 
 Outputs and the gradients of q, k, v, r, u and of the channel-gate logits are
-held to relative L2 <= 1e-4 (float32) and <= 2e-2 (bf16); a gradient that is
+held to relative L2 <= 1e-4 (float32) and <= 2e-2 (bf16), the output and the
+five stream gradients also per row (<= 1e-4 float32, <= 5e-2 bf16); a gradient that is
 zero by definition (n = 1; reference norm below 1e-6 of the largest of the
 five) is measured against the largest reference gradient norm.  The per-head sums
 dtau = <q_hat, dq_core> and dgamma = <dy, o_hat g (1 - g)> are inner products
@@ -20,7 +21,7 @@ from oracle import layer as LY
 from paper_2608_09307_amd import linsimp as L
 from paper_2608_09307_amd.workloads import Workload, make_head_params, make_inputs
 
-from helpers import f64, rel_l2
+from helpers import ROW_TOL, f64, rel_l2, row_max_rel
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -71,14 +72,19 @@ def _run(wl: Workload, channel: bool, zero_rows: bool = False, pairs=None):
     heads = sorted({h for _, h in pairs})
     ys, ref, scale = _oracle(x, p, wl, pairs, channel)
     tol = TOL[wl.dtype]
-    errs = {"y": rel_l2(np.stack([f64(y[b, h]) for b, h in pairs]), np.stack([ys[q] for q in pairs]))}
+    ygot, yref = np.stack([f64(y[b, h]) for b, h in pairs]), np.stack([ys[q] for q in pairs])
+    errs = {"y": rel_l2(ygot, yref)}
+    rows = {"y": row_max_rel(ygot, yref)}
     exps = [np.stack([ref[q][gi] for q in pairs]) for gi in range(len(NAMES))]
     big = max(np.linalg.norm(e) for e in exps)
     for gi, nm in enumerate(NAMES):
         got = np.stack([f64(g[gi][b, h]) for b, h in pairs])
         assert np.all(np.isfinite(got)), nm
         nr = np.linalg.norm(exps[gi])
-        errs[nm] = float(np.linalg.norm(got - exps[gi]) / (nr if nr > 1e-6 * big else big))
+        zero = nr <= 1e-6 * big
+        errs[nm] = float(np.linalg.norm(got - exps[gi]) / (big if zero else nr))
+        nrows = exps[gi].size // exps[gi].shape[-1]
+        rows[nm] = row_max_rel(got, exps[gi], scale=big / np.sqrt(nrows) if zero else None)
     dtau_ref = np.zeros(wl.H)
     for (b, h) in pairs:
         dtau_ref[h] += ref[(b, h)][5]
@@ -94,8 +100,11 @@ def _run(wl: Workload, channel: bool, zero_rows: bool = False, pairs=None):
         cs = _cs_scale(scale, pairs, wl.H, "dy", "gate_factor", big)
         errs["dgamma"] = float(np.max((np.abs(g[6].cpu().double().numpy() - dg_ref) / np.maximum(cs, 1e-300))[heads]))
     print("      " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()), flush=True)
+    print("      rows " + " ".join(f"{k}={v:.2e}" for k, v in rows.items()), flush=True)
     for nm, e in errs.items():
         assert e <= tol, (nm, e)
+    for nm, e in rows.items():
+        assert e <= ROW_TOL[wl.dtype], (nm, "row", e)
     return x, p, y, saved, g
 
 
