@@ -22,13 +22,16 @@ the paper times); the default line is the 16k layer.
 With --decode the line is the autoregressive path instead (256 sequences x
 16 heads, d = m = 128, w = 64, after an 8192-token prefix): decode steps per
 second over all sequences, the decode kernel against the HBM peak, and the
-prefill and 16-token chunked decode times.
+prefill and 16-token chunked decode times.  The default line carries the same
+measurements as its `decode` object, taken in the same run after the timed
+forward + backward steps (--no-decode leaves them out).
 
 Prints one JSON line.  `value` is tokens/s (B*n per step time).  `roofline`
 reports the dominant kernel (largest share of the timed region) against the
 bf16 matrix-core peak, from HIP events recorded around every library kernel
 on its stream during the timed steps.  `cpu_baseline` times the float64 oracle
-on host cores on a causal prefix of one (batch, head) sequence.
+on host cores on a causal prefix of one (batch, head) sequence, and in `extra`
+on the single f32 head, the 2k-token layer's forward and the decode step.
 """
 
 from __future__ import annotations
@@ -84,9 +87,11 @@ def decode_step_bytes(wl, es=2):
     return wl.B * wl.H * per
 
 
-def run_decode(args, torch, L, dev):
-    """Decode-mode line: prefill once, then timed single decode steps and one
-    timed 16-token chunked call, all on the default stream."""
+def measure_decode(steps, warmup, torch, L, dev):
+    """The autoregressive path at 256 sequences x 16 heads after an
+    8192-token prefix: one timed prefill, `steps` timed single decode steps
+    (after `warmup` untimed ones) and one timed 16-token chunked call, all on
+    the current stream.  Returns the measurements as a dict."""
     from paper_2608_09307_amd.workloads import WORKLOADS, make_decode_inputs
     wl = WORKLOADS["decode_s256_h16"]
     x = make_decode_inputs(wl, device=dev)
@@ -98,13 +103,13 @@ def run_decode(args, torch, L, dev):
     ev[0].record(stream)
     st = L.prefill(pre["k"], pre["v"], pre["r"], pre["u"], x["omega"], wl.w)
     ev[1].record(stream)
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         L.decode_step(st, tok["q"], tok["k"], tok["v"], tok["r"], tok["u"], x["omega"], wl.w)
     torch.cuda.synchronize()
     L.timing_enable(True)
     L.timing_read()
     ev[2].record(stream)
-    for _ in range(args.steps):
+    for _ in range(steps):
         L.decode_step(st, tok["q"], tok["k"], tok["v"], tok["r"], tok["u"], x["omega"], wl.w)
     ev[3].record(stream)
     torch.cuda.synchronize()
@@ -119,7 +124,7 @@ def run_decode(args, torch, L, dev):
     L.decode_chunk(st, *(chunk[nm] for nm in ("q", "k", "v", "r", "u")), x["omega"], wl.w)
     ev[5].record(stream)
     torch.cuda.synchronize()
-    ms = ev[2].elapsed_time(ev[3]) / args.steps
+    ms = ev[2].elapsed_time(ev[3]) / steps
     chunk_ms = ev[4].elapsed_time(ev[5])
     roofline = None
     if "decode" in kt:
@@ -129,25 +134,34 @@ def run_decode(args, torch, L, dev):
                     "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": traffic_for("decode", DECODE_TRAFFIC_FILE),
                     "kernel": "decode",
                     "avg_ms": round(avg_ms, 4), "bytes": decode_step_bytes(wl)}
-    line = {
+    del x, pre, tok, st, chunk
+    return {
         "metric": "LinSimp decode tokens/s (256 sequences x 16 heads, 8192-token prefix)",
         "value": round(wl.B / (ms * 1e-3), 1),
         "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": warmup,
         "ms_per_step": round(ms, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded N(0,1)*d^-1/4 prefix and tokens, N(0,1) feature bank)",
         "config": {"workload": "decode_s256_h16", "S": wl.B, "H": wl.H, "prefix": wl.n_prefix,
                    "d": wl.D, "m": wl.m, "w": wl.w},
         "roofline": roofline,
         "prefill_ms": round(ev[0].elapsed_time(ev[1]), 3),
         "chunk16": {"ms_per_call": round(chunk_ms, 4), "us_per_token_step": round(chunk_ms * 1e3 / T, 2),
                     "tokens_per_s": round(wl.B * T / (chunk_ms * 1e-3), 1)},
+    }
+
+
+def run_decode(args, torch, L, dev):
+    """Decode-mode line (--decode): the measurements of measure_decode as the
+    line itself."""
+    m = measure_decode(args.steps, args.warmup, torch, L, dev)
+    line = {
+        "metric": m["metric"], "value": m["value"], "unit": m["unit"], "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": m["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1)*d^-1/4 prefix and tokens, N(0,1) feature bank)",
+        "config": m["config"], "roofline": m["roofline"], "prefill_ms": m["prefill_ms"],
+        "chunk16": m["chunk16"],
     }
     print(json.dumps(line), flush=True)
 
@@ -209,17 +223,44 @@ def traffic_for(kernel, path=TRAFFIC_FILE):
     return per["fetch_bytes"] + per["write_bytes"]
 
 
-def cpu_baseline(x, wl, budget_s):
-    """Time the float64 oracle (forward + backward) on host cores on the first
-    rows of one (batch, head) sequence: rows are causal, so a prefix is a
-    complete sub-problem.  Scaled to the full job: tokens/s = rows/s / H."""
-    import numpy as np
-    from oracle import linsimp as O
+def host_info():
+    """Host cores this process may run on, BLAS threads and the CPU model."""
+    cores = len(os.sched_getaffinity(0))
+    blas = None
     try:
         from threadpoolctl import threadpool_info
-        cores = max([int(p.get("num_threads", 1)) for p in threadpool_info()] or [1])
+        blas = max([int(p.get("num_threads", 1)) for p in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
-        cores = os.cpu_count() or 1
+        pass
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
+    return cores, blas, model
+
+
+def cpu_baseline(x, wl, budget_s, dev):
+    """Time the float64 oracle on host cores.  The headline value: forward +
+    backward on the first rows of one (batch, head) sequence of the step's
+    workload (rows are causal, so a prefix is a complete sub-problem), scaled
+    to the full job as tokens/s = rows/s / H.  `extra` times the oracle on the
+    other workloads: the single f32 head in full, the 2k-token layer's
+    forward on two of its 32 (batch, head) pairs, and the decode step on 32
+    of the 4096 (sequence, head) pairs of the 256 x 16 decode workload (state
+    prefilled by the oracle outside the timed region), each scaled to its
+    whole job.  Inputs come from the seeded generators on `dev` (the values
+    the GPU path is measured on); only the sampled slices are copied to the
+    host."""
+    import numpy as np
+    from oracle import linsimp as O
+    from paper_2608_09307_amd.workloads import WORKLOADS, make_decode_inputs, make_inputs
+
+    cores, blas, model = host_info()
 
     def f64(t):
         return t.detach().float().cpu().double().numpy()
@@ -240,10 +281,54 @@ def cpu_baseline(x, wl, budget_s):
     rows = max(cal_rows, rows)
     t = run(rows) if rows != cal_rows else t_cal
     rate = rows / t / wl.H
+    extra = {}
+    # the single f32 head (1 x 1 x 256, d = m = 32), forward, in full
+    w1 = WORKLOADS["head_f32_n256"]
+    x1 = make_inputs(w1, device=dev)
+    a1 = [f64(x1[nm][0, 0]) for nm in ("q", "k", "v", "r", "u")] + [f64(x1["omega"][0])]
+    t0 = time.perf_counter()
+    O.forward_recurrent(*a1, w1.w)
+    t1 = time.perf_counter() - t0
+    extra["head_f32_n256_fwd"] = {"value": round(w1.n / t1, 1), "unit": "tokens/s",
+                                  "sample": f"the whole workload ({w1.n} rows) in {t1:.3f} s"}
+    # the 2k-token layer forward (4 x 8 x 2048, d = m = 64) on two (batch, head) pairs
+    w2 = WORKLOADS["layer2k_bf16"]
+    x2 = make_inputs(w2, device=dev)
+    t0 = time.perf_counter()
+    for bb, hh in ((0, 0), (3, 7)):
+        O.forward_recurrent(*(f64(x2[nm][bb, hh]) for nm in ("q", "k", "v", "r", "u")),
+                            f64(x2["omega"][hh]), w2.w)
+    t2 = time.perf_counter() - t0
+    extra["layer2k_bf16_fwd"] = {
+        "value": round(2 * w2.n / t2 / w2.H, 1), "unit": "tokens/s",
+        "sample": (f"forward of 2 of the {w2.B * w2.H} (batch, head) pairs in {t2:.2f} s; "
+                   f"full-job tokens/s = rows/s / H (H={w2.H})")}
+    # the decode step (256 x 16 after 8192 tokens) on 32 (sequence, head) pairs
+    w4 = WORKLOADS["decode_s256_h16"]
+    x4 = make_decode_inputs(w4, device=dev)
+    pre, tok = x4["prefix"], x4["token"]
+    picks = [(7 * j % w4.B, j % w4.H) for j in range(32)]
+    states = [O.prefill_state(*(f64(pre[nm][s_, h_]) for nm in ("k", "v", "r", "u")),
+                              f64(x4["omega"][h_]), w4.w) for s_, h_ in picks]
+    toks = [[f64(tok[nm][s_, h_]) for nm in ("q", "k", "v", "r", "u")] for s_, h_ in picks]
+    oms = [f64(x4["omega"][h_]) for _, h_ in picks]
+    t0 = time.perf_counter()
+    for st_, tk, om4 in zip(states, toks, oms):
+        O.decode_step(st_, *tk, om4, w4.w)
+    t4 = time.perf_counter() - t0
+    del x4, pre, tok
+    pairs = w4.B * w4.H
+    extra["decode_s256_h16_step"] = {
+        "value": round(w4.B / (t4 * pairs / len(picks)), 2), "unit": "tokens/s",
+        "sample": (f"one decode step of {len(picks)} of the {pairs} (sequence, head) pairs in "
+                   f"{t4 * 1e3:.1f} ms (prefill excluded); a whole step over all pairs scaled "
+                   f"as {pairs}/{len(picks)} times that; tokens/s = sequences / step time")}
     return {"value": rate, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "blas_threads": blas, "cpu_model": model,
             "sample": (f"float64 oracle forward+backward of the first {rows} rows of one "
                        f"(batch, head) of the {wl.n}-token layer in {t:.1f} s; full-job "
-                       f"tokens/s = rows/s / H (H={wl.H})")}
+                       f"tokens/s = rows/s / H (H={wl.H})"),
+            "extra": extra}
 
 
 def copy_calibration(torch, dev, nbytes=1 << 30, reps=3):
@@ -271,6 +356,8 @@ def main():
                     help="time the full head (normalisation, core, gated RMSNorm) instead of the core")
     ap.add_argument("--decode", action="store_true",
                     help="time prefill, decode steps and chunked decode (256 x 16 sequences)")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="leave the decode measurement out of the forward + backward line")
     ap.add_argument("--workload", default=WORKLOAD,
                     help="forward + backward workload of the step (default: the 16k layer); "
                          "e.g. stress64k_m256 or layer2k_h6_d64_m128")
@@ -393,8 +480,14 @@ def main():
     }
     if head_streams is not None:
         line["head_streams"] = head_streams
+    if not args.no_decode and not args.head and args.workload == WORKLOAD:
+        # the HBM-bound path, measured in the same run after the timed steps
+        del x, ws_b, out, stats, grads
+        torch.cuda.empty_cache()
+        line["decode"] = measure_decode(args.steps, args.warmup, torch, L, dev)
+        x = make_inputs(wl, device=dev, with_grad=True) if not args.no_cpu_baseline else None
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(x, wl, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(x, wl, args.cpu_seconds, dev)
     print(json.dumps(line), flush=True)
 
 

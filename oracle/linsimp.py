@@ -256,7 +256,7 @@ def exact_window(q, k, v, r, u, w):
 # Backward: exact gradient of sum_i dO_i . o~_i
 # ---------------------------------------------------------------------------
 
-def backward(q, k, v, r, u, Omega, w, dO, eps=EPS):
+def backward(q, k, v, r, u, Omega, w, dO, eps=EPS, term_scale=None):
     """Exact gradient of L = sum_i dO_i . o~_i w.r.t. q, k, v, r, u.
 
     Follows the two sweeps of App. C ("Backward query sweep", "Backward
@@ -277,6 +277,12 @@ def backward(q, k, v, r, u, Omega, w, dO, eps=EPS):
     The rows are swept from the end of the sequence to the start, so G and h
     are running sums; the prefix state M_i is rebuilt on the way back by
     removing chi_i v_i^T (the recurrence run in reverse).
+
+    If ``term_scale`` is a dict, its entry "dk" receives, per key j, the norm
+    of the same sums taken over absolute values (|dA|, |dZ|, |v_j|, |Omega|,
+    |k_j|): the first-order bound on what a relative perturbation u of every
+    summed term can change in dk_j is u times that scale.  It does not change
+    the gradients.
     """
     q, k, v, r, u, Omega, dO = _f64(q, k, v, r, u, Omega, dO)
     n, D = q.shape
@@ -292,6 +298,8 @@ def backward(q, k, v, r, u, Omega, w, dO, eps=EPS):
     du = np.zeros_like(u)
     G = np.zeros((m, Dv))
     h = np.zeros(m)
+    if term_scale is not None:
+        Ga, ha, Tk = np.zeros((m, Dv)), np.zeros(m), np.zeros(n)
     for i in range(n - 1, -1, -1):
         C = anchor_window(i, w)
         z = composite_query(q[i], r[C])              # [|C|, D]
@@ -316,9 +324,16 @@ def backward(q, k, v, r, u, Omega, w, dO, eps=EPS):
         dv[i] += G.T @ chi[i]
         dlam = dchi * chi[i]
         dk[i] = dlam @ Omega - dlam.sum() * k[i]
+        if term_scale is not None:
+            Ga += F.T @ np.abs(dA)
+            ha += abs(dZ) * F.sum(axis=0)
+            t = (Ga @ np.abs(v[i]) + ha) * chi[i]
+            Tk[i] = np.linalg.norm(t @ np.abs(Omega) + t.sum() * np.abs(k[i]))
         # rebuild M_{i-1}, a_{i-1}
         M = M - np.outer(chi[i], v[i])
         a = a - chi[i]
+    if term_scale is not None:
+        term_scale["dk"] = Tk
     return dq, dk, dv, dr, du
 
 

@@ -1041,14 +1041,17 @@ __global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
       for (int g = 0; g < 4; ++g) {
         const f32x4 b4 = *(const f32x4*)(brow + 8 * g);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float x = fast_exp2(acc[an][4 * g + e] + b4[e]);
-          acc[an][4 * g + e] = x;
-          ps += x;
-        }
+        for (int e = 0; e < 4; ++e) acc[an][4 * g + e] = fast_exp2(acc[an][4 * g + e] + b4[e]);
       }
+      // f sums the features exactly as rounded for F's matrix product: the two
+      // cancel in dchi = F v + f (the output is a ratio), and a rounding in
+      // one of them only would be amplified by that cancellation
 #pragma unroll
-      for (int sp = 0; sp < F::CSTEPS; ++sp) pf[an][sp] = F::cfrag(acc[an], sp);
+      for (int sp = 0; sp < F::CSTEPS; ++sp) {
+        pf[an][sp] = F::cfrag(acc[an], sp);
+#pragma unroll
+        for (int e = 0; e < F::KPL; ++e) ps += fel(pf[an][sp], e);
+      }
     }
     if (fr != 1.0f) {
       fpart *= fr;
@@ -1268,9 +1271,8 @@ __global__ __launch_bounds__(512) void k_bwd_keys(BwdArgs a, int nfb) {
       for (int e = 0; e < 4; ++e) {
         const float c = vt ? ch[e] : 0.0f;
         const float dc = vt ? eps_j * (X[4 * g + e] + gh[e]) + di[e] : 0.0f;
-        const float dl = dc * c;
-        sk += dl;
-        dl4[e] = (T)(dl * kLn2);                      // paired with Omega * log2(e)
+        dl4[e] = (T)(dc * c * kLn2);                  // paired with Omega * log2(e)
+        sk += tof(dl4[e]) * kLog2e;                   // the rounded value the product uses
         ce4[e] = (T)(c * eps_j);
       }
       // natural feature order in LDS (the phase-2 operands read rows j, k = p)

@@ -2,8 +2,15 @@
 
 Each gradient (dq, dk, dv, dr, du) is held to relative L2 <= 1e-4 for float32
 inputs and <= 2e-2 for bf16 inputs, and every gradient row to its own relative
-L2 bar (1e-4 for float32, 5e-2 for bf16; a row far below the tensor's RMS row
-norm is measured against 1% of that RMS).  A gradient that is exactly zero in the
+L2 bar (1e-4 for float32, 5e-2 for bf16), measured against the larger of its
+own norm and the RMS norm of the rows within w positions (helpers.row_max_rel:
+dq of a sequence's first row is zero by definition, and the bf16 output the
+backward receives leaves a rounding residue there of the size of its
+neighbours' rounding).  dk rows also get the first-order rounding bound of
+their terms as slack (two bf16 unit roundoffs times the absolute term sum,
+oracle.linsimp.backward's term_scale): a key whose exact gradient cancels
+between much larger terms carries their rounding.  A gradient that is
+exactly zero in the
 definition (n = 1: the output is v_0 (*) u_0 whatever q, k, r are; its
 reference norm is below 1e-6 of the largest of the five) has no relative
 scale; its error is measured against the largest reference gradient norm,
@@ -20,7 +27,7 @@ import torch
 from paper_2608_09307_amd import linsimp as L
 from paper_2608_09307_amd.workloads import WORKLOADS, Workload, make_inputs
 
-from helpers import ROW_TOL, f64, oracle_backward, rel_l2, row_max_rel
+from helpers import ROW_TOL, UNIT_ROUNDOFF, f64, oracle_backward, rel_l2, row_max_rel
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -36,7 +43,13 @@ def _run(wl: Workload, pairs=None):
     torch.cuda.synchronize()
     if pairs is None:
         pairs = [(b, h) for b in range(wl.B) for h in range(wl.H)]
-    ref = oracle_backward(x, wl.w, pairs)
+    tscale = {}
+    ref = oracle_backward(x, wl.w, pairs, scales=tscale)
+    # dk of a key whose exact gradient cancels between much larger terms (a
+    # dominant feature fed by many (row, anchor) pairs of both signs) carries
+    # the rounding of those terms: two unit roundoffs of their absolute sum
+    # are allowed on top of the row bar
+    slack_dk = 2 * UNIT_ROUNDOFF[wl.dtype] * np.stack([tscale[p] for p in pairs])
     errs, rows = {}, {}
     exps = [np.stack([ref[p][gi] for p in pairs]) for gi in range(len(NAMES))]
     big = max(np.linalg.norm(e) for e in exps)
@@ -47,8 +60,12 @@ def _run(wl: Workload, pairs=None):
         zero = np.linalg.norm(exp) <= 1e-6 * big      # zero by definition (n = 1)
         den = big if zero else np.linalg.norm(exp)
         errs[nm] = float(np.linalg.norm(got - exp) / den)
-        nrows = exp.size // exp.shape[-1]
-        rows[nm] = row_max_rel(got, exp, scale=big / np.sqrt(nrows) if zero else None)
+        if not zero:                                   # (a zero tensor has no row scale)
+            slack = slack_dk if nm == "dk" else None
+            rows[nm] = row_max_rel(got, exp, slack=slack)
+            if rows[nm] > ROW_TOL[wl.dtype]:
+                print(f"      worst {nm} row (value, seq, row, err, norm, local):",
+                      row_max_rel(got, exp, where=True, slack=slack), flush=True)
     print("      " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()), flush=True)
     print("      rows " + " ".join(f"{k}={v:.2e}" for k, v in rows.items()), flush=True)
     for nm, e in errs.items():

@@ -4,7 +4,9 @@ oracle.layer, through the C ABI (include/linsimp_head.h).
 
 Outputs and the gradients of q, k, v, r, u and of the channel-gate logits are
 held to relative L2 <= 1e-4 (float32) and <= 2e-2 (bf16), the output and the
-five stream gradients also per row (<= 1e-4 float32, <= 5e-2 bf16); a gradient that is
+five stream gradients also per row (<= 1e-4 float32, <= 5e-2 bf16, each row
+against the larger of its own norm and the RMS norm of the rows within w
+positions, helpers.row_max_rel); a gradient that is
 zero by definition (n = 1; reference norm below 1e-6 of the largest of the
 five) is measured against the largest reference gradient norm.  The per-head sums
 dtau = <q_hat, dq_core> and dgamma = <dy, o_hat g (1 - g)> are inner products
@@ -83,8 +85,8 @@ def _run(wl: Workload, channel: bool, zero_rows: bool = False, pairs=None):
         nr = np.linalg.norm(exps[gi])
         zero = nr <= 1e-6 * big
         errs[nm] = float(np.linalg.norm(got - exps[gi]) / (big if zero else nr))
-        nrows = exps[gi].size // exps[gi].shape[-1]
-        rows[nm] = row_max_rel(got, exps[gi], scale=big / np.sqrt(nrows) if zero else None)
+        if not zero:                                   # (a zero tensor has no row scale)
+            rows[nm] = row_max_rel(got, exps[gi])
     dtau_ref = np.zeros(wl.H)
     for (b, h) in pairs:
         dtau_ref[h] += ref[(b, h)][5]

@@ -450,3 +450,44 @@ def test_sign_fix_gives_the_inverse_sqrt_m_trend():
     # one at large m and drops by much less than 16x over a 256x range
     assert raw[-1] > 4 * fixed[-1], (raw, fixed)
     assert raw[0] / raw[-1] < 4, raw
+
+
+def test_backward_dk_term_scale_bounds_relative_perturbations():
+    """oracle.linsimp.backward's term_scale (the per-key scale of dk's summed
+    terms taken in absolute value) leaves the gradients unchanged, is at
+    least |dk_j|, and bounds the first-order change of dk_j when every query
+    feature phi(z_ic)_p entering the state gradient is scaled by (1 + delta)
+    with |delta| <= u (what a rounding of those features does)."""
+    rng = np.random.default_rng(91)
+    n, D, Dv, m, w = 30, 6, 5, 12, 7
+    q, k, v, r, u, Om = _inputs(92, n, D, Dv, m)
+    dO = rng.standard_normal((n, Dv))
+    plain = O.backward(q, k, v, r, u, Om, w, dO)
+    ts = {}
+    g = O.backward(q, k, v, r, u, Om, w, dO, term_scale=ts)
+    assert all(np.array_equal(a, b) for a, b in zip(plain, g))
+    T = ts["dk"]
+    assert np.all(T >= np.linalg.norm(g[1], axis=1) * (1 - 1e-12))
+    # perturbed state gradient: dM_i = sum_c F_ic (1 + delta) dA_ic, da_i likewise
+    uu = 1e-6
+    chi = O.phi(k, Om)
+    worst = 0.0
+    for trial in range(3):
+        G, h = np.zeros((m, Dv)), np.zeros(m)
+        M, a = chi.T @ v, chi.sum(axis=0)
+        dk = np.zeros_like(k)
+        for i in range(n - 1, -1, -1):
+            C = O.anchor_window(i, w)
+            F = O.phi(O.composite_query(q[i], r[C]), Om)
+            Z = np.sum(F @ a)
+            o = np.sum((F @ M) * u[C], axis=0) / Z
+            dN, dZ = dO[i] / Z, -np.dot(dO[i], o) / Z
+            Fp = F * (1 + uu * rng.uniform(-1, 1, F.shape))
+            G += Fp.T @ (dN[None, :] * u[C])
+            h += dZ * Fp.sum(axis=0)
+            dlam = (G @ v[i] + h) * chi[i]
+            dk[i] = dlam @ Om - dlam.sum() * k[i]
+            M, a = M - np.outer(chi[i], v[i]), a - chi[i]
+        worst = max(worst, float(np.max(np.linalg.norm(dk - g[1], axis=1) / (uu * T))))
+    assert worst <= 1.0 + 1e-6, worst
+    assert worst > 1e-3, worst          # the bound is not vacuous
