@@ -97,6 +97,25 @@ int linsimp_fwd(const linsimp_dims* dims, const void* q, const void* k, const vo
                 const void* r, const void* u, const float* omega, void* out, float* stats,
                 void* workspace, size_t workspace_bytes, void* stream);
 
+/* linsimp_fwd for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same forward, with its scratch taken from a static array inside the library
+ * instead of a caller workspace.  It calls no hipMalloc, hipFree or other
+ * allocating routine; each GPU holds one such array of
+ * LINSIMP_FWD_STATIC_MAX_BYTES from the library's load on that GPU until the
+ * process ends.  Dims whose forward workspace (linsimp_workspace_size(dims, 0))
+ * exceeds it return LINSIMP_E_WORKSPACE without launching anything.  The
+ * array belongs to the current device, so `stream` must be a stream of that
+ * device.  Every call on a GPU uses the same array: calls that overlap on one
+ * GPU (on different streams or host threads) race and give undefined results;
+ * calls ordered on one stream are safe.  Nothing in the array needs clearing
+ * between calls (every byte the forward reads it first writes).  Arguments,
+ * results and bits are those of linsimp_fwd. */
+#define LINSIMP_FWD_STATIC_MAX_BYTES (64u << 20)
+int linsimp_fwd_static(const linsimp_dims* dims, const void* q, const void* k, const void* v,
+                       const void* r, const void* u, const float* omega, void* out, float* stats,
+                       void* stream);
+
 /* Backward pass: exact gradient of sum_i dout_i . out_i with respect to q, k,
  * v, r, u, with the stabilising shifts treated as constants (they cancel in
  * the ratio, App. B.2); App. C "Backward query sweep" / "Backward state sweep".

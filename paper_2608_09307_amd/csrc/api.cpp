@@ -432,6 +432,74 @@ int linsimp_timing_read(char* names, int names_len, float* total_ms, int* counts
   return rc < 0 ? rc : nk;
 }
 
+}  // extern "C"
+
+// ---- forward without a caller workspace (linsimp_fwd_static) ----
+// Its scratch is this file-scope device array: each GPU the library runs on
+// holds one copy, allocated with the code object, until the process ends.  In
+// host code `scratch` names a host-side stand-in, not a device address; the
+// address of the current device's copy comes from hipGetSymbolAddress, once
+// per device with that device current, and only that pointer is handed to
+// kernels.
+static __device__ __align__(256) unsigned char scratch[LINSIMP_FWD_STATIC_MAX_BYTES];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scr_mu;
+void* g_scr_ptr[kMaxScratchDevices] = {};
+
+int current_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) {
+    set_error("fwd_static: no usable current device (%s)", hipGetErrorString(e));
+    return LINSIMP_E_HIP;
+  }
+  std::lock_guard<std::mutex> lk(g_scr_mu);
+  if (g_scr_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr) {
+      set_error("fwd_static: address of the static scratch on device %d: %s", dev, hipGetErrorString(e));
+      return LINSIMP_E_HIP;
+    }
+    g_scr_ptr[dev] = p;
+  }
+  *out = g_scr_ptr[dev];
+  return LINSIMP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int linsimp_fwd_static(const linsimp_dims* dims, const void* q, const void* k, const void* v,
+                       const void* r, const void* u, const float* omega, void* out, float* stats,
+                       void* stream) {
+  Shape s;
+  int rc = check_dims(dims, &s, false);
+  if (rc) return rc;
+  const void* ps[] = {q, k, v, r, u, omega, out};
+  if ((rc = check_ptrs("q,k,v,r,u,omega,out", ps, 7))) return rc;
+  if (stats != nullptr && !aligned16(stats)) {
+    set_error("stats is not 16-byte aligned");
+    return LINSIMP_E_INVALID_ARG;
+  }
+  const size_t need = workspace_bytes(s, false);
+  if (need > (size_t)LINSIMP_FWD_STATIC_MAX_BYTES) {
+    set_error("fwd_static: these dims need %zu bytes of scratch; the static scratch holds %zu "
+              "(use linsimp_fwd with a workspace)", need, (size_t)LINSIMP_FWD_STATIC_MAX_BYTES);
+    return LINSIMP_E_WORKSPACE;
+  }
+  void* base = nullptr;
+  if ((rc = current_scratch(&base))) return rc;
+  Workspace ws;
+  carve(s, base, false, &ws);
+  return launch_forward(s, q, k, v, r, u, omega, out, stats, nullptr, nullptr, nullptr, ws,
+                        (hipStream_t)stream);
+}
+
 // ---- full head (include/linsimp_head.h) ----
 }  // extern "C"
 

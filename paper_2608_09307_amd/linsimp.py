@@ -43,7 +43,8 @@ NORM_EPS, RMS_EPS = 1e-12, 1e-6
 
 BWD_REUSE_STATES = 1
 
-EXPORTS = ("linsimp_workspace_size", "linsimp_fwd", "linsimp_bwd", "linsimp_bwd_ex", "linsimp_prefill",
+EXPORTS = ("linsimp_workspace_size", "linsimp_fwd", "linsimp_fwd_static", "linsimp_bwd", "linsimp_bwd_ex",
+           "linsimp_prefill",
            "linsimp_decode_step", "linsimp_decode_chunk", "linsimp_timing_enable",
            "linsimp_timing_read", "linsimp_last_error", "linsimp_version")
 HEAD_EXPORTS = ("linsimp_head_saved_size", "linsimp_head_workspace_size", "linsimp_head_fwd",
@@ -69,6 +70,8 @@ def lib():
     L.linsimp_workspace_size.restype = sz
     L.linsimp_fwd.argtypes = [pd] + [vp] * 8 + [vp, sz, vp]
     L.linsimp_fwd.restype = ctypes.c_int
+    L.linsimp_fwd_static.argtypes = [pd] + [vp] * 8 + [vp]
+    L.linsimp_fwd_static.restype = ctypes.c_int
     L.linsimp_bwd.argtypes = [pd] + [vp] * 14 + [vp, sz, vp]
     L.linsimp_bwd.restype = ctypes.c_int
     L.linsimp_bwd_ex.argtypes = [pd] + [vp] * 14 + [i32, vp, sz, vp]
@@ -209,6 +212,29 @@ def fwd(q, k, v, r, u, omega, w, eps=EPS, out=None, stats=None, workspace=None,
                              _ptr(r, "r"), _ptr(u, "u"), _ptr(omega, "omega"), _ptr(out, "out"),
                              _ptr(stats, "stats"), _ptr(workspace, "workspace"),
                              workspace.numel(), _stream()))
+    return out, stats
+
+
+FWD_STATIC_MAX_BYTES = 64 << 20      # LINSIMP_FWD_STATIC_MAX_BYTES
+
+
+def fwd_static(q, k, v, r, u, omega, w, eps=EPS, out=None, stats=None, want_stats=True):
+    """Forward pass with the library's static scratch instead of a workspace
+    (linsimp_fwd_static: nothing is allocated by the library; ``out`` and
+    ``stats`` are allocated here unless given); returns (out, stats)."""
+    chk = _layer_inputs(q, k, v, r, u, omega)
+    d = dims_of(q, v, omega, w, eps)
+    if out is None:
+        out = torch.empty(q.shape[:3] + (v.shape[-1],), dtype=q.dtype, device=q.device)
+    if stats is None and want_stats:
+        stats = torch.empty(q.shape[:3] + (2,), dtype=torch.float32, device=q.device)
+    chk.append((out, "out", q.shape[:3] + (v.shape[-1],), q.dtype))
+    if stats is not None:
+        chk.append((stats, "stats", q.shape[:3] + (2,), torch.float32))
+    _expect(chk)
+    _check(lib().linsimp_fwd_static(ctypes.byref(d), _ptr(q, "q"), _ptr(k, "k"), _ptr(v, "v"),
+                                    _ptr(r, "r"), _ptr(u, "u"), _ptr(omega, "omega"), _ptr(out, "out"),
+                                    _ptr(stats, "stats"), _stream()))
     return out, stats
 
 
