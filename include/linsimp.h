@@ -44,8 +44,11 @@
  *     for the last failure on the calling thread.
  *   - Supported shapes: dtype bf16 with (D = Dv, m) in {(32,32), (64,64),
  *     (64,128), (128,64), (128,128), (128,256)}; dtype f32 with D = Dv in
- *     {32, 64} and m in {32, 64}; 1 <= w <= 64; any n >= 1 (tails are masked);
- *     B*H <= 65535 (the decode calls excepted) and B*H*n <= 2^31.
+ *     {32, 64} and m in {32, 64}; 1 <= w <= 64 for every combination, and
+ *     64 < w <= 128 where w * m <= 8192 (the launch rule of App. C
+ *     "Dispatch": m <= 64 here), except f32 with D = m = 64, which stops at
+ *     w = 96; any n >= 1 (tails are masked); B*H <= 65535 (the decode calls
+ *     excepted) and B*H*n <= 2^31.
  *     Other shapes return LINSIMP_E_UNSUPPORTED: there is no fallback path.
  */
 #ifndef LINSIMP_H

@@ -191,7 +191,9 @@ int check_states(const void* ws, const Shape& s, const void* k, const void* v, c
 }
 
 bool shape_supported(const Shape& s, bool /*backward*/) {
-  if (s.w < 1 || s.w > 64) return false;
+  if (s.w < 1 || s.w > 128) return false;
+  if (!wide_window_ok(s.dtype, s.D, s.m, (s.w + 31) / 32)) return false;
+  if (s.w * (s.m < 128 ? s.m : 128) > 8192 && s.w > 64) return false;
   return fwd_combo_supported(s.dtype, s.D, s.Dv, s.m);
 }
 

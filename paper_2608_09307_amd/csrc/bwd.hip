@@ -246,20 +246,22 @@ LS_DEV void frame_ratios(float (&sj)[16], const float* sRj, int t, float Ri) {
 // ---------------------------------------------------------------------------
 // k_bwd_du: du_c = sum_i dN_i (*) A_ic,  A_ic = psi_ic^T M^(i)  (regs <-> anchor,
 // lanes <-> d).  A workgroup stages once the boundary state M_b of its own
-// chunk kt and the key features, values and queries of chunks kt .. kt+2; the
-// state of any row i that sees the tile is then the boundary part plus a tail
-// of at most three chunks,
+// chunk kt and the key features, values and queries of chunks kt .. kt+NA
+// (NA = ceil(w / 32) anchor tiles per row); the state of any row i that sees
+// the tile is then the boundary part plus a tail of at most NA + 1 chunks,
 //   M^(i) = 2^(Rex_kt - R_i) M_b + sum_{c0 <= j <= i} 2^(R_j - R_i) chi_j v_j^T.
-// Row t of chunk kt sees anchors c <= t of the tile and row t of chunk kt+2
-// anchors c > t (w <= 64): the two run as one pair, each lane c taking the row
-// that sees anchor c, so the logits, features and boundary product are formed
-// once for both.  Rows of chunk kt+1 run one at a time.
+// Row t of chunk kt sees anchors c <= t of the tile and row t of chunk kt+NA
+// anchors c > t only (w <= 32 NA): the two run as one pair, each lane c taking
+// the row that sees anchor c, so the logits, features and boundary product are
+// formed once for both.  Rows of chunks kt+1 .. kt+NA-1 run one at a time.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int DV, int M>
+template <typename T, int D, int DV, int M, int NA>
 struct DuCfg {
   static constexpr int PAD = MF<T>::PAD;
   static constexpr int FB = M < 128 ? M : 128;
   static constexpr int NW = 8;
+  static constexpr int NCH = NA + 1;                         // staged row chunks
+  static constexpr int ROWS = 32 * NCH;
   static constexpr int ES = sizeof(T);
   static constexpr int a16(int x) { return (x + 15) & ~15; }
   static constexpr int mx(int x, int y) { return x > y ? x : y; }
@@ -268,11 +270,11 @@ struct DuCfg {
   static constexpr int oOm = 0;                              // Omega block [p][D]
   static constexpr int oM = oOm + a16(FB * (D + PAD) * ES);  // M_b^T [d][sigma(p)]
   static constexpr int oChi = oM + a16(DV * (FB + PAD) * ES);
-  static constexpr int oV = oChi + a16(96 * CST * ES);
-  static constexpr int oQ = oV + a16(96 * VST * ES);
-  static constexpr int oR = oQ + a16(96 * (D + PAD) * ES);   // r of the anchor tile
-  static constexpr int oRj = oR + a16(32 * (D + PAD) * ES);  // R_j of the 96 rows
-  static constexpr int BYTES0 = oRj + a16(96 * 4);
+  static constexpr int oV = oChi + a16(ROWS * CST * ES);
+  static constexpr int oQ = oV + a16(ROWS * VST * ES);
+  static constexpr int oR = oQ + a16(ROWS * (D + PAD) * ES); // r of the anchor tile
+  static constexpr int oRj = oR + a16(32 * (D + PAD) * ES);  // R_j of the staged rows
+  static constexpr int BYTES0 = oRj + a16(ROWS * 4);
   static constexpr int RED = (NW / 2) * 32 * DV * 4;         // end-of-sweep reduction
   static constexpr int BYTES = mx(BYTES0, RED);
 };
@@ -280,8 +282,8 @@ struct DuCfg {
 template <typename T, int D, int DV, int M, int NA>
 __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
   using F = MF<T>;
-  using C = DuCfg<T, D, DV, M>;
-  constexpr int PAD = C::PAD, FB = C::FB, NW = C::NW, CST = C::CST, VST = C::VST;
+  using C = DuCfg<T, D, DV, M, NA>;
+  constexpr int PAD = C::PAD, FB = C::FB, NW = C::NW, CST = C::CST, VST = C::VST, ROWS = C::ROWS;
   constexpr int NT = 64 * NW;
   constexpr int S = M * DV + M;
   static_assert(C::BYTES <= 160 * 1024, "du LDS budget");
@@ -342,18 +344,18 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
     }
   }
   {
-    // key features, values, queries and frames of rows c0 .. c0 + 95 (zero past n)
-    StageRows<T, 96, FB, NT> sc;
-    StageRows<T, 96, DV, NT> sv;
+    // key features, values, queries and frames of rows c0 .. c0 + ROWS - 1 (zero past n)
+    StageRows<T, ROWS, FB, NT> sc;
+    StageRows<T, ROWS, DV, NT> sv;
     sc.load(chis, M, c0, 0, n, tid);
     sv.load(vs, DV, c0, 0, n, tid);
     sc.store(sChi, CST, c0, 0, n, tid);
     sv.store(sV, VST, c0, 0, n, tid);
-    StageRows<T, 96, D, NT> sq;
+    StageRows<T, ROWS, D, NT> sq;
     sq.load(qs, D, c0, 0, n, tid);
     if constexpr (sizeof(T) == 2) sq.store((f16*)sQ, D + PAD, c0, 0, n, tid);
     else sq.store(sQ, D + PAD, c0, 0, n, tid);
-    for (int j = tid; j < 96; j += NT) sRj[j] = (c0 + j < n) ? a.rj[seq + c0 + j] : 0.0f;
+    for (int j = tid; j < ROWS; j += NT) sRj[j] = (c0 + j < n) ? a.rj[seq + c0 + j] : 0.0f;
   }
   __syncthreads();
 
@@ -361,22 +363,24 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
 #pragma unroll
   for (int dt = 0; dt < DV / 32; ++dt) du[dt] = zero16();
 
-  // items 0..31: pair t (rows c0 + t and c0 + 64 + t); 32..63: row c0 + 32 + t
+  // items 0..31: pair t (rows c0 + t and c0 + 32 NA + t); item 32 r + t
+  // (r = 1 .. NA - 1): row c0 + 32 r + t alone.  Row c0 + 32 r + t sees some
+  // anchor of the tile iff 32 r + t - 31 < w.
 #pragma unroll 1
-  for (int it = wv; it < 64; it += NW) {
+  for (int it = wv; it < 32 * NA; it += NW) {
     const bool pair = it < 32;
     const int t = it & 31;
-    const int iA = pair ? c0 + t : c0 + 32 + t;
-    const int iB = c0 + 64 + t;
-    const bool okA = iA < n && (pair || t + 1 < w);            // the row sees the tile
-    const bool okB = pair && iB < n && t + 33 < w;
+    const int rcA = pair ? 0 : it >> 5;                        // chunk of row A relative to kt
+    const int iA = c0 + 32 * rcA + t;
+    const int iB = c0 + 32 * NA + t;
+    const bool okA = iA < n && 32 * rcA + t - 31 < w;          // the row sees the tile
+    const bool okB = pair && iB < n && 32 * NA + t - 31 < w;
     if (!okA && !okB) continue;
-    const int rcA = pair ? 0 : 1;                              // chunk of row A relative to kt
     // row scalars of the (at most two) rows
     const int iAc = min(iA, n - 1), iBc = min(iB, n - 1);
     const float LA = uniform(a.stats[(seq + iAc) * 2]), LB = uniform(a.stats[(seq + iBc) * 2]);
     const float invA = uniform(a.rowstat[(seq + iAc) * 2]), invB = uniform(a.rowstat[(seq + iBc) * 2]);
-    const float RA = uniform(okA ? sRj[rcA * 32 + t] : -kNegInf), RB = uniform(okB ? sRj[64 + t] : -kNegInf);
+    const float RA = uniform(okA ? sRj[rcA * 32 + t] : -kNegInf), RB = uniform(okB ? sRj[32 * NA + t] : -kNegInf);
     const float sbA = uniform(has_bnd ? fast_exp2(Rexb - RA) : 0.0f);
     const float sbB = uniform(has_bnd ? fast_exp2(Rexb - RB) : 0.0f);
     float dNA[DV / 32], dNB[DV / 32];
@@ -388,15 +392,15 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
     // this lane's row: the one that sees anchor c0 + col
     const bool useB = pair && col > t;
     const int i = useB ? iB : iA;
-    const int rc = useB ? 2 : rcA;
+    const int rc = useB ? NA : rcA;
     const float Ri = useB ? RB : RA;
     const bool valid = (useB ? okB : okA) && (i - c0 - col >= 0) && (i - c0 - col < w);
     typename F::frag pf[FB / 32][F::CSTEPS];
     query_features<T, D, FB>(pf, sQ + (rc * 32 + t) * (D + PAD), sR + col * (D + PAD), sOm, valid, useB ? LB : LA);
     // tails: P^T[j, c] = chi_j . psi_c of chunk kt + rj, framed, j <= row(c)
-    constexpr int NTL = 3;
+    constexpr int NTL = NA + 1;
     typename F::frag ppf[NTL][F::CSTEPS];
-    const int ntl = okB ? 3 : rcA + 1;                          // tails any lane needs
+    const int ntl = okB ? NTL : rcA + 1;                        // tails any lane needs
 #pragma unroll
     for (int rj = 0; rj < NTL; ++rj) {
       if (rj >= ntl) {
@@ -819,8 +823,12 @@ struct StCfg {
     return a16(WIN * (DV + tp) * ES) + a16(32 * (FB + PAD) * ES) + a16(32 * AW * 4) + 2 * a16(32 * 4) +
            a16(NW * D * ES) + a16(NW * RB * DV * 4);
   }
-  // full-rate transposing reads of u when two workgroups still fit a CU
-  static constexpr int TP = (oU + tail(tr_pad<T, DV>()) <= 80 * 1024 || sizeof(T) != 2) ? tr_pad<T, DV>() : 16;
+  // two workgroups per CU up to two anchor tiles per row (w <= 64); wider
+  // windows stage up to 159 anchor rows and run one workgroup per CU
+  static constexpr int LDS_CAP = NA <= 2 ? 80 * 1024 : 160 * 1024;
+  static constexpr int MINB = NA <= 2 ? 2 : 1;
+  // full-rate transposing reads of u when the budget allows
+  static constexpr int TP = (oU + tail(tr_pad<T, DV>()) <= LDS_CAP || sizeof(T) != 2) ? tr_pad<T, DV>() : 16;
   static constexpr int oChi = oU + a16(WIN * (DV + TP) * ES);
   static constexpr int oNz = oChi + a16(32 * (FB + PAD) * ES);
   static constexpr int oRj = oNz + a16(32 * AW * 4);
@@ -858,12 +866,12 @@ template <typename T> LS_DEV void sq_split(const typename MF<T>::frag& x, typena
 }
 
 template <typename T, int D, int DV, int M, int NA>
-__global__ __launch_bounds__(256, 2) void k_bwd_state(BwdArgs a) {
+__global__ __launch_bounds__(256, (NA <= 2 ? 2 : 1)) void k_bwd_state(BwdArgs a) {
   using F = MF<T>;
   using C = StCfg<T, D, DV, M, NA>;
   constexpr int PAD = C::PAD, FB = C::FB, WIN = C::WIN, NW = C::NW, AW = C::AW, RB = C::RB;
   constexpr int NT = 64 * NW;
-  static_assert(C::BYTES <= 80 * 1024, "state LDS budget (two groups per CU)");
+  static_assert(C::BYTES <= C::LDS_CAP, "state LDS budget");
   __shared__ __align__(16) char smem[C::BYTES];
   T* sR = (T*)(smem + C::oR);
   T* sU = (T*)(smem + C::oU);
@@ -1448,7 +1456,13 @@ int launch_backward(const Shape& s, const void* q, const void* k, const void* v,
 #define X(T, D_, DV_, M_)                                                            \
   if (s.dtype == (sizeof(T) == 2 ? 1 : 0) && s.D == D_ && s.Dv == DV_ && s.m == M_) { \
     if (NA == 1) return run_bwd<T, D_, DV_, M_, 1>(s, a, st);                        \
-    return run_bwd<T, D_, DV_, M_, 2>(s, a, st);                                     \
+    if (NA == 2) return run_bwd<T, D_, DV_, M_, 2>(s, a, st);                        \
+    if constexpr (wide_window_ok(sizeof(T) == 2 ? 1 : 0, D_, M_, 3)) {                \
+      if (NA == 3) return run_bwd<T, D_, DV_, M_, 3>(s, a, st);                      \
+    }                                                                                \
+    if constexpr (wide_window_ok(sizeof(T) == 2 ? 1 : 0, D_, M_, 4)) {                \
+      if (NA == 4) return run_bwd<T, D_, DV_, M_, 4>(s, a, st);                      \
+    }                                                                                \
   }
   LS_BWD_CASES(X)
 #undef X

@@ -655,7 +655,13 @@ int launch_decode(int64_t S, int H, int ntok, int D, int Dv, int m, int w, int d
 #define X(T, D_, DV_, M_)                                                              \
   if (dtype == (sizeof(T) == 2 ? 1 : 0) && D == D_ && Dv == DV_ && m == M_) {          \
     if (NA == 1) return run_decode<T, D_, DV_, M_, 1>(S, A, ntok, st);                 \
-    return run_decode<T, D_, DV_, M_, 2>(S, A, ntok, st);                              \
+    if (NA == 2) return run_decode<T, D_, DV_, M_, 2>(S, A, ntok, st);                 \
+    if constexpr (wide_window_ok(sizeof(T) == 2 ? 1 : 0, D_, M_, 3)) {                  \
+      if (NA == 3) return run_decode<T, D_, DV_, M_, 3>(S, A, ntok, st);               \
+    }                                                                                  \
+    if constexpr (wide_window_ok(sizeof(T) == 2 ? 1 : 0, D_, M_, 4)) {                  \
+      if (NA == 4) return run_decode<T, D_, DV_, M_, 4>(S, A, ntok, st);               \
+    }                                                                                  \
   }
   LS_DEC_CASES(X)
 #undef X

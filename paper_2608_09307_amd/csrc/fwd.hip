@@ -808,7 +808,8 @@ int launch_ring_fill(const Shape& s, const void* r, const void* u, void* ring_r,
   return 0;
 }
 
-// Supported (dtype, D = Dv, m) combinations; w <= 64.
+// Supported (dtype, D = Dv, m) combinations; w <= 64, and up to 128 where
+// wide_window_ok allows it.
 #define LS_FWD_CASES(X)               \
   X(bf16, 32, 32, 32)                 \
   X(bf16, 64, 64, 64)                 \
@@ -844,7 +845,13 @@ int launch_forward(const Shape& s, const void* q, const void* k, const void* v, 
 #define X(T, D_, DV_, M_)                                                          \
   if (s.dtype == (sizeof(T) == 2 ? 1 : 0) && s.D == D_ && s.Dv == DV_ && s.m == M_) { \
     if (NA == 1) return run_fwd<T, D_, DV_, M_, 1>(s, a, st);                      \
-    return run_fwd<T, D_, DV_, M_, 2>(s, a, st);                                   \
+    if (NA == 2) return run_fwd<T, D_, DV_, M_, 2>(s, a, st);                      \
+    if constexpr (wide_window_ok(sizeof(T) == 2 ? 1 : 0, D_, M_, 3)) {              \
+      if (NA == 3) return run_fwd<T, D_, DV_, M_, 3>(s, a, st);                    \
+    }                                                                              \
+    if constexpr (wide_window_ok(sizeof(T) == 2 ? 1 : 0, D_, M_, 4)) {              \
+      if (NA == 4) return run_fwd<T, D_, DV_, M_, 4>(s, a, st);                    \
+    }                                                                              \
   }
   LS_FWD_CASES(X)
 #undef X

@@ -45,6 +45,14 @@ struct Workspace {
   float* rowstat;   // [BH][n][2]           per-row 1/(Z+eps) and dZ
 };
 
+// Windows wider than 64 (NA = ceil(w / 32) = 3 or 4 anchor tiles per row)
+// follow the launch rule w * min(m, 128) <= 8192: m <= 64.  The one exception
+// is float32 with D = m = 64 at NA = 4, whose du sweep would need 167 KB of
+// LDS for its five staged row chunks.
+constexpr bool wide_window_ok(int dtype, int D, int m, int NA) {
+  return NA <= 2 || (NA <= 4 && m <= 64 && 32 * NA * m <= 8192 && !(dtype == 0 && D == 64 && m == 64 && NA == 4));
+}
+
 // Row-side dq is summed over the anchor tiles a row sees: row i receives from
 // tiles floor(i/32) - ns + 1 .. floor(i/32), ns = ceil(w/32) + 1.
 inline int bwd_slots(int w) { return (w + kChunk - 1) / kChunk + 1; }

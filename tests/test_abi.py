@@ -57,8 +57,14 @@ def test_workspace_size_and_unsupported_shapes():
     d = L.make_dims(2, 16, 16384, 128, 128, 128, 64, L.BF16)
     fw, bw = L.workspace_size(d, False), L.workspace_size(d, True)
     assert 0 < fw < bw
+    # windows up to 128 under the launch rule w * min(m, 128) <= 8192
+    for ok in (L.make_dims(1, 1, 256, 128, 128, 64, 128, L.BF16), L.make_dims(1, 1, 256, 64, 64, 64, 96, L.F32),
+               L.make_dims(1, 1, 256, 32, 32, 64, 128, L.F32), L.make_dims(1, 1, 256, 64, 64, 128, 64, L.BF16)):
+        assert L.workspace_size(ok, True) > 0
     for bad in (L.make_dims(1, 1, 256, 48, 48, 32, 64, L.BF16),     # D not supported
-                L.make_dims(1, 1, 256, 32, 32, 32, 65, L.BF16),     # w > 64
+                L.make_dims(1, 1, 256, 32, 32, 32, 129, L.BF16),    # w > 128
+                L.make_dims(1, 1, 256, 128, 128, 128, 65, L.BF16),  # w * m > 8192
+                L.make_dims(1, 1, 256, 64, 64, 64, 97, L.F32),      # f32 D = m = 64 stops at w = 96
                 L.make_dims(1, 1, 256, 128, 128, 128, 64, L.F32),   # f32 only up to 64
                 L.make_dims(1, 1, 0, 32, 32, 32, 64, L.BF16),       # n = 0
                 L.make_dims(1, 1, 8, 32, 32, 32, 64, 7),            # bad dtype

@@ -103,6 +103,16 @@ def test_backward_edge_lengths(D, m, n, w, dt):
     _run(Workload("edge_bwd", 1, 2, n, D, D, m, w, dt, "fwdbwd", seed=34))
 
 
+@pytest.mark.parametrize("D,m,w,n,dt", [(128, 64, 96, 400, "bf16"), (128, 64, 128, 433, "bf16"),
+                                        (64, 64, 100, 300, "bf16"), (32, 32, 128, 290, "bf16"),
+                                        (64, 64, 96, 250, "f32"), (32, 64, 128, 333, "f32"),
+                                        (128, 64, 128, 40, "bf16")])
+def test_backward_wide_windows(D, m, w, n, dt):
+    """Windows of three and four anchor tiles (64 < w <= 128, w * m <= 8192):
+    the du sweep stages NA + 1 row chunks and pairs chunk kt with kt + NA."""
+    _run(Workload("wide_bwd", 1, 2, n, D, D, m, w, dt, "fwdbwd", seed=42))
+
+
 def test_backward_layer16k_sampled_heads():
     _run(WORKLOADS["layer16k_bf16"], pairs=[(1, 9), (0, 2)])
 

@@ -32,6 +32,7 @@ def _state_true(st, s, h):
 
 @pytest.mark.parametrize("dtype,D,m,w,P,steps", [("f32", 32, 32, 8, 5, 20), ("f32", 64, 64, 64, 70, 6),
                                                   ("bf16", 128, 128, 64, 40, 40),
+                                                  ("bf16", 128, 64, 128, 150, 12), ("f32", 64, 64, 96, 100, 8),
                                                   ("bf16", 64, 128, 33, 3, 12),
                                                   ("bf16", 128, 256, 64, 100, 3)])
 def test_prefill_then_decode_matches_forward_rows(dtype, D, m, w, P, steps):
@@ -143,6 +144,7 @@ def test_decode_s256_h16_prefix8192_sampled():
 
 
 @pytest.mark.parametrize("dtype,D,m,w,P,T", [("f32", 32, 32, 8, 5, 20), ("bf16", 128, 128, 64, 40, 7),
+                                              ("bf16", 128, 64, 128, 100, 40),
                                               ("bf16", 128, 128, 64, 3, 90), ("bf16", 64, 128, 33, 0, 40),
                                               ("bf16", 128, 256, 64, 10, 12)])
 def test_decode_chunk_matches_steps_and_forward(dtype, D, m, w, P, T):

@@ -116,6 +116,14 @@ def test_first_key_underflow_is_handled():
     assert rel_l2(f64(out[0, 0]), ref) < 2e-2
 
 
+@pytest.mark.parametrize("D,m,w,n,dt", [(128, 64, 96, 400, "bf16"), (128, 64, 128, 433, "bf16"),
+                                        (64, 64, 100, 300, "bf16"), (32, 32, 128, 290, "bf16"),
+                                        (64, 64, 96, 250, "f32"), (32, 64, 128, 333, "f32")])
+def test_forward_wide_windows(D, m, w, n, dt):
+    """Windows of three and four anchor tiles (64 < w <= 128, w * m <= 8192)."""
+    _run_and_compare(Workload("wide_fwd", 1, 2, n, D, D, m, w, dt, "fwd", seed=41))
+
+
 @pytest.mark.parametrize("w,n", [(1, 70), (33, 97)])
 def test_forward_two_feature_blocks_short_windows(w, n):
     """m = 256 (feature-block partials merged by the online maximum) with one
