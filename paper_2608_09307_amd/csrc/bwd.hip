@@ -65,20 +65,6 @@ struct BwdArgs {
 
 static constexpr float kLn2 = 0.6931471805599453f;
 
-// Row padding (elements) of LDS buffers read with ds_read_b64_tr_b16.  One
-// transposing read touches 8 rows x 64 bytes; it runs at full rate when the
-// row pitch is 64 or 192 bytes modulo 256 (the four rows of each 16-lane group
-// 16 dwords apart), e.g. 320-byte rows for 128 bf16 columns, against a half
-// rate at 288 bytes and a third at 272 (measured on gfx950).  16-byte row
-// reads run at the same rate for any of these pitches.
-template <typename T, int N> constexpr int tr_pad() {
-  if (sizeof(T) != 2) return 1;
-  for (int p = 0; p < 128; p += 8) {
-    const int b = (2 * (N + p)) % 256;
-    if (b == 64 || b == 192) return p;
-  }
-  return 8;
-}
 
 // ---------------------------------------------------------------------------
 // prep: row scalars and zeroed float32 accumulators

@@ -150,6 +150,21 @@ LS_DEV bf16x8 MF<bf16>::tld_crow_map(const bf16* mat, int ld, int sp, int n0, Ro
   return cat44(a, b);
 }
 
+// Row padding (elements) of LDS buffers read with ds_read_b64_tr_b16.  One
+// transposing read touches 8 rows x 64 bytes; it runs at full rate when the
+// row pitch is 64 or 192 bytes modulo 256 (the four rows of each 16-lane group
+// 16 dwords apart), e.g. 320-byte rows for 128 bf16 columns, against a half
+// rate at 288 bytes and a third at 272 (measured on gfx950).  16-byte row
+// reads run at the same rate for any of these pitches.
+template <typename T, int N> constexpr int tr_pad() {
+  if (sizeof(T) != 2) return 1;
+  for (int p = 0; p < 128; p += 8) {
+    const int b = (2 * (N + p)) % 256;
+    if (b == 64 || b == 192) return p;
+  }
+  return 8;
+}
+
 // row index of accumulator register v in a 32x32 tile
 LS_DEV int crow(int v, int h) { return 8 * (v >> 2) + 4 * h + (v & 3); }
 

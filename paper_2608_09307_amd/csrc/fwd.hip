@@ -422,8 +422,12 @@ struct RCfg {
   static constexpr int oChi = oA + a16(M * 4);
   static constexpr int oVt = oChi + a16(BC * (FB + PAD) * ES);
   static constexpr int oR = oVt + a16(DV * (BC + PAD) * ES);
+  // u of the window: bf16 natural [window row][d] (read transposed, rows in
+  // crow order); float32 transposed [d][window row]
+  static constexpr int TPU = tr_pad<T, DV>();
+  static constexpr int UBYTES = sizeof(T) == 2 ? WIN * (DV + TPU) * ES : DV * UST * ES;
   static constexpr int oUt = oR + a16(WIN * (D + PAD) * ES);
-  static constexpr int oQ = oUt + a16(DV * UST * ES);
+  static constexpr int oQ = oUt + a16(UBYTES);
   static constexpr int oRj = oQ + a16(BC * (D + PAD) * ES);
   static constexpr int BYTES = oRj + a16(BC * 4);
 };
@@ -473,7 +477,7 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     StageRowsT<T, FB, DV, NT> sm16;
     StageRowsT<T, 32, DV, NT> sv;
     StageRows<T, WIN, D, NT> sr;
-    StageRowsT<T, WIN, DV, NT> su;
+    typename std::conditional<sizeof(T) == 2, StageRows<T, WIN, DV, NT>, StageRowsT<T, WIN, DV, NT>>::type su;
     StageRows<T, 32, D, NT> sq;
     StageRows<T, 32, FB, NT> sc;
     if constexpr (sizeof(T) == 2) so.load((const f16*)a.omh + ((size_t)hh * M + (size_t)fbk * FB) * D, D, 0, 0, FB, tid);
@@ -517,10 +521,14 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     });
     if constexpr (sizeof(T) == 2) sr.store((f16*)sR, D + PAD, wb, 0, n, tid);
     else sr.store(sR, D + PAD, wb, 0, n, tid);
-    su.store(wb, 0, n, tid, [&](int wi, int d0, const typename StageRowsT<T, WIN, DV, NT>::V4& x) {
+    if constexpr (sizeof(T) == 2) {
+      su.store(sUt, DV + C::TPU, wb, 0, n, tid);
+    } else {
+      su.store(wb, 0, n, tid, [&](int wi, int d0, const typename StageRowsT<T, WIN, DV, NT>::V4& x) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) sUt[(d0 + e) * UST + wi] = x[e];
-    });
+        for (int e = 0; e < 4; ++e) sUt[(d0 + e) * UST + wi] = x[e];
+      });
+    }
     if constexpr (sizeof(T) == 2) sq.store((f16*)sQ, D + PAD, s0, 0, n, tid);
     else sq.store(sQ, D + PAD, s0, 0, n, tid);
     sc.store(sChi, FB + PAD, s0, 0, n, tid);
@@ -650,10 +658,22 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
 #pragma unroll
         for (int sp = 0; sp < F::CSTEPS; ++sp) accA = F::mma(ppf[sp], F::ldc(vrow, 0, sp, h), accA);
         // anchor row index crow(v,h) = 8*(v>>2) + 4h + (v&3) -> window index falls with it
-        const T* urow = sUt + (dt * 32 + col) * UST + (t + 32 * NA - 1 - 32 * an) - 4 * h;
         float sacc = 0.0f;
+        if constexpr (sizeof(T) == 2) {
+          // u of the register's anchor at this lane's d: transposed reads of rows
+          // t + 32 NA - 1 - 32 an - crow, in crow order
+          auto rmap = [&](int ar) { return t + 32 * NA - 1 - 32 * an - ar; };
 #pragma unroll
-        for (int v = 0; v < 16; ++v) sacc += accA[v] * tof(urow[-(8 * (v >> 2) + (v & 3))]);
+          for (int sp = 0; sp < F::CSTEPS; ++sp) {
+            const typename F::frag uf = F::tld_crow_map(sUt, DV + C::TPU, sp, dt * 32, rmap);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) sacc += accA[8 * sp + e] * fel(uf, e);
+          }
+        } else {
+          const T* urow = sUt + (dt * 32 + col) * UST + (t + 32 * NA - 1 - 32 * an) - 4 * h;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) sacc += accA[v] * tof(urow[-(8 * (v >> 2) + (v & 3))]);
+        }
         nacc[dt] += sacc;
       }
         zacc += zc;
