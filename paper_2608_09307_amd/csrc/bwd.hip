@@ -1043,8 +1043,7 @@ __global__ __launch_bounds__(256, (NA <= 2 ? 2 : 1)) void k_bwd_state(BwdArgs a)
 #pragma unroll
       for (int sp = 0; sp < F::CSTEPS; ++sp) {
         pf[an][sp] = F::cfrag(acc[an], sp);
-#pragma unroll
-        for (int e = 0; e < F::KPL; ++e) ps += fel(pf[an][sp], e);
+        ps = add_elems(pf[an][sp], ps);
       }
     }
     if (fr != 1.0f) {

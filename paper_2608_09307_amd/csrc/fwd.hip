@@ -422,8 +422,9 @@ struct RCfg {
   static constexpr int oChi = oA + a16(M * 4);
   static constexpr int oVt = oChi + a16(BC * (FB + PAD) * ES);
   static constexpr int oR = oVt + a16(DV * (BC + PAD) * ES);
-  // u of the window: bf16 natural [window row][d] (read transposed, rows in
-  // crow order); float32 transposed [d][window row]
+  // u of the window: bf16 inputs as f16 [window row][d] (read transposed, rows
+  // in crow order, then multiplied in mixed precision); float32 transposed
+  // [d][window row]
   static constexpr int TPU = tr_pad<T, DV>();
   static constexpr int UBYTES = sizeof(T) == 2 ? WIN * (DV + TPU) * ES : DV * UST * ES;
   static constexpr int oUt = oR + a16(WIN * (D + PAD) * ES);
@@ -522,7 +523,7 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     if constexpr (sizeof(T) == 2) sr.store((f16*)sR, D + PAD, wb, 0, n, tid);
     else sr.store(sR, D + PAD, wb, 0, n, tid);
     if constexpr (sizeof(T) == 2) {
-      su.store(sUt, DV + C::TPU, wb, 0, n, tid);
+      su.store((f16*)sUt, DV + C::TPU, wb, 0, n, tid);      // f16: exact for bf16 in its range
     } else {
       su.store(wb, 0, n, tid, [&](int wi, int d0, const typename StageRowsT<T, WIN, DV, NT>::V4& x) {
 #pragma unroll
@@ -665,9 +666,9 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
           auto rmap = [&](int ar) { return t + 32 * NA - 1 - 32 * an - ar; };
 #pragma unroll
           for (int sp = 0; sp < F::CSTEPS; ++sp) {
-            const typename F::frag uf = F::tld_crow_map(sUt, DV + C::TPU, sp, dt * 32, rmap);
+            const f16x8 uf = __builtin_bit_cast(f16x8, F::tld_crow_map(sUt, DV + C::TPU, sp, dt * 32, rmap));
 #pragma unroll
-            for (int e = 0; e < 8; ++e) sacc += accA[8 * sp + e] * fel(uf, e);
+            for (int e = 0; e < 8; ++e) sacc = __builtin_fmaf(accA[8 * sp + e], (float)uf[e], sacc);
           }
         } else {
           const T* urow = sUt + (dt * 32 + col) * UST + (t + 32 * NA - 1 - 32 * an) - 4 * h;
