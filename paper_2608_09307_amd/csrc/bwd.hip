@@ -352,16 +352,16 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
   // items 0..31: pair t (rows c0 + t and c0 + 32 NA + t); item 32 r + t
   // (r = 1 .. NA - 1): row c0 + 32 r + t alone.  Row c0 + 32 r + t sees some
   // anchor of the tile iff 32 r + t - 31 < w.
-#pragma unroll 1
-  for (int it = wv; it < 32 * NA; it += NW) {
-    const bool pair = it < 32;
+  // one body, compiled for the paired items (0..31) and for the single rows
+  auto item = [&](const int it, auto pair_c) {
+    constexpr bool pair = decltype(pair_c)::value;
     const int t = it & 31;
     const int rcA = pair ? 0 : it >> 5;                        // chunk of row A relative to kt
     const int iA = c0 + 32 * rcA + t;
     const int iB = c0 + 32 * NA + t;
     const bool okA = iA < n && 32 * rcA + t - 31 < w;          // the row sees the tile
     const bool okB = pair && iB < n && 32 * NA + t - 31 < w;
-    if (!okA && !okB) continue;
+    if (!okA && !okB) return;
     // row scalars of the (at most two) rows
     const int iAc = min(iA, n - 1), iBc = min(iB, n - 1);
     const float LA = uniform(a.stats[(seq + iAc) * 2]), LB = uniform(a.stats[(seq + iBc) * 2]);
@@ -373,8 +373,12 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
 #pragma unroll
     for (int dt = 0; dt < DV / 32; ++dt) {
       dNA[dt] = tof(gs[(size_t)iAc * DV + dt * 32 + col]) * invA;
-      dNB[dt] = tof(gs[(size_t)iBc * DV + dt * 32 + col]) * invB;
+      dNB[dt] = pair ? tof(gs[(size_t)iBc * DV + dt * 32 + col]) * invB : 0.0f;
     }
+    // boundary scale of each register's anchor row (registers crow(v, h) > t: row B)
+    float sbv[16];
+#pragma unroll
+    for (int v = 0; v < 16; ++v) sbv[v] = (pair && crow(v, h) > t) ? sbB : sbA;
     // this lane's row: the one that sees anchor c0 + col
     const bool useB = pair && col > t;
     const int i = useB ? iB : iA;
@@ -434,7 +438,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
 #pragma unroll
       for (int g = 0; g < G; ++g)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) accA[g][v] *= (pair && crow(v, h) > t) ? sbB : sbA;
+        for (int v = 0; v < 16; ++v) accA[g][v] *= sbv[v];
 #pragma unroll
       for (int rj = 0; rj < NTL; ++rj) {
         if (rj >= ntl) continue;
@@ -449,7 +453,11 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) du[d0 + g][v] += accA[g][v] * ((pair && crow(v, h) > t) ? dNB[d0 + g] : dNA[d0 + g]);
     }
-  }
+  };
+#pragma unroll 1
+  for (int it = wv; it < 32; it += NW) item(it, std::true_type{});
+#pragma unroll 1
+  for (int it = 32 + wv; it < 32 * NA; it += NW) item(it, std::false_type{});
   reduce_waves<DV / 32>(du, (float*)smem, wv, NW);
   if (wv == 0) {
 #pragma unroll
