@@ -111,6 +111,12 @@ __global__ __launch_bounds__(256) void k_chunk_state(FwdArgs a) {
   const float rb = wave_max(mx);
   const float rs = rsqrtf((float)M);
   float* st = a.states + ((size_t)bh * a.nch + b) * S;
+  // bf16 inputs: the two operands of Mt_b = chi^T V are left in the chunk's
+  // (otherwise unused) float32 M slot, as the 16-byte fragments the matrix
+  // cores take: chi^T [p][sigma(j)] (m x 32) and V^T [d][sigma(j)] (DV x 32);
+  // k_state_scan_mma forms the product and scans it
+  bf16* cx = (bf16*)st;
+  bf16* vx = cx + M * 32;
 #pragma unroll
   for (int pt = 0; pt < M / 32; ++pt) {
     float asum = 0.0f;
@@ -122,15 +128,25 @@ __global__ __launch_bounds__(256) void k_chunk_state(FwdArgs a) {
     }
     asum = half_swap_add(asum);
     if (h == 0) st[M * DV + pt * 32 + col] = asum;
-#pragma unroll
-    for (int dt = 0; dt < DV / 32; ++dt) {
-      f32x16 o = zero16();
+    if constexpr (sizeof(T) == 2) {
 #pragma unroll
       for (int sp = 0; sp < F::CSTEPS; ++sp)
-        o = F::mma(F::cfrag(acc[pt], sp), F::ldc(&sVt[wv][dt * 32 + col][0], 0, sp, h), o);
+        *(bf16x8*)(cx + (pt * 32 + col) * 32 + 16 * sp + 8 * h) = F::cfrag(acc[pt], sp);
+    } else {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) st[(size_t)(pt * 32 + crow(v, h)) * DV + dt * 32 + col] = o[v];
+      for (int dt = 0; dt < DV / 32; ++dt) {
+        f32x16 o = zero16();
+#pragma unroll
+        for (int sp = 0; sp < F::CSTEPS; ++sp)
+          o = F::mma(F::cfrag(acc[pt], sp), F::ldc(&sVt[wv][dt * 32 + col][0], 0, sp, h), o);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) st[(size_t)(pt * 32 + crow(v, h)) * DV + dt * 32 + col] = o[v];
+      }
     }
+  }
+  if constexpr (sizeof(T) == 2) {
+    for (int idx = l; idx < DV * 4; idx += 64)
+      *(bf16x8*)(vx + (idx >> 2) * 32 + 8 * (idx & 3)) = *(const bf16x8*)(&sVt[wv][idx >> 2][8 * (idx & 3)]);
   }
   if (l == 0) a.rho[(size_t)bh * a.nch + b] = rb;
 }
@@ -400,6 +416,104 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     if (h == 0) a.final_a[(size_t)bh * M + wv * 32 + col] = at;
   }
   if (tid == 0) a.final_rex[bh] = R;
+}
+
+// ---------------------------------------------------------------------------
+// K2b for bf16 inputs: the same exclusive scan, with each chunk's contribution
+// Mt_b = chi^T V formed here on the matrix cores from the operand fragments the
+// chunk kernel left in the chunk's M slot (0.2 of the bytes of a float32
+// contribution).  One wave per (sequence-head, 32 features, 32 columns): the
+// running state tile stays in its registers, the fragments of the chunks ahead
+// are loaded PF chunks in advance (they do not depend on the recurrence), and
+// each chunk's boundary state is written in bf16 to states16.  The wave of the
+// first 32 columns also scans a in place.  Workgroups are dealt to the eight
+// XCDs in turn; the waves of one sequence-head are numbered to land on one XCD,
+// so the fragments they share come through one L2.
+// [App. C "Host preparation": exclusive cumulative sum -> boundary states]
+// ---------------------------------------------------------------------------
+template <int M, int DV>
+__global__ __launch_bounds__(64) void k_state_scan_mma(FwdArgs a) {
+  constexpr int S = M * DV + M;
+  constexpr int NDT = DV / 32, NPD = (M / 32) * NDT;
+  constexpr int PF = 6;
+  // the state tile passes through LDS so that each lane stores 32 contiguous
+  // bytes (16 two-byte stores per lane would take most of the memory counter
+  // that the loads in flight need)
+  __shared__ __align__(16) bf16 sT[32][40];
+  const int l = threadIdx.x, col = l & 31, h = l >> 5;
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int bh = xcd + 8 * (slot / NPD), tt = slot % NPD;
+  if (bh >= a.BH) return;                              // wave-uniform
+  const int p0 = (tt / NDT) * 32, d0 = (tt % NDT) * 32;
+  const int nch = a.nch;
+  float* stb = a.states + (size_t)bh * nch * S;
+  bf16* s16 = (bf16*)a.states16 + (size_t)bh * nch * M * DV;
+  const float* rh = a.rho + (size_t)bh * nch;
+  float* rx = a.rex + (size_t)bh * (nch + 1);
+  const bool aw = d0 == 0;                              // also scans a (lanes of half 0)
+  const bool writer = p0 == 0 && d0 == 0 && l == 0;
+  bf16x8 xq[PF][4];
+  float aq[PF], rq[PF];
+  // every load unconditional (clamped chunk index), so that the compiler's
+  // memory-counter waits see PF chunks in flight
+  auto fetch = [&](int b, int e) {
+    const bf16* cx = (const bf16*)(stb + (size_t)b * S);
+    const bf16* vx = cx + M * 32;
+    xq[e][0] = *(const bf16x8*)(cx + (p0 + col) * 32 + 8 * h);
+    xq[e][1] = *(const bf16x8*)(cx + (p0 + col) * 32 + 16 + 8 * h);
+    xq[e][2] = *(const bf16x8*)(vx + (d0 + col) * 32 + 8 * h);
+    xq[e][3] = *(const bf16x8*)(vx + (d0 + col) * 32 + 16 + 8 * h);
+    aq[e] = stb[(size_t)b * S + M * DV + p0 + col];
+    rq[e] = rh[b];
+  };
+#pragma unroll
+  for (int e = 0; e < PF; ++e) fetch(min(e, nch - 1), e);
+  f32x16 run = zero16();
+  float runa = 0.0f, R = kNegInf;
+  // chunk b from ring slot e, then slot e takes chunk b + PF
+  auto step = [&](int b, int e) {
+    // the state of every token before chunk b (frame R)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) sT[crow(v, h)][col] = (bf16)run[v];
+    wave_lds_sync();
+    {
+      const int rr = l >> 1, c0 = 16 * (l & 1);
+      const bf16x8 y0 = *(const bf16x8*)&sT[rr][c0], y1 = *(const bf16x8*)&sT[rr][c0 + 8];
+      bf16* o = s16 + ((size_t)b * M + p0 + rr) * DV + d0 + c0;
+      *(bf16x8*)o = y0;
+      *(bf16x8*)(o + 8) = y1;
+    }
+    if (aw) stb[(size_t)b * S + M * DV + p0 + col] = runa;   // both halves: the same value
+    if (writer) rx[b] = R;
+    f32x16 c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xq[e][0], xq[e][2], zero16(), 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(xq[e][1], xq[e][3], c, 0, 0, 0);
+    const float rb = uniform(rq[e]);
+    const float Rn = fmaxf(R, rb);
+    const float sa = fast_exp2(R - Rn);                // 0 when R = -inf
+    const float sb = fast_exp2(rb - Rn);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) run[v] = run[v] * sa + c[v] * sb;
+    runa = runa * sa + aq[e] * sb;
+    R = Rn;
+    fetch(min(b + PF, nch - 1), e);
+  };
+  int b0 = 0;
+  for (; b0 + PF <= nch; b0 += PF) {
+#pragma unroll
+    for (int e = 0; e < PF; ++e) step(b0 + e, e);
+  }
+#pragma unroll
+  for (int e = 0; e < PF; ++e)
+    if (b0 + e < nch) step(b0 + e, e);
+  if (a.final_M != nullptr) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) a.final_M[((size_t)bh * M + p0 + crow(v, h)) * DV + d0 + col] = run[v];
+    if (aw) a.final_a[(size_t)bh * M + p0 + col] = runa;
+  }
+  if (writer) {
+    rx[nch] = R;
+    if (a.final_rex != nullptr) a.final_rex[bh] = R;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -764,7 +878,11 @@ static int run_fwd(const Shape& s, FwdArgs a, hipStream_t st) {
   }
   { ProfScope ps("chunk_state", st);
   k_chunk_state<T, D, DV, M><<<dim3((nch + 3) / 4, BH), 256, 0, st>>>(a); }
-  {
+  if constexpr (sizeof(T) == 2) {
+    constexpr int NPD = (M / 32) * (DV / 32);
+    ProfScope ps("state_scan", st);
+    k_state_scan_mma<M, DV><<<(unsigned)((BH + 7) / 8 * 8 * NPD), 64, 0, st>>>(a);
+  } else {
     constexpr int S = M * DV + M;
     ProfScope ps("state_scan", st);
     k_state_scan<M, DV><<<dim3((S / 4 + 255) / 256, BH), 256, 0, st>>>(a);

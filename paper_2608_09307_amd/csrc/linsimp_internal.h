@@ -27,7 +27,8 @@ struct Workspace {
   void* omq;        // [H][m][D] operand type: query-side Omega * log2(e)
   void* omk;        // bf16: [H][2][m][D] hi/lo split of Omega*log2(e); f32: [H][m][D]
   void* omh;        // [H][m][D] f16 Omega*log2(e): the query-side logits of bf16 inputs
-  float* states;    // [BH][nch][m*Dv + m]  chunk contributions, then boundary states (bf16 inputs: a only)
+  float* states;    // [BH][nch][m*Dv + m]  chunk contributions, then boundary states (bf16 inputs: a only;
+                   //                      the M slot holds the chunk's chi^T and V^T operand fragments)
   void* states16;   // [BH][nch][m*Dv]      bf16 inputs: the boundary states' M, in bf16 (the operand type of
                    //                      every reader); states then keeps the chunk contributions' M
   float* rho;       // [BH][nch]            chunk max of key log2-features
