@@ -693,13 +693,15 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
           dps = F::mma(cf, qqf[sp], dps);
         }
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const float dl = __builtin_fmaf(fel(pf[pt][v / F::KPL], v % F::KPL), dps[v], 0.0f);
-          sc += dl;
-          dps[v] = dl;
-        }
+        for (int v = 0; v < 16; ++v) dps[v] = __builtin_fmaf(fel(pf[pt][v / F::KPL], v % F::KPL), dps[v], 0.0f);
+        // s_c sums dlambda as rounded for dz's matrix product: the two terms of
+        // dz = sum_p dlambda_p (Omega_p - z) partly cancel, and a rounding in
+        // one of them only would be amplified by that
 #pragma unroll
-        for (int sp = 0; sp < F::CSTEPS; ++sp) dlf[pt][sp] = F::cfrag(dps, sp);
+        for (int sp = 0; sp < F::CSTEPS; ++sp) {
+          dlf[pt][sp] = F::cfrag(dps, sp);
+          sc = add_elems(dlf[pt][sp], sc);
+        }
       }
       sc = half_swap_add(sc);
       if (h == 0) sSc[col] = valid ? sc : 0.0f;
