@@ -205,14 +205,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   // overlaps the staging, the key features and the logits.
   constexpr bool PRE = PTW == 1;
   float mreg[PRE ? DV / 32 : 1][16];
-  if constexpr (PRE) {
-    if (wv < PT) {
-#pragma unroll
-      for (int dt = 0; dt < DV / 32; ++dt)
-#pragma unroll
-        for (int vv = 0; vv < 16; ++vv) mreg[dt][vv] = Ms[(size_t)(wv * 32 + crow(vv, h)) * DV + dt * 32 + col];
-    }
-  }
   const float a_old = tid < M ? as[tid] : 0.0f;
 
   // ---- stage the token, the ring (slot t mod w replaced by the new token) and Omega ----
@@ -229,6 +221,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   // give the logits' operand fragments (no LDS copy of the bank) ----
   typename F::frag omf[PRE ? D / F::KS : 1];
   const float rho_t = key_log2_features<T, D, M, PRE>(sk, om, schi, sred, omf);
+  // the state rows this thread updates are fetched after the key GEMV's loads:
+  // their latency overlaps the logits and exponentials (the memory counter
+  // drains in issue order, so loads issued before them would wait for them)
+  if constexpr (PRE) {
+    if (wv < PT) {
+#pragma unroll
+      for (int dt = 0; dt < DV / 32; ++dt)
+#pragma unroll
+        for (int vv = 0; vv < 16; ++vv) mreg[dt][vv] = Ms[(size_t)(wv * 32 + crow(vv, h)) * DV + dt * 32 + col];
+    }
+  }
   const float lam = tid < M ? schi[tid] : kNegInf;   // each thread rewrites only its own entry below
   const float Rn = fmaxf(Rold, rho_t);
   const float sa = fast_exp2(Rold - Rn);          // 0 for an empty state (R = -inf)
