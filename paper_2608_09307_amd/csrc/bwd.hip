@@ -809,7 +809,8 @@ struct StCfg {
   static constexpr int AW = 32 * NA;                 // anchor offsets i - c per row
   static constexpr int WIN = 32 + AW - 1;            // anchor window rows of a chunk
   static constexpr int NT32 = (WIN + 31) / 32;
-  static constexpr int RB = 4;                       // rows per intra-dv flush
+  static constexpr int RB = 2;                       // rows per intra-dv flush (two: the
+                                                     // room goes to full-rate u rows below)
   static constexpr int ES = sizeof(T);
   static constexpr int a16(int x) { return (x + 15) & ~15; }
   static constexpr int oR = 0;
