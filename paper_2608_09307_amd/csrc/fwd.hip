@@ -533,7 +533,7 @@ struct RCfg {
   static constexpr int oOm = 0;
   static constexpr int oMt = oOm + a16(FB * (D + PAD) * ES);
   static constexpr int oA = oMt + a16(DV * (FB + PAD) * ES);
-  static constexpr int oChi = oA + a16(M * 4);
+  static constexpr int oChi = oA + (sizeof(T) == 4 ? a16(M * 4) : 0);   // float32: a of the boundary
   static constexpr int oVt = oChi + a16(BC * (FB + PAD) * ES);
   static constexpr int oR = oVt + a16(DV * (BC + PAD) * ES);
   // u of the window: bf16 inputs as f16 [window row][d] (read transposed, rows
@@ -544,7 +544,9 @@ struct RCfg {
   static constexpr int oUt = oR + a16(WIN * (D + PAD) * ES);
   static constexpr int oQ = oUt + a16(UBYTES);
   static constexpr int oRj = oQ + a16(BC * (D + PAD) * ES);
-  static constexpr int BYTES = oRj + a16(BC * 4);
+  // bf16: the block's slice of a as a 3-row B operand (hi, lo, zero), permuted
+  static constexpr int oAz = oRj + a16(BC * 4);
+  static constexpr int BYTES = oAz + (sizeof(T) == 2 ? a16(3 * (FB + PAD) * ES) : 0);
 };
 
 template <typename T, int D, int DV, int M, int NW, int NA>
@@ -553,6 +555,7 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
   using C = RCfg<T, D, DV, M, NW, NA>;
   constexpr int PAD = C::PAD, FB = C::FB, WIN = C::WIN, UST = C::UST, RPW = C::RPW;
   static_assert(C::BYTES <= 160 * 1024, "readout LDS budget");
+  static_assert(64 * NW >= FB, "one thread per feature of the block");
   __shared__ __align__(16) char smem[C::BYTES];
   T* sOm = (T*)(smem + C::oOm);
   T* sMt = (T*)(smem + C::oMt);
@@ -563,6 +566,7 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
   T* sUt = (T*)(smem + C::oUt);
   T* sQ = (T*)(smem + C::oQ);
   float* sRj = (float*)(smem + C::oRj);
+  T* sAz = (T*)(smem + C::oAz);
 
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
   constexpr int NT = 64 * NW;
@@ -608,11 +612,12 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     sq.load(qs, D, s0, 0, n, tid);
     sc.load((const T*)a.chi + seq * M + fbk * FB, M, s0, 0, n, tid);   // this block's features
     const float rjv = (tid < 32) ? a.rj[seq + min(s0 + tid, n - 1)] : 0.0f;
+    const float azv = (sizeof(T) == 2 && has_bnd && tid < FB) ? bst[(size_t)M * DV + fbk * FB + tid] : 0.0f;
     float av[(M + NT - 1) / NT];
 #pragma unroll
     for (int k = 0; k < (M + NT - 1) / NT; ++k) {
       const int p = tid + NT * k;
-      av[k] = (has_bnd && p < M) ? bst[(size_t)M * DV + p] : 0.0f;
+      av[k] = (sizeof(T) == 4 && has_bnd && p < M) ? bst[(size_t)M * DV + p] : 0.0f;
     }
     if constexpr (sizeof(T) == 2) so.store((f16*)sOm, D + PAD, 0, 0, FB, tid);
     else so.store(sOm, D + PAD, 0, 0, FB, tid);
@@ -627,9 +632,11 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
         for (int e = 0; e < 4; ++e) sMt[(d0 + e) * (FB + PAD) + F::sigma(p)] = has_bnd ? (T)x[e] : (T)0.0f;
       });
     }
+    if constexpr (sizeof(T) == 4) {
 #pragma unroll
-    for (int k = 0; k < (M + NT - 1) / NT; ++k)
-      if (tid + NT * k < M) sA[tid + NT * k] = av[k];
+      for (int k = 0; k < (M + NT - 1) / NT; ++k)
+        if (tid + NT * k < M) sA[tid + NT * k] = av[k];
+    }
     sv.store(s0, 0, n, tid, [&](int jj, int d0, const typename StageRowsT<T, 32, DV, NT>::V4& x) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) sVt[(d0 + e) * (32 + PAD) + F::sigma(jj)] = x[e];
@@ -648,6 +655,15 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     else sq.store(sQ, D + PAD, s0, 0, n, tid);
     sc.store(sChi, FB + PAD, s0, 0, n, tid);
     if (tid < 32) sRj[tid] = (s0 + tid < n) ? rjv : 0.0f;
+    if constexpr (sizeof(T) == 2) {
+      if (tid < FB) {
+        const T hi = (T)azv;
+        const int ps = F::sigma(tid);
+        sAz[ps] = hi;
+        sAz[FB + PAD + ps] = (T)(azv - (float)hi);
+        sAz[2 * (FB + PAD) + ps] = (T)0.0f;
+      }
+    }
   }
   __syncthreads();
 
@@ -720,21 +736,44 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
       float zc = 0.0f;
       // psi in place, boundary part of Z, then the operand-typed copy
       typename F::frag pf[FB / 32][F::CSTEPS];
-      const float* sAh = sA + fb * FB + 4 * h;      // + pt*32 + 8*(v>>2) + (v&3)
+      if constexpr (sizeof(T) == 2) {
+        // bf16: the boundary part of Z (phi(z)^T a over the block's features)
+        // is one more matrix product, of psi as rounded for the boundary
+        // readout of N against the columns (a_hi, a_lo, 0, ...), a_hi + a_lo
+        // being a to 16 significant bits; so N and Z see the same psi
 #pragma unroll
-      for (int pt = 0; pt < FB / 32; ++pt) {
+        for (int pt = 0; pt < FB / 32; ++pt) {
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x4 av = *(const f32x4*)(sAh + pt * 32 + 8 * g);
+          for (int v = 0; v < 16; ++v) accL[pt][v] = fast_exp2(accL[pt][v] + off);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            float psi = fast_exp2(accL[pt][4 * g + e] + off);
-            accL[pt][4 * g + e] = psi;
-            zc += psi * av[e];
-          }
+          for (int sp = 0; sp < F::CSTEPS; ++sp) pf[pt][sp] = F::cfrag(accL[pt], sp);
         }
+        f32x16 accZ = zero16();
+        const T* zrow = sAz + min(col, 2) * (FB + PAD);
 #pragma unroll
-        for (int sp = 0; sp < F::CSTEPS; ++sp) pf[pt][sp] = F::cfrag(accL[pt], sp);
+        for (int pt = 0; pt < FB / 32; ++pt)
+#pragma unroll
+          for (int sp = 0; sp < F::CSTEPS; ++sp)
+            accZ = F::mma(pf[pt][sp], F::ldc(zrow, pt * 32, sp, h), accZ);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) zc += accZ[v];
+      } else {
+        const float* sAh = sA + fb * FB + 4 * h;      // + pt*32 + 8*(v>>2) + (v&3)
+#pragma unroll
+        for (int pt = 0; pt < FB / 32; ++pt) {
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const f32x4 av = *(const f32x4*)(sAh + pt * 32 + 8 * g);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              float psi = fast_exp2(accL[pt][4 * g + e] + off);
+              accL[pt][4 * g + e] = psi;
+              zc += psi * av[e];
+            }
+          }
+#pragma unroll
+          for (int sp = 0; sp < F::CSTEPS; ++sp) pf[pt][sp] = F::cfrag(accL[pt], sp);
+        }
       }
       zc *= sb;
       // intra-chunk causal correction: P^T[j, anchor] = chi_j . psi_anchor, scaled
