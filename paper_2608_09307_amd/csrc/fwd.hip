@@ -527,7 +527,7 @@ struct RCfg {
   static constexpr int NFB = M / FB;
   static constexpr int WIN = BC + 32 * NA - 1;           // anchor rows the chunk can touch
   static constexpr int UST = ((WIN + 2) / 4) * 4 + 2;   // odd dword stride: conflict-free 2-byte column reads
-  static constexpr int RPW = BC / NW;
+  static constexpr int RPW = (BC + NW - 1) / NW;
   static constexpr int ES = sizeof(T);
   static constexpr int a16(int x) { return (x + 15) & ~15; }
   static constexpr int oOm = 0;
@@ -672,7 +672,7 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
   for (int rr = 0; rr < RPW; ++rr) {
     const int t = wv + NW * rr;
     const int i = s0 + t;
-    if (i >= n) continue;
+    if (t >= C::BC || i >= n) continue;
     float nacc[DV / 32];
     float zacc = 0.0f, Lrun = kNegInf;
 #pragma unroll
@@ -895,7 +895,11 @@ __global__ __launch_bounds__(256) void k_merge_blocks(FwdArgs a) {
 // ---------------------------------------------------------------------------
 template <typename T, int D, int DV, int M, int NA>
 static int run_fwd(const Shape& s, FwdArgs a, hipStream_t st) {
-  constexpr int NW = 8;
+  // readout waves per workgroup: the workgroup's LDS fills a CU, so its wave
+  // count sets the occupancy; 12 waves (three per SIMD, at most 168 registers
+  // each) hide more of each row's dependent matrix-core / VALU chain than 8,
+  // although four of them get two of the chunk's 32 rows instead of three
+  constexpr int NW = 12;
   const int BH = (int)s.BH();
   const int nch = (int)s.nch();
   {
