@@ -127,7 +127,8 @@ struct AsCfg {
   static constexpr int oR = oQ + a16(32 * (D + PAD) * ES);                  // r of the anchor tile
   static constexpr int oU = oR + a16(32 * RST * ES);                        // u of the anchor tile
   static constexpr int oRj = oU + a16(32 * (DV + PAD) * ES);                // R_j of the chunk
-  static constexpr int oA = oRj + a16(32 * 4);                              // boundary a
+  static constexpr int oRat = oRj + a16(32 * 4);                            // 2^(R_j - Rref) of the chunk
+  static constexpr int oA = oRat + a16(32 * 4);                             // boundary a
   static constexpr int oW = oA + a16(FB * 4);                               // per wave: dN (DV), s_c (32)
   static constexpr int oOb = oW + a16(NW * (DV + 32) * 4);                 // Omega*log2 e, operand type (dz)
   static constexpr int BYTES0 = oOb + a16(FB * (D + TPD) * ES);
@@ -213,19 +214,16 @@ LS_DEV void query_features(PF (&pf)[FB / 32][MF<T>::CSTEPS], const T* qrow,
   }
 }
 
-// frame ratios 2^(R_j - R_i) of the chunk tokens j <= t for the registers' rows j
-// (all sixteen computed, later tokens then zeroed: no branches around the reads)
-LS_DEV void frame_ratios(float (&sj)[16], const float* sRj, int t, float Ri) {
+// frame ratios 2^(R_j - Rref) of the chunk's rows (sRat), masked to j <= t, for
+// the registers' rows j (all sixteen read, later rows then zeroed: no branches)
+LS_DEV void masked_ratios(float (&sj)[16], const float* sRat, int t) {
   const int h = lane_id() >> 5;
-  const float* sRjh = sRj + 4 * h;
+  const float* sh = sRat + 4 * h;
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
-    const f32x4 r4 = *(const f32x4*)(sRjh + 8 * g);
+    const f32x4 r4 = *(const f32x4*)(sh + 8 * g);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const float x = fast_exp2(r4[e] - Ri);
-      sj[4 * g + e] = (8 * g + 4 * h + e <= t) ? x : 0.0f;
-    }
+    for (int e = 0; e < 4; ++e) sj[4 * g + e] = (8 * g + 4 * h + e <= t) ? r4[e] : 0.0f;
   }
 }
 
@@ -235,7 +233,9 @@ LS_DEV void frame_ratios(float (&sj)[16], const float* sRj, int t, float Ri) {
 // chunk kt and the key features, values and queries of chunks kt .. kt+NA
 // (NA = ceil(w / 32) anchor tiles per row); the state of any row i that sees
 // the tile is then the boundary part plus a tail of at most NA + 1 chunks,
-//   M^(i) = 2^(Rex_kt - R_i) M_b + sum_{c0 <= j <= i} 2^(R_j - R_i) chi_j v_j^T.
+//   M^(i) = 2^(Rex_kt - R_i) M_b + sum_{c0 <= j <= i} 2^(R_j - R_i) chi_j v_j^T
+// (computed in the reference frame Rref = Rex_kt, the row factor 2^(Rref - R_i)
+// applied to dN_i once).
 // Row t of chunk kt sees anchors c <= t of the tile and row t of chunk kt+NA
 // anchors c > t only (w <= 32 NA): the two run as one pair, each lane c taking
 // the row that sees anchor c, so the logits, features and boundary product are
@@ -260,7 +260,8 @@ struct DuCfg {
   static constexpr int oQ = oV + a16(ROWS * VST * ES);
   static constexpr int oR = oQ + a16(ROWS * (D + PAD) * ES); // r of the anchor tile
   static constexpr int oRj = oR + a16(32 * (D + PAD) * ES);  // R_j of the staged rows
-  static constexpr int BYTES0 = oRj + a16(ROWS * 4);
+  static constexpr int oRat = oRj + a16(ROWS * 4);           // 2^(R_j - Rref) of the staged rows
+  static constexpr int BYTES0 = oRat + a16(ROWS * 4);
   static constexpr int RED = (NW / 2) * 32 * DV * 4;         // end-of-sweep reduction
   static constexpr int BYTES = mx(BYTES0, RED);
 };
@@ -281,6 +282,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
   T* sQ = (T*)(smem + C::oQ);
   T* sR = (T*)(smem + C::oR);
   float* sRj = (float*)(smem + C::oRj);
+  float* sRat = (float*)(smem + C::oRat);
 
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
   const int kt = blockIdx.x, bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
@@ -294,6 +296,11 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
   const T* omq_h = (const T*)a.omq + (size_t)hh * M * D;
   const bool has_bnd = kt > 0;
   const float Rexb = a.rex[(size_t)bh * (nch + 1) + kt];
+  // reference frame of the staged rows: the boundary frame (the first chunk,
+  // whose boundary state is zero, takes R of its first row); then
+  //   A_ic = 2^(Rref - R_i) [psi_c^T M_b + sum_{c0 <= j <= i} 2^(R_j - Rref) (chi_j . psi_c) v_j^T]
+  // and the row factor 2^(Rref - R_i) goes into dN_i
+  const float Rref = uniform(has_bnd ? Rexb : a.rj[seq + c0]);
 
   // ---- staging, once per workgroup ----
   {
@@ -341,7 +348,11 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
     sq.load(qs, D, c0, 0, n, tid);
     if constexpr (sizeof(T) == 2) sq.store((f16*)sQ, D + PAD, c0, 0, n, tid);
     else sq.store(sQ, D + PAD, c0, 0, n, tid);
-    for (int j = tid; j < ROWS; j += NT) sRj[j] = (c0 + j < n) ? a.rj[seq + c0 + j] : 0.0f;
+    for (int j = tid; j < ROWS; j += NT) {
+      const float rj = (c0 + j < n) ? a.rj[seq + c0 + j] : 0.0f;
+      sRj[j] = rj;
+      sRat[j] = (c0 + j < n) ? fast_exp2(rj - Rref) : 0.0f;
+    }
   }
   __syncthreads();
 
@@ -367,27 +378,22 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
     const float LA = uniform(a.stats[(seq + iAc) * 2]), LB = uniform(a.stats[(seq + iBc) * 2]);
     const float invA = uniform(a.rowstat[(seq + iAc) * 2]), invB = uniform(a.rowstat[(seq + iBc) * 2]);
     const float RA = uniform(okA ? sRj[rcA * 32 + t] : -kNegInf), RB = uniform(okB ? sRj[32 * NA + t] : -kNegInf);
-    const float sbA = uniform(has_bnd ? fast_exp2(Rexb - RA) : 0.0f);
-    const float sbB = uniform(has_bnd ? fast_exp2(Rexb - RB) : 0.0f);
+    // dN with the row factor 2^(Rref - R_i) (zero for a row that does not take part)
+    const float sbA = uniform(fast_exp2(Rref - RA)), sbB = uniform(fast_exp2(Rref - RB));
     float dNA[DV / 32], dNB[DV / 32];
 #pragma unroll
     for (int dt = 0; dt < DV / 32; ++dt) {
-      dNA[dt] = tof(gs[(size_t)iAc * DV + dt * 32 + col]) * invA;
-      dNB[dt] = pair ? tof(gs[(size_t)iBc * DV + dt * 32 + col]) * invB : 0.0f;
+      dNA[dt] = tof(gs[(size_t)iAc * DV + dt * 32 + col]) * (invA * sbA);
+      dNB[dt] = pair ? tof(gs[(size_t)iBc * DV + dt * 32 + col]) * (invB * sbB) : 0.0f;
     }
-    // boundary scale of each register's anchor row (registers crow(v, h) > t: row B)
-    float sbv[16];
-#pragma unroll
-    for (int v = 0; v < 16; ++v) sbv[v] = (pair && crow(v, h) > t) ? sbB : sbA;
     // this lane's row: the one that sees anchor c0 + col
     const bool useB = pair && col > t;
     const int i = useB ? iB : iA;
     const int rc = useB ? NA : rcA;
-    const float Ri = useB ? RB : RA;
     const bool valid = (useB ? okB : okA) && (i - c0 - col >= 0) && (i - c0 - col < w);
     typename F::frag pf[FB / 32][F::CSTEPS];
     query_features<T, D, FB>(pf, sQ + (rc * 32 + t) * (D + PAD), sR + col * (D + PAD), sOm, valid, useB ? LB : LA);
-    // tails: P^T[j, c] = chi_j . psi_c of chunk kt + rj, framed, j <= row(c)
+    // tails: P^T[j, c] = chi_j . psi_c of chunk kt + rj, times 2^(R_j - Rref), j <= row(c)
     constexpr int NTL = NA + 1;
     typename F::frag ppf[NTL][F::CSTEPS];
     const int ntl = okB ? NTL : rcA + 1;                        // tails any lane needs
@@ -406,15 +412,12 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
         for (int sp = 0; sp < F::CSTEPS; ++sp)
           accP = F::mma(F::ldc(chirow, pt * 32, sp, h), pf[pt][sp], accP);
       const int lim = rj < rc ? 31 : (rj == rc ? t : -1);      // last token of chunk rj this lane's row sees
-      const float* sRjh = sRj + rj * 32 + 4 * h;
+      const float* sRh = sRat + rj * 32 + 4 * h;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const f32x4 r4 = *(const f32x4*)(sRjh + 8 * g);
+        const f32x4 r4 = *(const f32x4*)(sRh + 8 * g);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float x = fast_exp2(r4[e] - Ri);
-          accP[4 * g + e] *= (8 * g + 4 * h + e <= lim) ? x : 0.0f;
-        }
+        for (int e = 0; e < 4; ++e) accP[4 * g + e] *= (8 * g + 4 * h + e <= lim) ? r4[e] : 0.0f;
       }
 #pragma unroll
       for (int sp = 0; sp < F::CSTEPS; ++sp) ppf[rj][sp] = F::cfrag(accP, sp);
@@ -435,10 +438,6 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
 #pragma unroll
           for (int g = 0; g < G; ++g)
             accA[g] = F::mma(pf[pt][sp], F::ldc(sMt + ((d0 + g) * 32 + col) * (FB + PAD), pt * 32, sp, h), accA[g]);
-#pragma unroll
-      for (int g = 0; g < G; ++g)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) accA[g][v] *= sbv[v];
 #pragma unroll
       for (int rj = 0; rj < NTL; ++rj) {
         if (rj >= ntl) continue;
@@ -499,6 +498,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
   T* sU = (T*)(smem + C::oU);
   float* sRj = (float*)(smem + C::oRj);
   float* sA = (float*)(smem + C::oA);
+  float* sRat = (float*)(smem + C::oRat);
 
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
   float* sDN = (float*)(smem + C::oW) + wv * (DV + 32);
@@ -544,6 +544,11 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
     const int s0 = ch * 32;
     const bool has_bnd = ch > 0;
     const float Rexb = a.rex[(size_t)bh * (nch + 1) + ch];
+    // reference frame of the chunk's rows: the boundary frame (the first chunk,
+    // whose boundary state is zero, takes R of its first row); with it
+    //   dpsi = 2^(Rref - R_i) [M_b dA + dZ a_b + sum_{j <= i} 2^(R_j - Rref) chi_j (v_j . dA + dZ)]
+    // and the row factor 2^(Rref - R_i) goes into dN and dZ once per row
+    const float Rref = uniform(has_bnd ? Rexb : a.rj[seq + s0]);
     {
       // the chunk's global loads, each batch issued in full before its LDS
       // stores (float32 inputs: the state in two halves, the second with
@@ -587,7 +592,10 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       sv.store(sV, C::VST, s0, 0, n, tid);
       if constexpr (sizeof(T) == 2) sq.store((f16*)sQ, D + PAD, s0, 0, n, tid);
       else sq.store(sQ, D + PAD, s0, 0, n, tid);
-      if (tid < 32) sRj[tid] = (s0 + tid < n) ? rjv : 0.0f;
+      if (tid < 32) {
+        sRj[tid] = (s0 + tid < n) ? rjv : 0.0f;
+        sRat[tid] = (s0 + tid < n) ? fast_exp2(rjv - Rref) : 0.0f;
+      }
     }
     __syncthreads();
 
@@ -613,10 +621,12 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       const float inv = uniform(a.rowstat[(seq + i) * 2]);
       const float dZ = uniform(a.rowstat[(seq + i) * 2 + 1]);
       const float Ri = uniform(sRj[t]);
-      const float sb = uniform(has_bnd ? fast_exp2(Rexb - Ri) : 0.0f);
+      const float sbr = uniform(fast_exp2(Rref - Ri));
+      const float dZr = dZ * sbr;
+      const float invr = inv * sbr;
 #pragma unroll
       for (int e = 0; e < NG; ++e)
-        if (e * 64 + l < DV) sDN[e * 64 + l] = gv[e] * inv;
+        if (e * 64 + l < DV) sDN[e * 64 + l] = gv[e] * invr;
       const T* qrow = sQ + t * (D + PAD);
       float qD[D / 32];
 #pragma unroll
@@ -647,15 +657,16 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
           daf[s] = F::ld(urow, k0) * sDN[k0];
         }
       }
-      // Q^T[j, c] = (v_j . dA_c + dZ_i) 2^(R_j - R_i), j <= i  (regs <-> j, lanes <-> anchor)
+      // Q^T[j, c] = (v_j . dA_c + dZ_i) 2^(R_j - Rref), j <= i  (regs <-> j, lanes <-> anchor;
+      // dA and dZ carry the row factor)
       f32x16 accQ = zero16();
 #pragma unroll
       for (int s = 0; s < DV / F::KS; ++s)
         accQ = F::mma(F::ld(sV + col * C::VST, s * F::KS + h * F::KPL), daf[s], accQ);
       float sj[16];
-      frame_ratios(sj, sRj, t, Ri);
+      masked_ratios(sj, sRat, t);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) accQ[v] = (accQ[v] + dZ) * sj[v];
+      for (int v = 0; v < 16; ++v) accQ[v] = (accQ[v] + dZr) * sj[v];
       typename F::frag qqf[F::CSTEPS];
 #pragma unroll
       for (int sp = 0; sp < F::CSTEPS; ++sp) qqf[sp] = F::cfrag(accQ, sp);
@@ -665,7 +676,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
 #pragma unroll
       for (int pt = 0; pt < FB / 32; ++pt) {
         no_hoist();
-        // boundary part sb_i (M_b dA_c + dZ_i a_b), zero in the first chunk
+        // boundary part M_b dA_c + dZ_i a_b (row factor in dA, dZ), zero in the first chunk
         f32x16 dps = zero16();
 #pragma unroll
         for (int s = 0; s < DV / F::KS; ++s)
@@ -675,7 +686,7 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
         for (int g = 0; g < 4; ++g) {
           const f32x4 av = *(const f32x4*)(sAh + 8 * g);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) dps[4 * g + e] = (dps[4 * g + e] + dZ * av[e]) * sb;
+          for (int e = 0; e < 4; ++e) dps[4 * g + e] = __builtin_fmaf(dZr, av[e], dps[4 * g + e]);
         }
         // chi^T rows p, k = token j in crow order (chi stored [j][sigma(p)])
 #pragma unroll
