@@ -580,6 +580,15 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
         if (has_bnd) sm.load(bst + (size_t)(fb * FB + FH) * DV, tid);
       }
       if (tid < FB) sA[tid] = av;
+      if constexpr (sizeof(T) == 2) {
+        // bf16: a_b rides in the padding of M_b's row p as one more k-step of
+        // the boundary product, (a_hi, a_hi, a_lo, 0, ...) against the row's
+        // (dZ_hi, dZ_lo, dZ_hi, 0, ...): a_b dZ to about 16 bits
+        if (tid < FB) {
+          const bf16 ah = (bf16)av, al = (bf16)(av - (float)ah), z = (bf16)0.0f;
+          *(bf16x8*)(sMp + tid * (DV + PAD) + DV) = bf16x8{ah, ah, al, z, z, z, z, z};
+        }
+      }
       StageRows<T, 32, FB, NT> sc;
       StageRows<T, 32, DV, NT> sv;
       StageRows<T, 32, D, NT> sq;
@@ -670,6 +679,12 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
       typename F::frag qqf[F::CSTEPS];
 #pragma unroll
       for (int sp = 0; sp < F::CSTEPS; ++sp) qqf[sp] = F::cfrag(accQ, sp);
+      // the boundary product's k-step for dZ a_b (bf16; lanes of the upper half zero)
+      typename F::frag zb = F::zero();
+      if constexpr (sizeof(T) == 2) {
+        const bf16 zh = (bf16)dZr, zl = (bf16)(dZr - (float)zh);
+        if (h == 0) { zb[0] = zh; zb[1] = zl; zb[2] = zh; }
+      }
       // dell = dpsi (*) psi (derivative with respect to the natural-log feature)
       typename F::frag dlf[FB / 32][F::CSTEPS];
       float sc = 0.0f;
@@ -681,12 +696,16 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
 #pragma unroll
         for (int s = 0; s < DV / F::KS; ++s)
           dps = F::mma(F::ld(sMp + (pt * 32 + col) * (DV + PAD), s * F::KS + h * F::KPL), daf[s], dps);
-        const float* sAh = sA + pt * 32 + 4 * h;
+        if constexpr (sizeof(T) == 2) {
+          dps = F::mma(*(const bf16x8*)(sMp + (pt * 32 + col) * (DV + PAD) + DV), zb, dps);
+        } else {
+          const float* sAh = sA + pt * 32 + 4 * h;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x4 av = *(const f32x4*)(sAh + 8 * g);
+          for (int g = 0; g < 4; ++g) {
+            const f32x4 av = *(const f32x4*)(sAh + 8 * g);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) dps[4 * g + e] = __builtin_fmaf(dZr, av[e], dps[4 * g + e]);
+            for (int e = 0; e < 4; ++e) dps[4 * g + e] = __builtin_fmaf(dZr, av[e], dps[4 * g + e]);
+          }
         }
         // chi^T rows p, k = token j in crow order (chi stored [j][sigma(p)])
 #pragma unroll
