@@ -285,7 +285,8 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_du(BwdArgs a) {
   float* sRat = (float*)(smem + C::oRat);
 
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
-  const int kt = blockIdx.x, bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
+  const int2 gxy = xcd_grid_xy();
+  const int kt = gxy.x, bh = gxy.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
   const int c0 = kt * 32, w = a.w;
   const size_t seq = (size_t)bh * n;
   const T* qs = (const T*)a.q + seq * D;
@@ -503,7 +504,8 @@ __global__ __launch_bounds__(64 * 8) void k_bwd_dqdr(BwdArgs a) {
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
   float* sDN = (float*)(smem + C::oW) + wv * (DV + 32);
   float* sSc = sDN + DV;
-  const int kt = blockIdx.x, bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
+  const int2 gxy = xcd_grid_xy();
+  const int kt = gxy.x, bh = gxy.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
   const int c0 = kt * 32, w = a.w;
   const size_t seq = (size_t)bh * n;
   const T* qs = (const T*)a.q + seq * D;
@@ -910,7 +912,8 @@ __global__ __launch_bounds__(256, (NA <= 2 ? 2 : 1)) void k_bwd_state(BwdArgs a)
 
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
   T* sQ = (T*)(smem + C::oQ) + wv * D;
-  const int cb = blockIdx.x, bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
+  const int2 gxy = xcd_grid_xy();
+  const int cb = gxy.x, bh = gxy.y, hh = bh % a.H, n = a.n, nch = a.nch, fb = blockIdx.z;
   const int s0 = cb * 32;
   const int wb = s0 - (AW - 1);                // window row 0 = anchor s0 - (AW - 1)
   const int tlast = min(31, n - 1 - s0);

@@ -37,6 +37,19 @@ static constexpr float kNegInf = -__builtin_inff();
 
 LS_DEV int lane_id() { return threadIdx.x & 63; }
 
+// Workgroups are dealt to the eight XCDs in turn by linear id (x fastest, then
+// y).  This maps the (x, y) grid so that each XCD gets one contiguous run of it
+// (runs of x for a fixed y first): neighbouring tiles, which stage the same
+// rows, then share one L2.  A bijection when gridDim.x * gridDim.y is a
+// multiple of 8; the plain order otherwise.
+LS_DEV int2 xcd_grid_xy() {
+  const int gx = (int)gridDim.x, nxy = gx * (int)gridDim.y;
+  const int lin = (int)blockIdx.x + gx * (int)blockIdx.y;
+  if (nxy % 8 != 0) return int2{(int)blockIdx.x, (int)blockIdx.y};
+  const int v = (lin & 7) * (nxy >> 3) + (lin >> 3);
+  return int2{v % gx, v / gx};
+}
+
 template <typename T> struct MF;
 
 template <> struct MF<bf16> {

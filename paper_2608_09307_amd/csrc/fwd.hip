@@ -570,7 +570,8 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
 
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
   constexpr int NT = 64 * NW;
-  const int cb = blockIdx.x, bh = blockIdx.y, hh = bh % a.H, n = a.n, nch = a.nch;
+  const int2 gxy = xcd_grid_xy();
+  const int cb = gxy.x, bh = gxy.y, hh = bh % a.H, n = a.n, nch = a.nch;
   const int s0 = cb * 32;
   const int wb = s0 - (32 * NA - 1);
   constexpr int S = M * DV + M;
