@@ -85,13 +85,24 @@ __global__ __launch_bounds__(256) void k_chunk_state(FwdArgs a) {
   f32x16 acc[M / 32];
   float nk = 0.0f;
   if (active) {
-    // V^T of the chunk, token index permuted (it pairs with a register operand)
-    for (int idx = l; idx < 32 * (DV / 4); idx += 64) {
-      int jj = idx % 32, d0 = (idx / 32) * 4;
-      bool ok = tok0 + jj < n;
+    // V^T of the chunk, token index permuted (it pairs with a register operand):
+    // every 16-byte row piece is loaded first (rows clamped), then stored transposed
+    constexpr int VE = 16 / (int)sizeof(T);
+    constexpr int IT = 32 * (DV / VE) / 64;
+    static_assert(32 * (DV / VE) % 64 == 0, "whole pieces per lane");
+    typedef T VP __attribute__((ext_vector_type(VE)));
+    VP xv[IT];
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        sVt[wv][d0 + e][F::sigma(jj)] = ok ? vs[(size_t)(tok0 + jj) * DV + d0 + e] : (T)0.0f;
+    for (int it = 0; it < IT; ++it) {
+      const int idx = l + 64 * it, jj = idx % 32, d0 = (idx / 32) * VE;
+      xv[it] = *(const VP*)(vs + (size_t)min(tok0 + jj, n - 1) * DV + d0);
+    }
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = l + 64 * it, jj = idx % 32, d0 = (idx / 32) * VE;
+      const bool ok = tok0 + jj < n;
+#pragma unroll
+      for (int e = 0; e < VE; ++e) sVt[wv][d0 + e][F::sigma(jj)] = ok ? xv[it][e] : (T)0.0f;
     }
     key_logits<T, D, M, false>(acc, nk, ks, tok0, n, omk_h);
     if (h == 0) snk[wv][col] = nk;
@@ -103,8 +114,9 @@ __global__ __launch_bounds__(256) void k_chunk_state(FwdArgs a) {
   for (int pt = 0; pt < M / 32; ++pt)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      int tk = crow(v, h);
-      float x = (tok0 + tk < n) ? acc[pt][v] - 0.5f * kLog2e * snk[wv][tk] : kNegInf;
+      const int tk = crow(v, h);
+      const float nkt = snk[wv][tk];
+      float x = (tok0 + tk < n) ? acc[pt][v] - 0.5f * kLog2e * nkt : kNegInf;
       acc[pt][v] = x;
       mx = fmaxf(mx, x);
     }

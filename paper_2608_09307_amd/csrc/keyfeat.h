@@ -23,7 +23,8 @@ LS_DEV void key_logits(f32x16 (&acc)[M / 32], float& nk, const T* __restrict__ k
 #pragma unroll 1
   for (int s = 0; s < D / F::KS; ++s) {
     const int k0 = s * F::KS + h * F::KPL;
-    typename F::frag kf = vj ? F::ld(kseq + (size_t)j * D, k0) : F::zero();
+    typename F::frag kf = F::ld(kseq + (size_t)min(j, n - 1) * D, k0);
+    if (!vj) kf = F::zero();
 #pragma unroll
     for (int e = 0; e < F::KPL; ++e) { float x = fel(kf, e); nk += x * x; }
 #pragma unroll
