@@ -278,42 +278,6 @@ LS_DEV float half_reduce16(const float (&x)[16]) {
   return s + dpp<0xB1>(s);
 }
 
-// x[i] for a wave-uniform index i without dynamic register indexing
-template <int N> LS_DEV float pick(const float (&x)[N], int i) {
-  float r = x[0];
-#pragma unroll
-  for (int j = 1; j < N; ++j) r = (i == j) ? x[j] : r;
-  return r;
-}
-template <int N> LS_DEV void add_at(float (&x)[N], int i, float v) {
-#pragma unroll
-  for (int j = 0; j < N; ++j) x[j] += (i == j) ? v : 0.0f;
-}
-
-// ---- cooperative global -> LDS copies (block-wide) ----
-// 2D copy of a [rows][cols] T matrix (global row stride gstride) into LDS with
-// row stride lstride; rows >= valid_rows (or < 0 via row offset) become zero.
-template <typename T>
-LS_DEV void copy_rows(T* lds, int lstride, const T* g, int gstride, int rows, int cols,
-                      int row0, int valid_lo, int valid_hi, int tid, int nthreads) {
-  // row r of the LDS tile is global row row0 + r; valid if in [valid_lo, valid_hi)
-  const int vec = (sizeof(T) == 2) ? 8 : 4;   // 16-byte chunks
-  const int cpr = cols / vec;
-  for (int idx = tid; idx < rows * cpr; idx += nthreads) {
-    int rr = idx / cpr, cc = (idx % cpr) * vec;
-    int grow = row0 + rr;
-    T* dst = lds + rr * lstride + cc;
-    if (grow >= valid_lo && grow < valid_hi) {
-      const T* src = g + (size_t)grow * gstride + cc;
-#pragma unroll
-      for (int e = 0; e < vec; ++e) dst[e] = src[e];
-    } else {
-#pragma unroll
-      for (int e = 0; e < vec; ++e) dst[e] = (T)0.0f;
-    }
-  }
-}
-
 // ---- composite-query logits from f16 operands (bf16 inputs) ----
 // q, r and Omega*log2(e) are kept in LDS as f16 (converted once per row,
 // anchor window or workgroup), so z = q (*) r takes four packed f16
@@ -346,37 +310,6 @@ LS_DEV float logits_f16(f32x16 (&acc)[FB / 32], const f16* qrow, const f16* rrow
       acc[pt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(*(const f16x8*)(om + (pt * 32 + col) * LD + k0), z, acc[pt], 0, 0, 0);
   }
   return half_swap_add(nz);
-}
-
-// rows [row0, row0 + rows) of a [*, gstride] matrix (bf16 or float) into LDS
-// as Tout (row stride lstride), times `scale`; rows outside [valid_lo,
-// valid_hi) become zero.
-template <typename Tout, typename Tin>
-LS_DEV void copy_rows_as(Tout* lds, int lstride, const Tin* g, int gstride, int rows, int cols, int row0,
-                         int valid_lo, int valid_hi, int tid, int nthreads, float scale = 1.0f) {
-  const int cpr = cols / 4;
-  for (int idx = tid; idx < rows * cpr; idx += nthreads) {
-    const int rr = idx / cpr, cc = (idx % cpr) * 4;
-    const int grow = row0 + rr;
-    typedef Tout V4 __attribute__((ext_vector_type(4)));
-    V4 x;
-    if (grow >= valid_lo && grow < valid_hi) {
-      const Tin* src = g + (size_t)grow * gstride + cc;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) x[e] = (Tout)((float)src[e] * scale);
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) x[e] = (Tout)0.0f;
-    }
-    *(V4*)(lds + rr * lstride + cc) = x;
-  }
-}
-
-// the same into f16 (q, r and Omega*log2(e) of the f16 logits)
-template <typename Tin>
-LS_DEV void copy_rows_f16(f16* lds, int lstride, const Tin* g, int gstride, int rows, int cols, int row0,
-                          int valid_lo, int valid_hi, int tid, int nthreads, float scale = 1.0f) {
-  copy_rows_as<f16, Tin>(lds, lstride, g, gstride, rows, cols, row0, valid_lo, valid_hi, tid, nthreads, scale);
 }
 
 // crow-order operand fragment (see MF<bf16>::tld_crow) of a 16-bit matrix
