@@ -269,10 +269,14 @@ __global__ __launch_bounds__(256) void k_keyfeat(FwdArgs a) {
     if (col >= o) R = fmaxf(R, t);
   }
   R = fmaxf(R, a.rex[(size_t)bh * (nch + 1) + cb]);
-  if (!vt) return;
-  if (h == 0) a.rj[seq + s0 + col] = R;
+  if (vt && h == 0) a.rj[seq + s0 + col] = R;
   const float rsm = rsqrtf((float)M);
-  T* row = (T*)a.chi + (seq + s0 + col) * M;
+  // the wave's 32 x M tile goes through LDS, so that the global stores are
+  // whole 16-byte pieces of rows (lanes along a row) instead of 8-byte pieces
+  // of 32 different rows
+  constexpr int CP = M + 16 / (int)sizeof(T);              // row pitch (elements)
+  __shared__ __align__(16) T sX[4][32][CP];
+  T* xr = &sX[wv][col][0];
 #pragma unroll
   for (int pt = 0; pt < M / 32; ++pt)
 #pragma unroll
@@ -281,8 +285,18 @@ __global__ __launch_bounds__(256) void k_keyfeat(FwdArgs a) {
       V4 x4;
 #pragma unroll
       for (int e = 0; e < 4; ++e) x4[e] = (T)(fast_exp2(acc[pt][4 * g + e] - R) * rsm);
-      *(V4*)(row + F::sigma(pt * 32 + 8 * g + 4 * h)) = x4;   // sigma keeps 4-groups contiguous
+      *(V4*)(xr + F::sigma(pt * 32 + 8 * g + 4 * h)) = x4;   // sigma keeps 4-groups contiguous
     }
+  wave_lds_sync();
+  constexpr int VE = 16 / (int)sizeof(T), PPR = M / VE;    // 16-byte pieces per row
+  typedef T V __attribute__((ext_vector_type(VE)));
+  T* dst = (T*)a.chi + (seq + s0) * M;
+  const int nrow = min(32, n - s0);
+#pragma unroll
+  for (int it = 0; it < 32 * PPR / 64; ++it) {
+    const int idx = l + 64 * it, r = idx / PPR, c = (idx % PPR) * VE;
+    if (r < nrow) *(V*)(dst + (size_t)r * M + c) = *(const V*)(&sX[wv][r][c]);
+  }
 }
 
 // ---------------------------------------------------------------------------
