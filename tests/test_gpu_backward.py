@@ -113,6 +113,14 @@ def test_backward_wide_windows(D, m, w, n, dt):
     _run(Workload("wide_bwd", 1, 2, n, D, D, m, w, dt, "fwdbwd", seed=42))
 
 
+@pytest.mark.parametrize("D,m,n,w,dt", [(128, 128, 250, 64, "bf16"), (64, 64, 200, 40, "f32")])
+def test_backward_tile_grid_multiple_of_8(D, m, n, w, dt):
+    """Tiles x heads a multiple of eight (here 8 x 4 and 7 x 8): the sweeps
+    deal their tiles to the XCDs in contiguous runs, every row checked."""
+    B, H = (2, 2) if n == 250 else (2, 4)
+    _run(Workload("grid8_bwd", B, H, n, D, D, m, w, dt, "fwdbwd", seed=36))
+
+
 def test_backward_layer16k_sampled_heads():
     _run(WORKLOADS["layer16k_bf16"], pairs=[(1, 9), (0, 2)])
 

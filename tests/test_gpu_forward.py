@@ -69,6 +69,14 @@ def test_bf16_shapes_reduced_n(D, m, n, w):
     _run_and_compare(wl)
 
 
+@pytest.mark.parametrize("D,m,n,w,dt", [(128, 128, 250, 64, "bf16"), (64, 64, 200, 40, "f32")])
+def test_tile_grid_multiple_of_8(D, m, n, w, dt):
+    """Chunks x heads a multiple of eight (here 8 x 4 and 7 x 8): the readout
+    deals its chunks to the XCDs in contiguous runs, every row checked."""
+    B, H = (2, 2) if n == 250 else (2, 4)
+    _run_and_compare(Workload("grid8_fwd", B, H, n, D, D, m, w, dt, "fwd", seed=6))
+
+
 def test_layer16k_bf16_sampled_heads():
     wl = WORKLOADS["layer16k_bf16"]
     _run_and_compare(wl, pairs=[(0, 3), (1, 14), (1, 0)])
