@@ -48,11 +48,13 @@ struct DCfg {
 
 // LDS staging in which every thread issues all of its 16-byte global loads
 // before its first LDS store (one memory round trip per call, not per element).
-// Ring rows c < w come from `ring` ([w][COLS]), row `slot` from `fresh` when it
-// is given, rows w .. ROWS-1 are zero.  TRANS stores column-major with the
-// row index permuted by MF<T>::sigma (the readout's anchor operand layout).
+// Ring rows c < nv come from `ring` ([w][COLS]), row `slot` from `fresh` when
+// it is given; rows nv .. ROWS-1 (nv <= w: past the window, or slots that hold
+// no token yet) are zero, so that a product with them needs no mask.  TRANS
+// stores column-major with the row index permuted by MF<T>::sigma (the
+// readout's anchor operand layout).
 template <typename T, int ROWS, int COLS, bool TRANS>
-LS_DEV void stage_ring(T* dst, int ldst, const T* ring, const T* fresh, int slot, int w, int tid) {
+LS_DEV void stage_ring(T* dst, int ldst, const T* ring, const T* fresh, int slot, int w, int nv, int tid) {
   constexpr int VE = 16 / sizeof(T);
   constexpr int CPR = COLS / VE;
   constexpr int N = ROWS * CPR;
@@ -61,7 +63,7 @@ LS_DEV void stage_ring(T* dst, int ldst, const T* ring, const T* fresh, int slot
   V x[IT];
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
-    // unconditional loads (row clamped into the ring); rows past w are zeroed below
+    // unconditional loads (row clamped into the ring); rows from nv on are zeroed below
     const int idx = min(tid + 256 * it, N - 1), c = idx / CPR, e = (idx % CPR) * VE;
     const int cr = c < w ? c : w - 1;
     x[it] = *(const V*)((fresh != nullptr && cr == slot) ? fresh + e : ring + (size_t)cr * COLS + e);
@@ -70,7 +72,7 @@ LS_DEV void stage_ring(T* dst, int ldst, const T* ring, const T* fresh, int slot
   for (int it = 0; it < IT; ++it) {
     const int idx = tid + 256 * it, c = idx / CPR, e = (idx % CPR) * VE;
     if (idx >= N) continue;
-    if (c >= w) {
+    if (c >= nv) {
 #pragma unroll
       for (int k = 0; k < VE; ++k) x[it][k] = (T)0.0f;
     }
@@ -162,6 +164,25 @@ LS_DEV float key_log2_features(const float* sk, const float* om, float* lam, flo
   return fmaxf(fmaxf(sred[0], sred[1]), fmaxf(sred[2], sred[3]));
 }
 
+// z = q (*) r of one anchor at one k-step as an operand fragment (q float32
+// in LDS, read in full for every lane), its |z|^2 summed into nz
+template <typename T>
+LS_DEV void composite_query(const float* q, const typename MF<T>::frag& rf, float& nz, typename MF<T>::frag& zf) {
+  if constexpr (sizeof(T) == 2) {
+    const f32x4 q0 = *(const f32x4*)q, q1 = *(const f32x4*)(q + 4);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float p = (e < 4 ? q0[e] : q1[e - 4]) * fel(rf, e);
+      nz += p * p;
+      zf[e] = (bf16)p;
+    }
+  } else {
+    const float p = q[0] * rf;
+    nz += p * p;
+    zf = p;
+  }
+}
+
 template <typename T, int D, int DV, int M, int NA>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_decode(DecArgs A) {
   using F = MF<T>;
@@ -210,8 +231,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   // ---- stage the token, the ring (slot t mod w replaced by the new token) and Omega ----
   for (int i = tid; i < D; i += 256) { sq[i] = tof(qt[i]); sk[i] = tof(kt[i]); }
   for (int i = tid; i < DV; i += 256) sv[i] = tof(vt[i]);
-  stage_ring<T, W, D, false>(sRr, D + PAD, rr, rt, slot, w, tid);
-  stage_ring<T, W, DV, true>(sUt, W + PAD, ru, ut, slot, w, tid);
+  // slots from nvalid on hold no token yet: staged as zero rows
+  stage_ring<T, W, D, false>(sRr, D + PAD, rr, rt, slot, w, nvalid, tid);
+  stage_ring<T, W, DV, true>(sUt, W + PAD, ru, ut, slot, w, nvalid, tid);
   if constexpr (!PRE) stage_omega<T, D, M>(sOm, om, tid);
   const float Rold = A.rho[sh];
   __syncthreads();
@@ -251,26 +273,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     for (int ct = 0; ct < NA; ++ct) acc[pi][ct] = zero16();
 #pragma unroll
   for (int ct = 0; ct < NA; ++ct) nz[ct] = 0.0f;
+  // (anchors past nvalid read zero ring rows, so z = 0 there without a mask)
 #pragma unroll
   for (int ct = 0; ct < NA; ++ct) {
     const int c = ct * 32 + col;
     const bool valid = c < nvalid;
 #pragma unroll
     for (int ks = 0; ks < D / F::KS; ++ks) {
+      no_hoist();                                 // the step's q reads stay in the step
       const int k0 = ks * F::KS + h * F::KPL;
       typename F::frag rf = F::ld(sRr + c * (D + PAD), k0), zf;
-      if constexpr (sizeof(T) == 2) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          float p = valid ? sq[k0 + e] * fel(rf, e) : 0.0f;
-          nz[ct] += p * p;
-          zf[e] = (bf16)p;
-        }
-      } else {
-        float p = valid ? sq[k0] * rf : 0.0f;
-        nz[ct] += p * p;
-        zf = p;
-      }
+      composite_query<T>(sq + k0, rf, nz[ct], zf);
       if constexpr (PRE) {
         if (wv < PT) acc[0][ct] = F::mma(zf, omf[ks], acc[0][ct]);
       } else {
@@ -413,9 +426,12 @@ __global__ __launch_bounds__(256) void k_decode_chunk(DecArgs A, int NTOK) {
   float* Ms = A.M + (size_t)sh * M * DV;
   float* as = A.a + (size_t)sh * M;
 
-  // ring, Omega and the state, once per chunk
-  stage_ring<T, W, D, false>(sRr, D + PAD, rr, nullptr, 0, w, tid);
-  stage_ring<T, W, DV, true>(sUt, W + PAD, ru, nullptr, 0, w, tid);
+  // ring, Omega and the state, once per chunk; while t0 < w the slots t0 .. w-1
+  // hold no token yet: they are staged as zero rows and the chunk's tokens
+  // fill them in order
+  const int nv0 = (int)(t0 < w ? t0 : w);
+  stage_ring<T, W, D, false>(sRr, D + PAD, rr, nullptr, 0, w, nv0, tid);
+  stage_ring<T, W, DV, true>(sUt, W + PAD, ru, nullptr, 0, w, nv0, tid);
   stage_omega<T, D, M>(sOm, om, tid);
   float areg = (tid < M) ? as[tid] : 0.0f;
   float R = A.rho[sh];
@@ -478,20 +494,10 @@ __global__ __launch_bounds__(256) void k_decode_chunk(DecArgs A, int NTOK) {
       const bool valid = c < nvalid;
 #pragma unroll 2
       for (int ks = 0; ks < D / F::KS; ++ks) {
+        no_hoist();
         const int k0 = ks * F::KS + h * F::KPL;
         typename F::frag rf = F::ld(sRr + c * (D + PAD), k0), zf;
-        if constexpr (sizeof(T) == 2) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float p = valid ? sq[k0 + e] * fel(rf, e) : 0.0f;
-            nz[ct] += p * p;
-            zf[e] = (bf16)p;
-          }
-        } else {
-          const float p = valid ? sq[k0] * rf : 0.0f;
-          nz[ct] += p * p;
-          zf = p;
-        }
+        composite_query<T>(sq + k0, rf, nz[ct], zf);
 #pragma unroll
         for (int pi = 0; pi < PTW; ++pi) {
           const int pt = wv + 4 * pi;

@@ -706,12 +706,19 @@ __global__ __launch_bounds__(64 * NW) void k_readout(FwdArgs a) {
     for (int dt = 0; dt < DV / 32; ++dt) nacc[dt] = 0.0f;
     const float Ri = uniform(sRj[t]);
     const float sb = uniform(has_bnd ? fast_exp2(Rexb - Ri) : 0.0f);
+    // frame ratios 2^(R_j - R_i) of the registers' rows j = crow(v, h), zero for
+    // j > t: all sixteen read and formed, then selected (a load under the
+    // condition would be a branch per register, each waiting for its read)
     float sj[16];
     const float* sRjh = sRj + 4 * h;
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int j = crow(v, h);
-      sj[v] = (j <= t) ? fast_exp2(sRjh[8 * (v >> 2) + (v & 3)] - Ri) : 0.0f;
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 r4 = *(const f32x4*)(sRjh + 8 * g);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x = fast_exp2(r4[e] - Ri);
+        sj[4 * g + e] = (8 * g + 4 * h + e <= t) ? x : 0.0f;
+      }
     }
     const T* qrow = sQ + t * (D + PAD);
 #pragma unroll 1
