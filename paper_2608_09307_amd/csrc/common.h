@@ -181,6 +181,20 @@ template <typename T, int N> constexpr int tr_pad() {
 // row index of accumulator register v in a 32x32 tile
 LS_DEV int crow(int v, int h) { return 8 * (v >> 2) + 4 * h + (v & 3); }
 
+// x[v] = row[crow(v, h)] for the 16 registers of an accumulator, from a
+// 16-byte aligned 32-entry LDS row, as four 16-byte reads (read in full, so
+// that a caller's per-register condition selects after the read instead of
+// guarding it: a guarded read becomes a branch that waits for it)
+LS_DEV void crow_vals(const float* row, float (&x)[16]) {
+  const int h = lane_id() >> 5;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const f32x4 r4 = *(const f32x4*)(row + 8 * g + 4 * h);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[4 * g + e] = r4[e];
+  }
+}
+
 LS_DEV f32x16 zero16() {
   f32x16 z;
 #pragma unroll

@@ -73,7 +73,7 @@ __global__ __launch_bounds__(256) void k_chunk_state(FwdArgs a) {
   constexpr int PAD = F::PAD;
   constexpr int S = M * DV + M;
   __shared__ __align__(16) T sVt[4][DV][32 + PAD];
-  __shared__ float snk[4][32];
+  __shared__ __align__(16) float snk[4][32];
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
   const int b = blockIdx.x * 4 + wv;
   const int bh = blockIdx.y, hh = bh % a.H, n = a.n;
@@ -110,15 +110,15 @@ __global__ __launch_bounds__(256) void k_chunk_state(FwdArgs a) {
   __syncthreads();
   if (!active) return;
   float mx = kNegInf;
+  float nkt[16];
+  crow_vals(snk[wv], nkt);
 #pragma unroll
   for (int pt = 0; pt < M / 32; ++pt)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const int tk = crow(v, h);
-      const float nkt = snk[wv][tk];
-      float x = (tok0 + tk < n) ? acc[pt][v] - 0.5f * kLog2e * nkt : kNegInf;
-      acc[pt][v] = x;
-      mx = fmaxf(mx, x);
+      const float x = acc[pt][v] - 0.5f * kLog2e * nkt[v];
+      acc[pt][v] = (tok0 + crow(v, h) < n) ? x : kNegInf;
+      mx = fmaxf(mx, acc[pt][v]);
     }
   const float rb = wave_max(mx);
   const float rs = rsqrtf((float)M);
@@ -322,7 +322,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   __shared__ __align__(16) T sK[2][32][D + PAD];
   __shared__ __align__(16) T sOl[M][D + PAD];
   __shared__ __align__(16) T sVt[2][DV][32 + PAD];
-  __shared__ float snk[4][32];
+  __shared__ __align__(16) float snk[4][32];
   __shared__ float smx[4];
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = uniform(tid >> 6);
   const int bh = blockIdx.x, hh = bh % a.H, n = a.n, nch = a.nch;
@@ -396,12 +396,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       const float nk = half_swap_add(nkp);     // |k|^2 of token col
       if (h == 0) snk[wv][col] = nk;
       wave_lds_sync();
+      float nkt[16];
+      crow_vals(snk[wv], nkt);
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int tk = crow(v, h);
-        const float x = (b * 32 + tk < n) ? acc[v] - 0.5f * kLog2e * snk[wv][tk] : kNegInf;
-        acc[v] = x;
-        mx = fmaxf(mx, x);
+        const float x = acc[v] - 0.5f * kLog2e * nkt[v];
+        acc[v] = (b * 32 + crow(v, h) < n) ? x : kNegInf;
+        mx = fmaxf(mx, acc[v]);
       }
       mx = wave_max(mx);
     }
