@@ -175,7 +175,9 @@ int linsimp_prefill(const linsimp_dims* dims, const void* k, const void* v, cons
 /* One autoregressive decode step (Theorem 1) for S independent sequences:
  * token t = pos[s] of sequence s updates M and a (eq:Mstate, eq:astate),
  * writes (r_t, u_t) into ring slot t mod w, and reads q_t out over the
- * min(t+1, w) most recent anchors, the new token included.
+ * min(t+1, w) most recent anchors, the new token included.  Ring slots that
+ * hold no token yet (slots t+1 .. w-1 while t + 1 < w) do not affect the
+ * result, whatever they contain.
  *   q, k, r : [S, H, D] dtype;  v, u : [S, H, Dv] dtype;  omega [H, m, D] f32
  *   M, a, rho, ring_r, ring_u, pos : in/out, layouts as in linsimp_prefill
  *   out : [S, H, Dv] dtype

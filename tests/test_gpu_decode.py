@@ -64,6 +64,46 @@ def test_prefill_then_decode_matches_forward_rows(dtype, D, m, w, P, steps):
     assert max(rows) <= ROW_TOL[dtype]
 
 
+@pytest.mark.parametrize("D,m,w,P,steps,T", [(128, 128, 64, 10, 6, 8), (64, 128, 33, 0, 4, 5), (32, 32, 16, 3, 2, 4)])
+def test_unused_ring_slots_do_not_matter(D, m, w, P, steps, T):
+    """Ring slots that hold no token yet (P + tokens < w) filled with NaN: the
+    decode step and the chunked decode give bit for bit the outputs and state
+    of the zero-filled state that prefill writes."""
+    wl = Workload("ring", 2, 2, P + steps + T, D, D, m, w, "bf16", "fwd", seed=23)
+    print(f"[decode] {wl}", flush=True)
+    assert P + steps + T < w
+    x = make_inputs(wl, device=DEV, with_grad=False)
+    if P > 0:
+        st = L.prefill(x["k"][:, :, :P].contiguous(), x["v"][:, :, :P].contiguous(),
+                       x["r"][:, :, :P].contiguous(), x["u"][:, :, :P].contiguous(), x["omega"], w)
+    else:                                               # the empty state
+        dt = x["k"].dtype
+        st = {"M": torch.zeros(wl.B, wl.H, m, D, device=DEV), "a": torch.zeros(wl.B, wl.H, m, device=DEV),
+              "rho": torch.full((wl.B, wl.H), float("-inf"), device=DEV),
+              "ring_r": torch.zeros(wl.B, wl.H, w, D, dtype=dt, device=DEV),
+              "ring_u": torch.zeros(wl.B, wl.H, w, D, dtype=dt, device=DEV),
+              "pos": torch.zeros(wl.B, dtype=torch.int64, device=DEV)}
+    dirty = {nm: t.clone() for nm, t in st.items()}
+    dirty["ring_r"][:, :, P:] = float("nan")
+    dirty["ring_u"][:, :, P:] = float("nan")
+    outs = {"clean": [], "dirty": []}
+    for nm, s in (("clean", st), ("dirty", dirty)):
+        for t in range(P, P + steps):
+            tok = {k: x[k][:, :, t].contiguous() for k in ("q", "k", "v", "r", "u")}
+            outs[nm].append(L.decode_step(s, tok["q"], tok["k"], tok["v"], tok["r"], tok["u"], x["omega"], w).clone())
+        ch = {k: x[k][:, :, P + steps:P + steps + T].contiguous() for k in ("q", "k", "v", "r", "u")}
+        outs[nm].append(L.decode_chunk(s, ch["q"], ch["k"], ch["v"], ch["r"], ch["u"], x["omega"], w).clone())
+    torch.cuda.synchronize()
+    for a, b in zip(outs["clean"], outs["dirty"]):
+        assert torch.isfinite(a.float()).all()
+        assert torch.equal(a, b)
+    for nm in ("M", "a", "rho", "pos"):
+        assert torch.equal(st[nm], dirty[nm]), nm
+    n_tok = P + steps + T
+    assert torch.equal(st["ring_r"][:, :, :n_tok], dirty["ring_r"][:, :, :n_tok])
+    assert torch.equal(st["ring_u"][:, :, :n_tok], dirty["ring_u"][:, :, :n_tok])
+
+
 def test_state_update_and_resume():
     wl = Workload("dec2", 1, 2, 80, 128, 128, 128, 64, "bf16", "fwd", seed=22)
     x = make_inputs(wl, device=DEV, with_grad=False)
