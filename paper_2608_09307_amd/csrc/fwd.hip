@@ -292,10 +292,20 @@ __global__ __launch_bounds__(256) void k_keyfeat(FwdArgs a) {
   typedef T V __attribute__((ext_vector_type(VE)));
   T* dst = (T*)a.chi + (seq + s0) * M;
   const int nrow = min(32, n - s0);
+  // every piece read from LDS first, only the stores conditional (a read under
+  // the condition would be a branch that waits for it)
+  constexpr int IT = 32 * PPR / 64;
+  V xs[IT];
 #pragma unroll
-  for (int it = 0; it < 32 * PPR / 64; ++it) {
+  for (int it = 0; it < IT; ++it) {
     const int idx = l + 64 * it, r = idx / PPR, c = (idx % PPR) * VE;
-    if (r < nrow) *(V*)(dst + (size_t)r * M + c) = *(const V*)(&sX[wv][r][c]);
+    xs[it] = *(const V*)(&sX[wv][r][c]);
+  }
+  no_hoist();                                   // (and not sunk into the branches)
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int idx = l + 64 * it, r = idx / PPR, c = (idx % PPR) * VE;
+    if (r < nrow) *(V*)(dst + (size_t)r * M + c) = xs[it];
   }
 }
 
