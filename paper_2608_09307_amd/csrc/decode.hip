@@ -445,31 +445,47 @@ __global__ __launch_bounds__(256) void k_decode_chunk(DecArgs A, int NTOK) {
     }
   }
 
+  // a token's q, k, r (element tid of D) and v, u (element tid of DV) are
+  // loaded one token ahead into registers: their latency then overlaps the
+  // previous token's work instead of opening each token's chain.  Every
+  // thread loads (index clamped into the row), so no load sits under a branch.
+  static_assert(D <= 256 && DV <= 256, "one element of a token row per thread");
+  const int iD = min(tid, D - 1), iV = min(tid, DV - 1);
+  T xq, xk, xr, xv, xu;
+  auto fetch_token = [&](int j) {
+    const size_t tok = (size_t)sh * NTOK + j;
+    xq = ((const T*)A.q)[tok * D + iD];
+    xk = ((const T*)A.k)[tok * D + iD];
+    xr = ((const T*)A.r)[tok * D + iD];
+    xv = ((const T*)A.v)[tok * DV + iV];
+    xu = ((const T*)A.u)[tok * DV + iV];
+  };
+  fetch_token(0);
+
 #pragma unroll 1
   for (int j = 0; j < NTOK; ++j) {
     const int64_t t = t0 + j;
     const int slot = (int)(t % w);
     const int nvalid = (int)((t + 1 < w) ? t + 1 : w);
     const size_t tok = (size_t)sh * NTOK + j;
-    const T* qt = (const T*)A.q + tok * D;
-    const T* kt = (const T*)A.k + tok * D;
-    const T* vt = (const T*)A.v + tok * DV;
-    const T* rt = (const T*)A.r + tok * D;
-    const T* ut = (const T*)A.u + tok * DV;
     __syncthreads();                              // the previous token is done with LDS
-    for (int i = tid; i < D; i += 256) {
-      sq[i] = tof(qt[i]);
-      sk[i] = tof(kt[i]);
-      sRr[slot * (D + PAD) + i] = rt[i];
+    if (tid < D) {
+      sq[tid] = tof(xq);
+      sk[tid] = tof(xk);
+      sRr[slot * (D + PAD) + tid] = xr;
     }
-    for (int i = tid; i < DV; i += 256) {
-      sv[i] = tof(vt[i]);
-      sUt[i * (W + PAD) + F::sigma(slot)] = ut[i];
+    if (tid < DV) {
+      sv[tid] = tof(xv);
+      sUt[tid * (W + PAD) + F::sigma(slot)] = xu;
     }
     __syncthreads();
 
     // key features of k_t and the frame update
     const float rho_t = key_log2_features<T, D, M, false>(sk, om, schi, sred, nullptr);
+    // the next token's rows, issued after the bank loads of the key GEMV (the
+    // memory counter drains in issue order: issued before them, they would be
+    // waited for with them)
+    if (j + 1 < NTOK) fetch_token(j + 1);
     const float lam = tid < M ? schi[tid] : kNegInf;
     const float Rn = fmaxf(R, rho_t);
     const float sa = fast_exp2(R - Rn);
