@@ -184,7 +184,8 @@ LS_DEV void composite_query(const float* q, const typename MF<T>::frag& rf, floa
 }
 
 template <typename T, int D, int DV, int M, int NA>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_decode(DecArgs A) {
+// two waves per SIMD where the LDS allows two workgroups per CU (m <= 128)
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(M > 128 ? 1 : 2))) void k_decode(DecArgs A) {
   using F = MF<T>;
   constexpr int PT = M / 32;                  // feature tiles
   constexpr int PTW = (PT + 3) / 4;           // feature tiles per wave
@@ -634,7 +635,7 @@ __global__ __launch_bounds__(256) void k_decode_advance(int64_t* pos, int64_t S,
 template <typename T, int D, int DV, int M, int NA>
 static int run_decode(int64_t S, DecArgs a, int ntok, hipStream_t st) {
   // the caller bounds S*H by kMaxDecodeGroups (one workgroup each)
-  hipGetLastError();                                   // an earlier call's error is not this one's
+  (void)hipGetLastError();                             // an earlier call's error is not this one's
   if (ntok == 1) {
     ProfScope ps("decode", st);
     k_decode<T, D, DV, M, NA><<<(unsigned)(S * a.H), 256, 0, st>>>(a);
