@@ -46,45 +46,49 @@ struct DCfg {
   static constexpr int BYTES = oN + a16(4 * DV * 4);
 };
 
-// LDS staging in which every thread issues all of its 16-byte global loads
-// before its first LDS store (one memory round trip per call, not per element).
-// Ring rows c < nv come from `ring` ([w][COLS]), row `slot` from `fresh` when
-// it is given; rows nv .. ROWS-1 (nv <= w: past the window, or slots that hold
-// no token yet) are zero, so that a product with them needs no mask.  TRANS
-// stores column-major with the row index permuted by MF<T>::sigma (the
-// readout's anchor operand layout).
+// LDS staging of a ring in two phases, so that a caller issues every global
+// load of its staging before the first LDS store (one memory round trip per
+// call, not one per staged array).  Ring rows c < nv come from `ring`
+// ([w][COLS]), row `slot` from `fresh` when it is given; rows nv .. ROWS-1
+// (nv <= w: past the window, or slots that hold no token yet) are zero, so
+// that a product with them needs no mask.  TRANS stores column-major with
+// the row index permuted by MF<T>::sigma (the readout's anchor operand layout).
 template <typename T, int ROWS, int COLS, bool TRANS>
-LS_DEV void stage_ring(T* dst, int ldst, const T* ring, const T* fresh, int slot, int w, int nv, int tid) {
-  constexpr int VE = 16 / sizeof(T);
-  constexpr int CPR = COLS / VE;
-  constexpr int N = ROWS * CPR;
-  constexpr int IT = (N + 255) / 256;
+struct RingStage {
+  static constexpr int VE = 16 / sizeof(T);
+  static constexpr int CPR = COLS / VE;
+  static constexpr int N = ROWS * CPR;
+  static constexpr int IT = (N + 255) / 256;
   typedef T V __attribute__((ext_vector_type(VE)));
   V x[IT];
+  // unconditional loads (row clamped into the ring)
+  LS_DEV void load(const T* ring, const T* fresh, int slot, int w, int tid) {
 #pragma unroll
-  for (int it = 0; it < IT; ++it) {
-    // unconditional loads (row clamped into the ring); rows from nv on are zeroed below
-    const int idx = min(tid + 256 * it, N - 1), c = idx / CPR, e = (idx % CPR) * VE;
-    const int cr = c < w ? c : w - 1;
-    x[it] = *(const V*)((fresh != nullptr && cr == slot) ? fresh + e : ring + (size_t)cr * COLS + e);
-  }
-#pragma unroll
-  for (int it = 0; it < IT; ++it) {
-    const int idx = tid + 256 * it, c = idx / CPR, e = (idx % CPR) * VE;
-    if (idx >= N) continue;
-    if (c >= nv) {
-#pragma unroll
-      for (int k = 0; k < VE; ++k) x[it][k] = (T)0.0f;
-    }
-    if constexpr (TRANS) {
-#pragma unroll
-      for (int k = 0; k < VE; ++k) dst[(e + k) * ldst + MF<T>::sigma(c)] = x[it][k];
-    } else {
-#pragma unroll
-      for (int k = 0; k < VE; ++k) dst[c * ldst + e + k] = x[it][k];
+    for (int it = 0; it < IT; ++it) {
+      const int idx = min(tid + 256 * it, N - 1), c = idx / CPR, e = (idx % CPR) * VE;
+      const int cr = c < w ? c : w - 1;
+      x[it] = *(const V*)((fresh != nullptr && cr == slot) ? fresh + e : ring + (size_t)cr * COLS + e);
     }
   }
-}
+  LS_DEV void store(T* dst, int ldst, int nv, int tid) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int idx = tid + 256 * it, c = idx / CPR, e = (idx % CPR) * VE;
+      if (N % 256 != 0 && idx >= N) continue;
+      if (c >= nv) {
+#pragma unroll
+        for (int k = 0; k < VE; ++k) x[it][k] = (T)0.0f;
+      }
+      if constexpr (TRANS) {
+#pragma unroll
+        for (int k = 0; k < VE; ++k) dst[(e + k) * ldst + MF<T>::sigma(c)] = x[it][k];
+      } else {
+#pragma unroll
+        for (int k = 0; k < VE; ++k) dst[c * ldst + e + k] = x[it][k];
+      }
+    }
+  }
+};
 
 // Omega * log2(e) of one head into LDS rows of pitch D + PAD, operand type
 template <typename T, int D, int M>
@@ -229,14 +233,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(M > 128 ? 1
   float mreg[PRE ? DV / 32 : 1][16];
   const float a_old = tid < M ? as[tid] : 0.0f;
 
-  // ---- stage the token, the ring (slot t mod w replaced by the new token) and Omega ----
-  for (int i = tid; i < D; i += 256) { sq[i] = tof(qt[i]); sk[i] = tof(kt[i]); }
-  for (int i = tid; i < DV; i += 256) sv[i] = tof(vt[i]);
-  // slots from nvalid on hold no token yet: staged as zero rows
-  stage_ring<T, W, D, false>(sRr, D + PAD, rr, rt, slot, w, nvalid, tid);
-  stage_ring<T, W, DV, true>(sUt, W + PAD, ru, ut, slot, w, nvalid, tid);
-  if constexpr (!PRE) stage_omega<T, D, M>(sOm, om, tid);
+  // ---- stage the token, the ring (slot t mod w replaced by the new token) and
+  // Omega: the token's elements and both rings are loaded before any of them is
+  // stored (one memory round trip); slots from nvalid on hold no token yet and
+  // are staged as zero rows ----
+  static_assert(D <= 256 && DV <= 256, "one element of a token row per thread");
+  RingStage<T, W, D, false> rgr;
+  RingStage<T, W, DV, true> rgu;
+  rgr.load(rr, rt, slot, w, tid);
+  rgu.load(ru, ut, slot, w, tid);
+  const T xq = qt[min(tid, D - 1)], xk = kt[min(tid, D - 1)], xv = vt[min(tid, DV - 1)];
   const float Rold = A.rho[sh];
+  if (tid < D) {
+    sq[tid] = tof(xq);
+    sk[tid] = tof(xk);
+  }
+  if (tid < DV) sv[tid] = tof(xv);
+  rgr.store(sRr, D + PAD, nvalid, tid);
+  rgu.store(sUt, W + PAD, nvalid, tid);
+  if constexpr (!PRE) stage_omega<T, D, M>(sOm, om, tid);
   __syncthreads();
 
   // ---- key features of k_t (float32 GEMV) and the frame update; with one
@@ -431,8 +446,14 @@ __global__ __launch_bounds__(256) void k_decode_chunk(DecArgs A, int NTOK) {
   // hold no token yet: they are staged as zero rows and the chunk's tokens
   // fill them in order
   const int nv0 = (int)(t0 < w ? t0 : w);
-  stage_ring<T, W, D, false>(sRr, D + PAD, rr, nullptr, 0, w, nv0, tid);
-  stage_ring<T, W, DV, true>(sUt, W + PAD, ru, nullptr, 0, w, nv0, tid);
+  {
+    RingStage<T, W, D, false> rgr;
+    RingStage<T, W, DV, true> rgu;
+    rgr.load(rr, nullptr, 0, w, tid);
+    rgu.load(ru, nullptr, 0, w, tid);
+    rgr.store(sRr, D + PAD, nv0, tid);
+    rgu.store(sUt, W + PAD, nv0, tid);
+  }
   stage_omega<T, D, M>(sOm, om, tid);
   float areg = (tid < M) ? as[tid] : 0.0f;
   float R = A.rho[sh];
