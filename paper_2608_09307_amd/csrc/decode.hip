@@ -105,67 +105,133 @@ LS_DEV void stage_omega(T* dst, const float* om, int tid) {
   }
 }
 
+// Omega rows of one token's key GEMV held by this thread (M <= 128): feature
+// p = 32 wv + col, the KPL-wide pieces at k0 = ks KS + h KPL.  Loaded apart
+// from the GEMV so that a caller can issue the loads early.
+template <typename T, int D>
+struct KeyBankRows {
+  float o[D / MF<T>::KS][MF<T>::KPL];
+  LS_DEV void load(const float* om, int M, int tid) {
+    using F = MF<T>;
+    const int l = tid & 63, col = l & 31, h = l >> 5, wv = tid >> 6;
+    const int p = wv * 32 + col;
+    const float* orow = om + (size_t)(p < M ? p : 0) * D;
+#pragma unroll
+    for (int ks = 0; ks < D / F::KS; ++ks) {
+      const int k0 = ks * F::KS + h * F::KPL;
+      if constexpr (F::KPL % 4 == 0) {
+#pragma unroll
+        for (int e4 = 0; e4 < F::KPL; e4 += 4) {
+          const f32x4 x = *(const f32x4*)(orow + k0 + e4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) o[ks][e4 + e] = x[e];
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < F::KPL; ++e) o[ks][e] = orow[k0 + e];
+      }
+    }
+  }
+};
+
 // Log2 key features of one token, lambda_p = (omega_p . k - |k|^2 / 2) log2(e),
-// in float32 into lam[p] (LDS, p < M).  Feature p's dot product is split over
-// lanes l and l ^ 32, which take the alternate KPL-wide pieces of D that make
-// up an MFMA operand fragment of row p; with FRAGS (M <= 128) the fragments
-// of Omega * log2(e) in the operand type are kept in omf[D / KS] for the
-// query logits, so the bank is read once.  Returns max_p lambda_p; every
-// thread calls it (it ends with a barrier).
+// in float32 into lam[p] (LDS, p < M), from Omega rows already loaded
+// (M <= 128).  Feature p's dot product is split over lanes l and l ^ 32, which
+// take the alternate KPL-wide pieces of D that make up an MFMA operand
+// fragment of row p; with FRAGS the fragments of Omega * log2(e) in the
+// operand type are kept in omf[D / KS] for the query logits, so the bank is
+// read once.  Returns max_p lambda_p; every thread calls it (it ends with a
+// barrier).
 template <typename T, int D, int M, bool FRAGS>
-LS_DEV float key_log2_features(const float* sk, const float* om, float* lam, float* sred,
-                               typename MF<T>::frag* omf) {
+LS_DEV float key_log2_features_rows(const KeyBankRows<T, D>& kb, const float* sk, float* lam, float* sred,
+                                    typename MF<T>::frag* omf) {
   using F = MF<T>;
-  static_assert(!FRAGS || M <= 128, "fragments for one feature tile per wave");
+  static_assert(M <= 128, "one feature row per thread");
   const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = tid >> 6;
   float nk = 0.0f;
 #pragma unroll
   for (int e = l; e < D; e += 64) nk += sk[e] * sk[e];
   nk = wave_sum(nk);
   float mx = kNegInf;
+  const int p = wv * 32 + col;
+  float acc = 0.0f;
 #pragma unroll
-  for (int p0 = 0; p0 < M; p0 += 128) {
-    const int p = p0 + wv * 32 + col;
-    const bool act = p < M;
-    const float* orow = om + (size_t)(act ? p : 0) * D;
-    float acc = 0.0f;
+  for (int ks = 0; ks < D / F::KS; ++ks) {
+    const int k0 = ks * F::KS + h * F::KPL;
 #pragma unroll
-    for (int ks = 0; ks < D / F::KS; ++ks) {
-      const int k0 = ks * F::KS + h * F::KPL;
-      float o[F::KPL];
-      if constexpr (F::KPL % 4 == 0) {
+    for (int e = 0; e < F::KPL; ++e) acc += kb.o[ks][e] * sk[k0 + e];
+    if constexpr (FRAGS) {
+      if constexpr (sizeof(T) == 2) {
 #pragma unroll
-        for (int e4 = 0; e4 < F::KPL; e4 += 4) {
-          const f32x4 x = *(const f32x4*)(orow + k0 + e4);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) o[e4 + e] = x[e];
-        }
+        for (int e = 0; e < F::KPL; ++e) omf[ks][e] = (T)(kb.o[ks][e] * kLog2e);
       } else {
-#pragma unroll
-        for (int e = 0; e < F::KPL; ++e) o[e] = orow[k0 + e];
-      }
-#pragma unroll
-      for (int e = 0; e < F::KPL; ++e) acc += o[e] * sk[k0 + e];
-      if constexpr (FRAGS) {
-        if constexpr (sizeof(T) == 2) {
-#pragma unroll
-          for (int e = 0; e < F::KPL; ++e) omf[ks][e] = (T)(o[e] * kLog2e);
-        } else {
-          omf[ks] = o[0] * kLog2e;
-        }
+        omf[ks] = kb.o[ks][0] * kLog2e;
       }
     }
-    acc = half_swap_add(acc);
-    const float x = (acc - 0.5f * nk) * kLog2e;
-    if (act) {
-      mx = fmaxf(mx, x);
-      if (h == 0) lam[p] = x;
-    }
+  }
+  acc = half_swap_add(acc);
+  const float x = (acc - 0.5f * nk) * kLog2e;
+  if (p < M) {
+    mx = x;
+    if (h == 0) lam[p] = x;
   }
   mx = wave_max(mx);
   if (l == 0) sred[wv] = mx;
   __syncthreads();
   return fmaxf(fmaxf(sred[0], sred[1]), fmaxf(sred[2], sred[3]));
+}
+
+// The same, loading the bank itself; any M (feature blocks of 128)
+template <typename T, int D, int M, bool FRAGS>
+LS_DEV float key_log2_features(const float* sk, const float* om, float* lam, float* sred,
+                               typename MF<T>::frag* omf) {
+  using F = MF<T>;
+  static_assert(!FRAGS || M <= 128, "fragments for one feature tile per wave");
+  if constexpr (M <= 128) {
+    KeyBankRows<T, D> kb;
+    kb.load(om, M, threadIdx.x);
+    return key_log2_features_rows<T, D, M, FRAGS>(kb, sk, lam, sred, omf);
+  } else {
+    static_assert(M % 128 == 0, "whole feature blocks");
+    const int tid = threadIdx.x, l = tid & 63, col = l & 31, h = l >> 5, wv = tid >> 6;
+    float nk = 0.0f;
+#pragma unroll
+    for (int e = l; e < D; e += 64) nk += sk[e] * sk[e];
+    nk = wave_sum(nk);
+    float mx = kNegInf;
+#pragma unroll
+    for (int p0 = 0; p0 < M; p0 += 128) {
+      const int p = p0 + wv * 32 + col;
+      const float* orow = om + (size_t)p * D;
+      float acc = 0.0f;
+#pragma unroll
+      for (int ks = 0; ks < D / F::KS; ++ks) {
+        const int k0 = ks * F::KS + h * F::KPL;
+        float o[F::KPL];
+        if constexpr (F::KPL % 4 == 0) {
+#pragma unroll
+          for (int e4 = 0; e4 < F::KPL; e4 += 4) {
+            const f32x4 x = *(const f32x4*)(orow + k0 + e4);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e4 + e] = x[e];
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < F::KPL; ++e) o[e] = orow[k0 + e];
+        }
+#pragma unroll
+        for (int e = 0; e < F::KPL; ++e) acc += o[e] * sk[k0 + e];
+      }
+      acc = half_swap_add(acc);
+      const float x = (acc - 0.5f * nk) * kLog2e;
+      mx = fmaxf(mx, x);
+      if (h == 0) lam[p] = x;
+    }
+    mx = wave_max(mx);
+    if (l == 0) sred[wv] = mx;
+    __syncthreads();
+    return fmaxf(fmaxf(sred[0], sred[1]), fmaxf(sred[2], sred[3]));
+  }
 }
 
 // z = q (*) r of one anchor at one k-step as an operand fragment (q float32
@@ -233,16 +299,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(M > 128 ? 1
   float mreg[PRE ? DV / 32 : 1][16];
   const float a_old = tid < M ? as[tid] : 0.0f;
 
-  // ---- stage the token, the ring (slot t mod w replaced by the new token) and
-  // Omega: the token's elements and both rings are loaded before any of them is
-  // stored (one memory round trip); slots from nvalid on hold no token yet and
-  // are staged as zero rows ----
+  // ---- the Omega rows of the key GEMV (m <= 128), then the token and both
+  // rings (slot t mod w replaced by the new token): every load is issued before
+  // the first LDS store, the bank's L2 latency under the staging's HBM loads
+  // (one memory round trip); slots from nvalid on hold no token yet and are
+  // staged as zero rows ----
   static_assert(D <= 256 && DV <= 256, "one element of a token row per thread");
+  KeyBankRows<T, D> kb;
+  if constexpr (PRE) kb.load(om, M, tid);
   RingStage<T, W, D, false> rgr;
   RingStage<T, W, DV, true> rgu;
   rgr.load(rr, rt, slot, w, tid);
   rgu.load(ru, ut, slot, w, tid);
+  // (r_t and u_t are kept for the ring slot written at the end)
   const T xq = qt[min(tid, D - 1)], xk = kt[min(tid, D - 1)], xv = vt[min(tid, DV - 1)];
+  const T xr = rt[min(tid, D - 1)], xu = ut[min(tid, DV - 1)];
   const float Rold = A.rho[sh];
   if (tid < D) {
     sq[tid] = tof(xq);
@@ -252,16 +323,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(M > 128 ? 1
   rgr.store(sRr, D + PAD, nvalid, tid);
   rgu.store(sUt, W + PAD, nvalid, tid);
   if constexpr (!PRE) stage_omega<T, D, M>(sOm, om, tid);
-  __syncthreads();
-
-  // ---- key features of k_t (float32 GEMV) and the frame update; with one
-  // feature tile per wave the GEMV's loads of the wave's Omega rows also
-  // give the logits' operand fragments (no LDS copy of the bank) ----
-  typename F::frag omf[PRE ? D / F::KS : 1];
-  const float rho_t = key_log2_features<T, D, M, PRE>(sk, om, schi, sred, omf);
-  // the state rows this thread updates are fetched after the key GEMV's loads:
-  // their latency overlaps the logits and exponentials (the memory counter
-  // drains in issue order, so loads issued before them would wait for them)
+  // the state rows this thread updates, issued once the staging has been
+  // waited for: the memory counter drains in issue order, so no wait before
+  // the update includes them, and they arrive under the GEMV, the logits and
+  // the exponentials
   if constexpr (PRE) {
     if (wv < PT) {
 #pragma unroll
@@ -270,6 +335,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(M > 128 ? 1
         for (int vv = 0; vv < 16; ++vv) mreg[dt][vv] = Ms[(size_t)(wv * 32 + crow(vv, h)) * DV + dt * 32 + col];
     }
   }
+  __syncthreads();
+
+  // ---- key features of k_t (float32 GEMV) and the frame update; with one
+  // feature tile per wave the Omega rows of the GEMV also give the logits'
+  // operand fragments (no LDS copy of the bank) ----
+  typename F::frag omf[PRE ? D / F::KS : 1];
+  float rho_t;
+  if constexpr (PRE) rho_t = key_log2_features_rows<T, D, M, PRE>(kb, sk, schi, sred, omf);
+  else rho_t = key_log2_features<T, D, M, PRE>(sk, om, schi, sred, omf);
   const float lam = tid < M ? schi[tid] : kNegInf;   // each thread rewrites only its own entry below
   const float Rn = fmaxf(Rold, rho_t);
   const float sa = fast_exp2(Rold - Rn);          // 0 for an empty state (R = -inf)
@@ -395,8 +469,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(M > 128 ? 1
     ((T*)A.out)[(size_t)sh * DV + d] = (T)(N * inv);
   }
   // ring slot and frame
-  for (int e = tid; e < D; e += 256) rr[(size_t)slot * D + e] = rt[e];
-  for (int e = tid; e < DV; e += 256) ru[(size_t)slot * DV + e] = ut[e];
+  if (tid < D) rr[(size_t)slot * D + tid] = xr;
+  if (tid < DV) ru[(size_t)slot * DV + tid] = xu;
   if (tid == 0) A.rho[sh] = Rn;
 }
 
@@ -638,12 +712,14 @@ __global__ __launch_bounds__(256) void k_decode_chunk(DecArgs A, int NTOK) {
   }
   if (tid < M) as[tid] = areg;
   if (tid == 0) A.rho[sh] = R;
-  const int jlo = NTOK > w ? NTOK - w : 0;        // the last min(NTOK, w) tokens stay in the ring
+  // the last min(NTOK, w) tokens stay in the ring: their rows are read from the
+  // LDS ring (written by their tokens and made visible by the tokens' barriers),
+  // not again from global memory (a global load per row, each waited for)
+  const int jlo = NTOK > w ? NTOK - w : 0;
   for (int j = jlo; j < NTOK; ++j) {
     const int slot = (int)((t0 + j) % w);
-    const size_t tok = (size_t)sh * NTOK + j;
-    for (int e = tid; e < D; e += 256) rr[(size_t)slot * D + e] = ((const T*)A.r)[tok * D + e];
-    for (int e = tid; e < DV; e += 256) ru[(size_t)slot * DV + e] = ((const T*)A.u)[tok * DV + e];
+    for (int e = tid; e < D; e += 256) rr[(size_t)slot * D + e] = sRr[slot * (D + PAD) + e];
+    for (int e = tid; e < DV; e += 256) ru[(size_t)slot * DV + e] = sUt[e * (W + PAD) + F::sigma(slot)];
   }
 }
 
