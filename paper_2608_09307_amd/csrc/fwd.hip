@@ -319,7 +319,8 @@ __global__ __launch_bounds__(256) void k_keyfeat(FwdArgs a) {
 // the lo half of all tiles in LDS, so that two workgroups fit on a CU with
 // two waves per SIMD), the chunk maximum shared across the waves,
 // the frame update (M, a scaled by 2^(R - R')), then M += chi^T V on the
-// matrix cores.  The chunk's k rows and V^T are staged in LDS one chunk ahead.
+// matrix cores.  The chunk's k rows and V^T are staged in LDS one chunk ahead,
+// from registers loaded two chunks ahead.
 // Nothing but the final state is written (the chunked forward materialises
 // every chunk's contribution instead).  bf16 inputs, m <= 128.
 // ---------------------------------------------------------------------------
@@ -371,18 +372,18 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       for (int e = 0; e < 4; ++e) sVt[buf][d0 + e][F::sigma(jj)] = x[e];
     });
   };
+  // chunk b + 1's rows are loaded while chunk b is folded in, and chunk b + 2's
+  // as soon as chunk b + 1 is in LDS: every load has about one chunk's work to land
   sk.load(ks, D, 0, 0, n, tid);
   sv.load(vs, DV, 0, 0, n, tid);
   stage_store(0, 0);
+  sk.load(ks, D, 32, 0, n, tid);
+  sv.load(vs, DV, 32, 0, n, tid);
 
 #pragma unroll 1
   for (int b = 0; b < nch; ++b) {
     const int cur = b & 1;
     __syncthreads();                           // chunk b staged; the other buffer is free
-    if (b + 1 < nch) {
-      sk.load(ks, D, (b + 1) * 32, 0, n, tid);
-      sv.load(vs, DV, (b + 1) * 32, 0, n, tid);
-    }
     // key log2-features of the tile: regs <-> token crow(v, h), lanes <-> p
     f32x16 acc = zero16();
     float mx = kNegInf;
@@ -417,7 +418,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
       mx = wave_max(mx);
     }
     if (l == 0) smx[wv] = mx;
-    if (b + 1 < nch) stage_store(b + 1, cur ^ 1);
+    if (b + 1 < nch) {
+      stage_store(b + 1, cur ^ 1);
+      sk.load(ks, D, (b + 2) * 32, 0, n, tid);
+      sv.load(vs, DV, (b + 2) * 32, 0, n, tid);
+    }
     __syncthreads();
     const float cm = fmaxf(fmaxf(smx[0], smx[1]), fmaxf(smx[2], smx[3]));
     const float Rn = fmaxf(R, cm);
