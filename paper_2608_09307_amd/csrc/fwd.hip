@@ -1002,23 +1002,42 @@ static int run_fwd(const Shape& s, FwdArgs a, hipStream_t st) {
   return 0;
 }
 
-// Prefill ring: slot j mod w holds token j of the last min(n, w) tokens.
+// Prefill ring: slot j mod w holds token j of the last min(n, w) tokens; the
+// slots no token reaches (n < w) are zero.  16-byte pieces of the rows, every
+// piece of a batch loaded (row index clamped) before the first is stored.
 template <typename T>
 __global__ __launch_bounds__(256) void k_ring_fill(const T* __restrict__ r, const T* __restrict__ u,
                                                    T* __restrict__ rr, T* __restrict__ ru,
                                                    int64_t* __restrict__ pos, int H, int n, int w,
                                                    int D, int DV) {
+  constexpr int VE = 16 / (int)sizeof(T), NB = 8;
+  typedef T V __attribute__((ext_vector_type(VE)));
   const int bh = blockIdx.x;
-  const int width = D + DV;
-  for (int idx = threadIdx.x; idx < w * width; idx += 256) {
-    int slot = idx / width, e = idx % width;
-    // newest token j < n with j mod w == slot
-    int j = (n - 1) - (((n - 1 - slot) % w + w) % w);
-    bool ok = j >= 0 && j >= n - w;
-    if (e < D)
-      rr[((size_t)bh * w + slot) * D + e] = ok ? r[((size_t)bh * n + j) * D + e] : (T)0.0f;
-    else
-      ru[((size_t)bh * w + slot) * DV + (e - D)] = ok ? u[((size_t)bh * n + j) * DV + (e - D)] : (T)0.0f;
+  const int pr = D / VE, pw = pr + DV / VE, total = w * pw;
+  // the newest token j <= n - 1 with j mod w == slot (negative: none)
+  auto token = [&](int slot) { return (n - 1) - (((n - 1 - slot) % w + w) % w); };
+  for (int base = 0; base < total; base += 256 * NB) {
+    V x[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int idx = min(base + (int)threadIdx.x + 256 * i, total - 1);
+      const int slot = idx / pw, c = idx % pw;
+      const size_t j = (size_t)max(token(slot), 0);
+      const T* src = c < pr ? r + ((size_t)bh * n + j) * D + c * VE : u + ((size_t)bh * n + j) * DV + (c - pr) * VE;
+      x[i] = *(const V*)src;
+    }
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      const int idx = base + (int)threadIdx.x + 256 * i;
+      if (idx >= total) continue;
+      const int slot = idx / pw, c = idx % pw;
+      const bool ok = token(slot) >= 0;
+      V y;
+#pragma unroll
+      for (int e = 0; e < VE; ++e) y[e] = ok ? x[i][e] : (T)0.0f;
+      T* dst = c < pr ? rr + ((size_t)bh * w + slot) * D + c * VE : ru + ((size_t)bh * w + slot) * DV + (c - pr) * VE;
+      *(V*)dst = y;
+    }
   }
   if (threadIdx.x == 0 && bh % H == 0) pos[bh / H] = n;
 }
@@ -1026,6 +1045,11 @@ __global__ __launch_bounds__(256) void k_ring_fill(const T* __restrict__ r, cons
 int launch_ring_fill(const Shape& s, const void* r, const void* u, void* ring_r, void* ring_u,
                      int64_t* pos, hipStream_t st) {
   const int BH = (int)s.BH();
+  const int es = s.dtype == 1 ? 2 : 4;
+  if ((s.D * es) % 16 != 0 || (s.Dv * es) % 16 != 0) {
+    set_error("ring fill: rows of %d and %d elements are not whole 16-byte pieces", s.D, s.Dv);
+    return -2;
+  }
   if (s.dtype == 1)
     k_ring_fill<bf16><<<BH, 256, 0, st>>>((const bf16*)r, (const bf16*)u, (bf16*)ring_r, (bf16*)ring_u,
                                           pos, (int)s.H, (int)s.n, s.w, s.D, s.Dv);
