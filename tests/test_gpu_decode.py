@@ -6,7 +6,9 @@ one-token update against the definition eq:Mstate / eq:astate; resuming from a
 copied state; and the 256-sequence x 16-head decode step with an 8192-token
 prefix on sampled (sequence, head) pairs, with the state update
 Delta M = phi(k_t) v_t^T of every (sequence, head) checked at that shape.
-Outputs are held to relative L2 per tensor and per row (5e-2 bf16, 1e-4 f32).
+Outputs are held to relative L2 per tensor and per row (5e-2 bf16, 1e-4 f32);
+the anchor rings, which are copies, bit for bit after the prefill and after
+the steps.
 """
 
 import numpy as np
@@ -41,6 +43,7 @@ def test_prefill_then_decode_matches_forward_rows(dtype, D, m, w, P, steps):
     x = make_inputs(wl, device=DEV, with_grad=False)
     st = L.prefill(x["k"][:, :, :P].contiguous(), x["v"][:, :, :P].contiguous(),
                    x["r"][:, :, :P].contiguous(), x["u"][:, :, :P].contiguous(), x["omega"], w)
+    rings0 = (st["ring_r"].clone(), st["ring_u"].clone())
     outs = []
     for t in range(P, P + steps):
         tok = {nm: x[nm][:, :, t].contiguous() for nm in ("q", "k", "v", "r", "u")}
@@ -55,10 +58,17 @@ def test_prefill_then_decode_matches_forward_rows(dtype, D, m, w, P, steps):
                                       f64(x["r"][b, h]), f64(x["u"][b, h]), f64(x["omega"][h]), w)
             errs.append(rel_l2(f64(got[b, h]), ref[P:]))
             rows.append(row_max_rel(f64(got[b, h]), ref[P:]))
-            Mref, aref = O.prefill_state(f64(x["k"][b, h]), f64(x["v"][b, h]), f64(x["r"][b, h]),
-                                         f64(x["u"][b, h]), f64(x["omega"][h]), w)["M"], None
+            full = O.prefill_state(f64(x["k"][b, h]), f64(x["v"][b, h]), f64(x["r"][b, h]),
+                                   f64(x["u"][b, h]), f64(x["omega"][h]), w)
             M_true, a_true = _state_true(st, b, h)
-            assert rel_l2(M_true, Mref) < TOL[dtype]
+            assert rel_l2(M_true, full["M"]) < TOL[dtype]
+            # the anchor rings are copies: bit-exact after the prefill and after the steps
+            pre = O.prefill_state(*(f64(x[nm][b, h, :P]) for nm in ("k", "v", "r", "u")),
+                                  f64(x["omega"][h]), w)
+            assert np.array_equal(f64(rings0[0][b, h]), pre["ring_r"])
+            assert np.array_equal(f64(rings0[1][b, h]), pre["ring_u"])
+            assert np.array_equal(f64(st["ring_r"][b, h]), full["ring_r"])
+            assert np.array_equal(f64(st["ring_u"][b, h]), full["ring_u"])
     print("      max rel_l2 over heads", max(errs), "row max", max(rows), flush=True)
     assert max(errs) < TOL[dtype]
     assert max(rows) <= ROW_TOL[dtype]
