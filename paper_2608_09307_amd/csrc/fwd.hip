@@ -45,19 +45,24 @@ struct FwdArgs {
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void k_prep_omega(const float* __restrict__ omega, T* __restrict__ omq,
-                                                    T* __restrict__ omk, f16* __restrict__ omh, int H, int MD) {
+                                                    T* __restrict__ omk, f16* __restrict__ omh, int H, int MD,
+                                                    int D) {
+  using F = MF<T>;
   int idx = blockIdx.x * 256 + threadIdx.x;
   if (idx >= H * MD) return;
   float x = omega[idx] * kLog2e;
   omq[idx] = (T)x;
+  // the key-side copy in fragment order (the order of bank_frag)
+  const int hh = idx / MD, e = idx % MD, p = e / D, k = e % D;
+  const size_t f = ((size_t)((p >> 5) * (D / F::KS) + k / F::KS) * 64 + ((k % F::KS) / F::KPL) * 32 + (p & 31))
+                   * F::KPL + k % F::KPL;
   if constexpr (sizeof(T) == 2) {
     omh[idx] = (f16)x;
-    int hh = idx / MD, e = idx % MD;
     bf16 hi = (bf16)x;
-    omk[(size_t)hh * 2 * MD + e] = hi;
-    omk[(size_t)hh * 2 * MD + MD + e] = (bf16)(x - (float)hi);
+    omk[(size_t)hh * 2 * MD + f] = hi;
+    omk[(size_t)hh * 2 * MD + MD + f] = (bf16)(x - (float)hi);
   } else {
-    omk[idx] = (T)x;
+    omk[(size_t)hh * MD + f] = (T)x;
   }
 }
 
@@ -345,15 +350,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   // hi half of this wave's Omega tile: B operands, lanes <-> feature p
   typename F::frag oh[D / F::KS];
 #pragma unroll
-  for (int s = 0; s < D / F::KS; ++s) {
-    const int k0 = s * F::KS + h * F::KPL;
-    const int pr = (owner ? wv : 0) * 32 + col;
-    oh[s] = F::ld(omk_h + (size_t)pr * D, k0);
-  }
+  for (int s = 0; s < D / F::KS; ++s) oh[s] = *(const typename F::frag*)(omk_h + bank_frag<T, D>(owner ? wv : 0, s, l));
   {
-    StageRows<T, M, D, 256> so;
-    so.load(omk_h + (size_t)M * D, D, 0, 0, M, tid);
-    so.store(&sOl[0][0], D + PAD, 0, 0, M, tid);
+    // the lo half into LDS rows: fragment f of the bank goes to row 32 pt + col,
+    // columns s KS + h KPL onwards (every load issued before the first store)
+    constexpr int NS = D / F::KS, NF = (M / 32) * NS * 64, IT = (NF + 255) / 256;
+    static_assert(NF * F::KPL == M * D, "one fragment per lane, k-step and tile");
+    typename F::frag xs[IT];
+#pragma unroll
+    for (int it = 0; it < IT; ++it)
+      xs[it] = *(const typename F::frag*)(omk_h + (size_t)M * D + (size_t)min(tid + 256 * it, NF - 1) * F::KPL);
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int f = tid + 256 * it;
+      if (NF % 256 != 0 && f >= NF) continue;
+      const int ln = f & 63, s = (f >> 6) % NS, pt = (f >> 6) / NS;
+      *(typename F::frag*)&sOl[pt * 32 + (ln & 31)][s * F::KS + (ln >> 5) * F::KPL] = xs[it];
+    }
   }
   const T* olrow = &sOl[(owner ? wv : 0) * 32 + col][0];
   f32x16 Macc[DV / 32];
@@ -955,7 +968,7 @@ static int run_fwd(const Shape& s, FwdArgs a, hipStream_t st) {
   {
     int tot = (int)s.H * M * D;
     ProfScope ps("prep_omega", st);
-    k_prep_omega<T><<<(tot + 255) / 256, 256, 0, st>>>(a.omega, (T*)a.omq, (T*)a.omk, (f16*)a.omh, (int)s.H, M * D);
+    k_prep_omega<T><<<(tot + 255) / 256, 256, 0, st>>>(a.omega, (T*)a.omq, (T*)a.omk, (f16*)a.omh, (int)s.H, M * D, D);
   }
   if constexpr (sizeof(T) == 2 && M <= 128) {
     if (a.out == nullptr && a.final_M != nullptr) {   // prefill: the final state only

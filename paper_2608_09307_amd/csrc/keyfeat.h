@@ -5,6 +5,19 @@
 namespace linsimp {
 
 // ---------------------------------------------------------------------------
+// The key-side bank copy (Omega log2 e, M x D per head, bf16 hi then lo halves)
+// is kept in matrix-core fragment order: for feature tile pt, k-step s and lane
+// (h, col), the KPL elements of row 32 pt + col, columns s KS + h KPL onwards,
+// are contiguous, so one fragment load of a wave reads 64 KPL contiguous
+// elements (a row-major bank spreads it over 32 rows).
+// ---------------------------------------------------------------------------
+template <typename T, int D>
+LS_DEV size_t bank_frag(int pt, int s, int lane) {
+  using F = MF<T>;
+  return ((size_t)(pt * (D / F::KS) + s) * 64 + lane) * F::KPL;
+}
+
+// ---------------------------------------------------------------------------
 // Key log2-features of 32 tokens [tok0, tok0+32) against all M feature rows.
 // TOKEN_COLS: lanes <-> token, registers <-> feature p (acc[pt] rows p = 32pt+crow).
 // else      : lanes <-> feature p, registers <-> token.
@@ -29,10 +42,10 @@ LS_DEV void key_logits(f32x16 (&acc)[M / 32], float& nk, const T* __restrict__ k
     for (int e = 0; e < F::KPL; ++e) { float x = fel(kf, e); nk += x * x; }
 #pragma unroll
     for (int pt = 0; pt < M / 32; ++pt) {
-      typename F::frag of = F::ld(omk_h + (size_t)(pt * 32 + col) * D, k0);
+      typename F::frag of = *(const typename F::frag*)(omk_h + bank_frag<T, D>(pt, s, l));
       acc[pt] = TOKEN_COLS ? F::mma(of, kf, acc[pt]) : F::mma(kf, of, acc[pt]);
       if constexpr (sizeof(T) == 2) {
-        typename F::frag ol = F::ld(omk_h + (size_t)M * D + (size_t)(pt * 32 + col) * D, k0);
+        typename F::frag ol = *(const typename F::frag*)(omk_h + (size_t)M * D + bank_frag<T, D>(pt, s, l));
         acc[pt] = TOKEN_COLS ? F::mma(ol, kf, acc[pt]) : F::mma(kf, ol, acc[pt]);
       }
     }

@@ -25,7 +25,7 @@ struct Shape {
 // Workspace carve shared by forward and backward.
 struct Workspace {
   void* omq;        // [H][m][D] operand type: query-side Omega * log2(e)
-  void* omk;        // bf16: [H][2][m][D] hi/lo split of Omega*log2(e); f32: [H][m][D]
+  void* omk;        // bf16: [H][2][m*D] hi/lo split of Omega*log2(e); f32: [H][m*D]; fragment order
   void* omh;        // [H][m][D] f16 Omega*log2(e): the query-side logits of bf16 inputs
   float* states;    // [BH][nch][m*Dv + m]  chunk contributions, then boundary states (bf16 inputs: a only;
                    //                      the M slot holds the chunk's chi^T and V^T operand fragments)
